@@ -1,0 +1,198 @@
+"""CPU oracle for the spatially gated MobileNetV2 block (Verelst & Tuytelaars,
+"Dynamic Convolutions: Exploiting Spatial Sparsity for Faster Inference").
+
+TEST INFRASTRUCTURE ONLY.  The test suite, the smoke check and the
+CPU-baseline leg of the benchmark are the only callers.  The product path (the
+HIP library and its binding in ``paper_1912_03203_amd``) never imports this
+package, and this package imports nothing from it.
+
+The arithmetic lives in ``dynconv_oracle.c`` (plain loops, fp64 except the
+pinned fp32 mask unit); this module only marshals numpy arrays through ctypes.
+Layout here is the paper's NCHW (Sec. 3.2); flat positions are raster ordered,
+i = (n*H + h)*W + w.
+
+Readings of the paper that the oracle fixes (each listed with its reason in the
+design notes):
+  * hard mask G = [m > 0] (Eq. 8 with zero Gumbel noise); m == 0 or NaN -> 0;
+  * mask logits: fp32, fmaf chain over channels ascending from +0, bias last;
+  * dilation: (2r+1)^2 square, clipped per image (Sec. 3.2);
+  * residual activation r = identity for the MobileNetV2 block (linear
+    bottleneck, Sec. 3.2), so y = x + G o F(x), and y == x bit for bit where
+    G = 0;
+  * depthwise zero padding is applied to the expanded tensor itself.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "dynconv_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+ACT_NONE, ACT_RELU, ACT_RELU6 = 0, 1, 2
+
+_lib = None
+
+
+def build() -> str:
+    """Compile the oracle with gcc (no fast-math, no FP contraction)."""
+    tmp = _LIB + ".tmp%d" % os.getpid()
+    cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-ffp-contract=off",
+           "-fno-fast-math", "-Wall", "-Wextra", "-o", tmp, _SRC, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB):
+        build()
+    lib = ctypes.CDLL(_LIB)
+    P = ctypes.c_void_p
+    i32 = ctypes.c_int
+    lib.oracle_mask.argtypes = [P, i32, i32, i32, i32, P, ctypes.c_float, P, P]
+    lib.oracle_mask.restype = None
+    lib.oracle_dilate.argtypes = [P, i32, i32, i32, i32, P]
+    lib.oracle_dilate.restype = None
+    lib.oracle_indices.argtypes = [P, P, i32, i32, i32, P, P, P, P]
+    lib.oracle_indices.restype = None
+    blk = [P, i32, i32, i32, i32, i32, i32, P, P, P, P, P, P, i32, i32, i32]
+    lib.oracle_block_dense.argtypes = blk + [P, P, P, P]
+    lib.oracle_block_dense.restype = i32
+    lib.oracle_block_sparse.argtypes = blk + [P, ctypes.c_int32, P, ctypes.c_int32, P, P, P, P]
+    lib.oracle_block_sparse.restype = i32
+    _lib = lib
+    return lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _c(a, dtype):
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def mask(x_nchw, w_m, b_m):
+    """Mask unit + hard threshold (Eq. 2, Eq. 8 at zero noise).
+
+    x_nchw: fp32-representable values [N, C, H, W]; w_m: [C] fp32; b_m: fp32.
+    Returns (G uint8 [N*H*W], logits fp32 [N*H*W]).
+    """
+    lib = _load()
+    x = _c(x_nchw, np.float32)
+    N, C, H, W = x.shape
+    w = _c(w_m, np.float32)
+    assert w.shape == (C,)
+    G = np.zeros(N * H * W, np.uint8)
+    m = np.zeros(N * H * W, np.float32)
+    lib.oracle_mask(_ptr(x), N, C, H, W, _ptr(w), ctypes.c_float(float(np.float32(b_m))),
+                    _ptr(G), _ptr(m))
+    return G, m
+
+
+def dilate(G, N, H, W, r=1):
+    """Morphological dilation of the hard mask (Sec. 3.2), per image."""
+    lib = _load()
+    g = _c(G, np.uint8).reshape(-1)
+    assert g.size == N * H * W
+    out = np.zeros(N * H * W, np.uint8)
+    lib.oracle_dilate(_ptr(g), N, H, W, int(r), _ptr(out))
+    return out
+
+
+def indices(G, Gd, N, H, W):
+    """Raster-ordered index maps (Sec. 3.2): returns (A, D, nbr[P, 9])."""
+    lib = _load()
+    g = _c(G, np.uint8).reshape(-1)
+    gd = _c(Gd, np.uint8).reshape(-1)
+    total = N * H * W
+    A = np.zeros(max(total, 1), np.int32)
+    D = np.zeros(max(total, 1), np.int32)
+    nbr = np.zeros(max(total, 1) * 9, np.int32)
+    counts = np.zeros(2, np.int32)
+    lib.oracle_indices(_ptr(g), _ptr(gd), N, H, W, _ptr(A), _ptr(D), _ptr(nbr), _ptr(counts))
+    P, Pd = int(counts[0]), int(counts[1])
+    return A[:P].copy(), D[:Pd].copy(), nbr[: P * 9].reshape(P, 9).copy()
+
+
+def _weights(wts):
+    w1 = _c(wts["w1"], np.float64)
+    b1 = _c(wts["b1"], np.float64)
+    w2 = _c(wts["w2"], np.float64).reshape(-1, 9)
+    b2 = _c(wts["b2"], np.float64)
+    w3 = _c(wts["w3"], np.float64)
+    b3 = _c(wts["b3"], np.float64)
+    E, C = w1.shape
+    Co = w3.shape[0]
+    assert w2.shape == (E, 9) and w3.shape == (Co, E) and b1.shape == (E,)
+    assert b2.shape == (E,) and b3.shape == (Co,)
+    acts = wts.get("acts", (ACT_RELU6, ACT_RELU6, ACT_NONE))
+    return (w1, b1, w2, b2, w3, b3), (E, C, Co), acts
+
+
+def block_dense(x_nchw, wts, G=None, want_h2=False):
+    """Dense block with masked output, y = x + G o F(x) (Eq. 1, Eq. 3).
+
+    Returns (y [N, C, H, W] fp64, h2 [N, E, H, W] or None, macs).
+    """
+    lib = _load()
+    x = _c(x_nchw, np.float64)
+    N, C, H, W = x.shape
+    (w1, b1, w2, b2, w3, b3), (E, Cw, Co), acts = _weights(wts)
+    assert Cw == C
+    g = None if G is None else _c(G, np.uint8).reshape(-1)
+    y = np.empty_like(x)
+    h2 = np.empty((N, E, H, W), np.float64) if want_h2 else None
+    macs = np.zeros(1, np.int64)
+    rc = lib.oracle_block_dense(_ptr(x), N, C, H, W, E, Co, _ptr(w1), _ptr(b1), _ptr(w2),
+                                _ptr(b2), _ptr(w3), _ptr(b3), acts[0], acts[1], acts[2],
+                                _ptr(g), _ptr(y), _ptr(h2), _ptr(macs))
+    if rc != 0:
+        raise ValueError("oracle_block_dense rejected its arguments (rc=%d)" % rc)
+    return y, h2, int(macs[0])
+
+
+def block_sparse(x_nchw, wts, A, D, nbr, want_h2=False):
+    """Gather / expand / modified depthwise / project / scatter loops (Sec. 3.2).
+
+    Returns (y [N, C, H, W] fp64, h2 [P, E] or None, macs).
+    """
+    lib = _load()
+    x = _c(x_nchw, np.float64)
+    N, C, H, W = x.shape
+    (w1, b1, w2, b2, w3, b3), (E, Cw, Co), acts = _weights(wts)
+    assert Cw == C
+    a = _c(A, np.int32).reshape(-1)
+    d = _c(D, np.int32).reshape(-1)
+    nb = _c(nbr, np.int32).reshape(-1)
+    assert nb.size == 9 * a.size
+    y = np.empty_like(x)
+    h2 = np.empty((a.size, E), np.float64) if want_h2 else None
+    macs = np.zeros(1, np.int64)
+    rc = lib.oracle_block_sparse(_ptr(x), N, C, H, W, E, Co, _ptr(w1), _ptr(b1), _ptr(w2),
+                                 _ptr(b2), _ptr(w3), _ptr(b3), acts[0], acts[1], acts[2],
+                                 _ptr(a), a.size, _ptr(d), d.size, _ptr(nb), _ptr(y), _ptr(h2),
+                                 _ptr(macs))
+    if rc != 0:
+        raise ValueError("oracle_block_sparse rejected its arguments (rc=%d)" % rc)
+    return y, h2, int(macs[0])
+
+
+def block_forward(x_nchw, wts, w_m, b_m, dilate_r=1):
+    """One gated block end to end: mask, dilation, index maps, dense block
+    with masked output.  Returns dict with G, Gd, A, D, nbr, logits, y."""
+    x = np.asarray(x_nchw)
+    N, C, H, W = x.shape
+    G, logits = mask(x.astype(np.float32), w_m, b_m)
+    Gd = dilate(G, N, H, W, dilate_r)
+    A, D, nbr = indices(G, Gd, N, H, W)
+    y, _, _ = block_dense(x, wts, G)
+    return {"G": G, "Gd": Gd, "A": A, "D": D, "nbr": nbr, "logits": logits, "y": y}

@@ -1,0 +1,298 @@
+/*
+ * dynconv_oracle.c -- plain CPU oracle for the spatially gated MobileNetV2
+ * inverted-residual block of Verelst & Tuytelaars, "Dynamic Convolutions:
+ * Exploiting Spatial Sparsity for Faster Inference" (CVPR 2020).
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the checker, not the product: only
+ * the test suite, the smoke check and the CPU-baseline leg of the benchmark
+ * may load it.  It shares no code, header, table or helper with the HIP
+ * library under paper_1912_03203_amd/csrc, and it includes nothing of it.
+ *
+ * Everything is a plain loop in the paper's notation.  Tensors are NCHW
+ * (I of dimension N x C x H x W, Sec. 3.2), flattened spatial positions are
+ * raster ordered: i = (n*H + h)*W + w.  Floating point is double precision,
+ * except the mask unit, whose fp32 arithmetic is pinned so that hard masks
+ * can be compared bit for bit:
+ *   acc = +0.0f; for c ascending: acc = fmaf(w_m[c], x[c], acc);
+ *   m = acc + b_m;  G = (m > 0)
+ * Build with -ffp-contract=off and without -ffast-math so the compiler keeps
+ * exactly these roundings (fmaf is the correctly rounded libm routine).
+ *
+ * Work counters: every multiply-accumulate the loops evaluate increments a
+ * counter, including the taps that read the zero padding of the depthwise
+ * convolution, so the counts can be compared with Eq. 9 and Eq. 10.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ACT_NONE 0
+#define ACT_RELU 1
+#define ACT_RELU6 2
+
+enum { ORACLE_OK = 0, ORACLE_ERR_ARG = 1, ORACLE_ERR_NOMEM = 2 };
+
+static double act(double v, int kind)
+{
+    if (kind == ACT_RELU || kind == ACT_RELU6) {
+        if (v < 0.0) v = 0.0;
+        if (kind == ACT_RELU6 && v > 6.0) v = 6.0;
+    }
+    return v;
+}
+
+static size_t nchw(int n, int c, int h, int w, int C, int H, int W)
+{
+    return (((size_t)n * C + c) * H + h) * W + w;
+}
+
+/*
+ * Mask unit M (Sec. 3.1.1, Eq. 2): a 1x1 convolution C -> 1 gives the soft
+ * decision m for every position; the hard decision of the straight-through
+ * forward pass (Sec. 3.1.2, Eq. 8) with the Gumbel noise fixed to zero at
+ * inference reduces to G = [m > 0].  Ties (m == 0) and NaN give 0.
+ * x: NCHW fp32.  G, logits: [N*H*W] raster order; logits may be NULL.
+ */
+void oracle_mask(const float *x, int N, int C, int H, int W,
+                 const float *w_m, float b_m, uint8_t *G, float *logits)
+{
+    for (int n = 0; n < N; ++n)
+        for (int h = 0; h < H; ++h)
+            for (int w = 0; w < W; ++w) {
+                float acc = 0.0f;
+                for (int c = 0; c < C; ++c)
+                    acc = fmaf(w_m[c], x[nchw(n, c, h, w, C, H, W)], acc);
+                float m = acc + b_m;
+                size_t i = ((size_t)n * H + h) * W + w;
+                if (logits) logits[i] = m;
+                G[i] = (m > 0.0f) ? 1 : 0;
+            }
+}
+
+/*
+ * Mask dilation (Sec. 3.2, "Mask dilation"): G_dilated is the morphological
+ * dilation of G with a (2r+1) x (2r+1) square, clipped to each image (it
+ * never reaches into the next image of the batch).
+ */
+void oracle_dilate(const uint8_t *G, int N, int H, int W, int r, uint8_t *Gd)
+{
+    for (int n = 0; n < N; ++n)
+        for (int h = 0; h < H; ++h)
+            for (int w = 0; w < W; ++w) {
+                uint8_t v = 0;
+                for (int dh = -r; dh <= r; ++dh)
+                    for (int dw = -r; dw <= r; ++dw) {
+                        int hh = h + dh, ww = w + dw;
+                        if (hh < 0 || hh >= H || ww < 0 || ww >= W) continue;
+                        if (G[((size_t)n * H + hh) * W + ww]) v = 1;
+                    }
+                Gd[((size_t)n * H + h) * W + w] = v;
+            }
+}
+
+static int32_t find_sorted(const int32_t *list, int32_t len, int32_t key)
+{
+    int32_t lo = 0, hi = len - 1;
+    while (lo <= hi) {
+        int32_t mid = lo + (hi - lo) / 2;
+        if (list[mid] == key) return mid;
+        if (list[mid] < key) lo = mid + 1; else hi = mid - 1;
+    }
+    return -1;
+}
+
+/*
+ * Index maps (Sec. 3.2, "Masked gather operation" and "Modified 3x3
+ * depthwise convolution"): the p-th active position of the flattened mask
+ * becomes row p of the intermediate tensor.
+ *   A   = ascending flat positions with G = 1            (length P = sum G, Eq. 11)
+ *   D   = ascending flat positions with G_dilated = 1    (length P_d)
+ *   nbr[p*9 + 3*(dh+1) + (dw+1)] = row of D holding position
+ *        (n, h+dh, w+dw) of A[p], or -1 when that position lies outside the
+ *        image or is not in D.
+ * counts[0] = P, counts[1] = P_d.  Arrays must hold N*H*W (nbr: 9*N*H*W).
+ */
+void oracle_indices(const uint8_t *G, const uint8_t *Gd, int N, int H, int W,
+                    int32_t *A, int32_t *D, int32_t *nbr, int32_t *counts)
+{
+    int32_t total = (int32_t)((size_t)N * H * W);
+    int32_t P = 0, Pd = 0;
+    for (int32_t i = 0; i < total; ++i) {
+        if (G[i]) A[P++] = i;
+        if (Gd[i]) D[Pd++] = i;
+    }
+    for (int32_t p = 0; p < P; ++p) {
+        int32_t i = A[p];
+        int n = i / (H * W), h = (i / W) % H, w = i % W;
+        for (int dh = -1; dh <= 1; ++dh)
+            for (int dw = -1; dw <= 1; ++dw) {
+                int k = 3 * (dh + 1) + (dw + 1);
+                int hh = h + dh, ww = w + dw;
+                int32_t j = -1;
+                if (hh >= 0 && hh < H && ww >= 0 && ww < W)
+                    j = find_sorted(D, Pd, (int32_t)(((size_t)n * H + hh) * W + ww));
+                nbr[(size_t)p * 9 + k] = j;
+            }
+    }
+    counts[0] = P;
+    counts[1] = Pd;
+}
+
+/*
+ * Dense residual block, masked output (Eq. 1 and Eq. 3, Sec. 3.1.1), for the
+ * MobileNetV2 inverted residual described in Sec. 3.2: pointwise expansion
+ * C -> E, depthwise 3x3 (zero padding, stride 1), linear pointwise
+ * projection E -> Co; batch norm arrives folded into weights and biases.
+ *   h1 = act1(W1 x + b1)
+ *   h2 = act2(DW3x3(h1) + b2)
+ *   F  = act3(W3 h2 + b3)
+ *   y  = x + G o F        (y = x exactly where G = 0; r = identity)
+ * G == NULL means the all-ones mask (the plain dense block of Eq. 1).
+ * Weights: w1[e*C + c], w2[e*9 + 3*(dh+1) + (dw+1)], w3[co*E + e].
+ * h2_out (optional): NCHW-like [N][E][H][W] depthwise output.
+ * macs (optional): multiply-accumulates evaluated.
+ * Returns ORACLE_ERR_ARG unless Co == C (the identity path needs it).
+ */
+int oracle_block_dense(const double *x, int N, int C, int H, int W, int E, int Co,
+                       const double *w1, const double *b1,
+                       const double *w2, const double *b2,
+                       const double *w3, const double *b3,
+                       int act1, int act2, int act3,
+                       const uint8_t *G, double *y, double *h2_out, int64_t *macs)
+{
+    if (Co != C || N < 0 || C <= 0 || H < 0 || W < 0 || E <= 0) return ORACLE_ERR_ARG;
+    size_t plane = (size_t)H * W;
+    double *h1 = (double *)malloc(sizeof(double) * (size_t)E * plane + 1);
+    double *h2 = (double *)malloc(sizeof(double) * (size_t)E * plane + 1);
+    if (!h1 || !h2) { free(h1); free(h2); return ORACLE_ERR_NOMEM; }
+    int64_t count = 0;
+    for (int n = 0; n < N; ++n) {
+        /* pointwise expansion on every position */
+        for (int e = 0; e < E; ++e)
+            for (int h = 0; h < H; ++h)
+                for (int w = 0; w < W; ++w) {
+                    double acc = 0.0;
+                    for (int c = 0; c < C; ++c) {
+                        acc += w1[(size_t)e * C + c] * x[nchw(n, c, h, w, C, H, W)];
+                        ++count;
+                    }
+                    h1[(size_t)e * plane + (size_t)h * W + w] = act(acc + b1[e], act1);
+                }
+        /* depthwise 3x3, zero padding of h1 */
+        for (int e = 0; e < E; ++e)
+            for (int h = 0; h < H; ++h)
+                for (int w = 0; w < W; ++w) {
+                    double acc = 0.0;
+                    for (int dh = -1; dh <= 1; ++dh)
+                        for (int dw = -1; dw <= 1; ++dw) {
+                            int hh = h + dh, ww = w + dw;
+                            double v = 0.0;
+                            if (hh >= 0 && hh < H && ww >= 0 && ww < W)
+                                v = h1[(size_t)e * plane + (size_t)hh * W + ww];
+                            acc += w2[(size_t)e * 9 + 3 * (dh + 1) + (dw + 1)] * v;
+                            ++count;
+                        }
+                    double v2 = act(acc + b2[e], act2);
+                    h2[(size_t)e * plane + (size_t)h * W + w] = v2;
+                    if (h2_out) h2_out[nchw(n, e, h, w, E, H, W)] = v2;
+                }
+        /* linear projection, then the residual sum on masked positions */
+        for (int co = 0; co < Co; ++co)
+            for (int h = 0; h < H; ++h)
+                for (int w = 0; w < W; ++w) {
+                    double acc = 0.0;
+                    for (int e = 0; e < E; ++e) {
+                        acc += w3[(size_t)co * E + e] * h2[(size_t)e * plane + (size_t)h * W + w];
+                        ++count;
+                    }
+                    double f = act(acc + b3[co], act3);
+                    size_t o = nchw(n, co, h, w, Co, H, W);
+                    int on = G ? G[((size_t)n * H + h) * W + w] != 0 : 1;
+                    y[o] = on ? x[o] + f : x[o];
+                }
+    }
+    free(h1);
+    free(h2);
+    if (macs) *macs = count;
+    return ORACLE_OK;
+}
+
+/*
+ * The same block executed the way Sec. 3.2 describes it, as plain loops over
+ * the index maps:
+ *   gather      T[j, c]  = x at position D[j]                  (j < P_d)
+ *   expand      H1[j, e] = act1(sum_c w1[e, c] T[j, c] + b1[e])
+ *   depthwise   H2[p, e] = act2(sum_k w2[e, k] H1[nbr[p, k], e] + b2[e]),
+ *               a missing neighbour (nbr = -1) contributing 0   (p < P)
+ *   project     F[p, co] = act3(sum_e w3[co, e] H2[p, e] + b3[co])
+ *   scatter     y = x; y at position A[p] += F[p]
+ * h2_out (optional): [P][E].  macs (optional): evaluated multiply-accumulates
+ * (Eq. 10 counts P_d*C*E + P*(9E + E*Co)).
+ */
+int oracle_block_sparse(const double *x, int N, int C, int H, int W, int E, int Co,
+                        const double *w1, const double *b1,
+                        const double *w2, const double *b2,
+                        const double *w3, const double *b3,
+                        int act1, int act2, int act3,
+                        const int32_t *A, int32_t P, const int32_t *D, int32_t Pd,
+                        const int32_t *nbr, double *y, double *h2_out, int64_t *macs)
+{
+    if (Co != C || N < 0 || C <= 0 || H < 0 || W < 0 || E <= 0 || P < 0 || Pd < 0)
+        return ORACLE_ERR_ARG;
+    size_t plane = (size_t)H * W;
+    double *T = (double *)malloc(sizeof(double) * (size_t)Pd * C + 1);
+    double *H1 = (double *)malloc(sizeof(double) * (size_t)Pd * E + 1);
+    double *H2 = (double *)malloc(sizeof(double) * (size_t)E + 1);
+    if (!T || !H1 || !H2) { free(T); free(H1); free(H2); return ORACLE_ERR_NOMEM; }
+    int64_t count = 0;
+
+    for (int32_t j = 0; j < Pd; ++j) {
+        int32_t i = D[j];
+        int n = (int)(i / (int32_t)plane);
+        int hw = (int)(i % (int32_t)plane);
+        for (int c = 0; c < C; ++c)
+            T[(size_t)j * C + c] = x[((size_t)n * C + c) * plane + hw];
+    }
+    for (int32_t j = 0; j < Pd; ++j)
+        for (int e = 0; e < E; ++e) {
+            double acc = 0.0;
+            for (int c = 0; c < C; ++c) {
+                acc += w1[(size_t)e * C + c] * T[(size_t)j * C + c];
+                ++count;
+            }
+            H1[(size_t)j * E + e] = act(acc + b1[e], act1);
+        }
+
+    memcpy(y, x, sizeof(double) * (size_t)N * C * plane);
+    for (int32_t p = 0; p < P; ++p) {
+        for (int e = 0; e < E; ++e) {
+            double acc = 0.0;
+            for (int k = 0; k < 9; ++k) {
+                int32_t j = nbr[(size_t)p * 9 + k];
+                double v = (j >= 0) ? H1[(size_t)j * E + e] : 0.0;
+                acc += w2[(size_t)e * 9 + k] * v;
+                ++count;
+            }
+            H2[e] = act(acc + b2[e], act2);
+            if (h2_out) h2_out[(size_t)p * E + e] = H2[e];
+        }
+        int32_t i = A[p];
+        int n = (int)(i / (int32_t)plane);
+        int hw = (int)(i % (int32_t)plane);
+        for (int co = 0; co < Co; ++co) {
+            double acc = 0.0;
+            for (int e = 0; e < E; ++e) {
+                acc += w3[(size_t)co * E + e] * H2[e];
+                ++count;
+            }
+            size_t o = ((size_t)n * Co + co) * plane + hw;
+            y[o] = x[o] + act(acc + b3[co], act3);
+        }
+    }
+    free(T);
+    free(H1);
+    free(H2);
+    if (macs) *macs = count;
+    return ORACLE_OK;
+}

@@ -1,0 +1,148 @@
+"""Pins for the oracle's mask unit (Eq. 2) and hard threshold (Eq. 8 at zero
+Gumbel noise).
+
+The oracle's logits are an fp32 fmaf chain over channels ascending from +0,
+with the bias added last.  These tests check that against an independent
+computation in exact rational arithmetic with one correct fp32 rounding per
+step, against special cases that need no chain at all, and against the
+density closed form of the percentile bias.
+"""
+import math
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from paper_1912_03203_amd import inputs
+
+FLT_MAX = Fraction(2) ** 127 * (2 - Fraction(1, 2 ** 23))
+
+
+def fp32_rne(q: Fraction) -> float:
+    """Round an exact rational to the nearest fp32 value, ties to even,
+    with gradual underflow."""
+    if q == 0:
+        return 0.0
+    neg = q < 0
+    q = -q if neg else q
+    # exponent e with 2**e <= q < 2**(e+1)
+    e = q.numerator.bit_length() - q.denominator.bit_length()
+    if Fraction(2) ** e > q:
+        e -= 1
+    elif Fraction(2) ** (e + 1) <= q:
+        e += 1
+    e = max(e, -126)
+    quantum = Fraction(2) ** (e - 23)
+    m = q / quantum
+    fl = m.numerator // m.denominator
+    rem = m - fl
+    if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and fl % 2 == 1):
+        fl += 1
+    v = fl * quantum
+    if v > FLT_MAX:
+        return -math.inf if neg else math.inf
+    out = float(v)
+    return -out if neg else out
+
+
+def chain_exact(w, x, b):
+    acc = 0.0
+    for wc, xc in zip(w, x):
+        acc = fp32_rne(Fraction(float(wc)) * Fraction(float(xc)) + Fraction(acc))
+    return fp32_rne(Fraction(acc) + Fraction(float(b)))
+
+
+def _nchw(x_nhwc):
+    return np.ascontiguousarray(np.transpose(x_nhwc, (0, 3, 1, 2)))
+
+
+@pytest.mark.parametrize("C", [1, 3, 8, 24])
+def test_logits_match_exact_fmaf_chain(orc, C):
+    rng = np.random.default_rng(100 + C)
+    N, H, W = 2, 4, 5
+    # wide dynamic range so that single and double rounding differ somewhere
+    x = (rng.standard_normal((N, C, H, W)) * np.exp2(rng.integers(-20, 20, (N, C, H, W))))
+    x = x.astype(np.float32)
+    w = (rng.standard_normal(C) * np.exp2(rng.integers(-10, 10, C))).astype(np.float32)
+    b = np.float32(rng.standard_normal() * 1e-3)
+    G, m = orc.mask(x, w, b)
+    for n in range(N):
+        for h in range(H):
+            for ww in range(W):
+                i = (n * H + h) * W + ww
+                want = chain_exact(w, x[n, :, h, ww], b)
+                assert m[i] == np.float32(want), (n, h, ww)
+                assert G[i] == (1 if want > 0 else 0)
+
+
+def test_chain_pin_has_power(orc):
+    """Negative control: separately rounded product and sum (no fused
+    multiply-add) differs from the oracle on these inputs, so the pin above
+    would catch a non-fused or reordered chain."""
+    rng = np.random.default_rng(7)
+    N, C, H, W = 1, 24, 8, 8
+    x = (rng.standard_normal((N, C, H, W)) * np.exp2(rng.integers(-12, 12, (N, C, H, W))))
+    x = x.astype(np.float32)
+    w = rng.standard_normal(C).astype(np.float32)
+    _, m = orc.mask(x, w, 0.0)
+    unfused = np.zeros(H * W, np.float32)
+    reverse = np.zeros(H * W, np.float32)
+    flat = x.reshape(C, H * W)
+    for c in range(C):
+        unfused = (unfused + (w[c] * flat[c]).astype(np.float32)).astype(np.float32)
+    for c in reversed(range(C)):
+        reverse = np.array([fp32_rne(Fraction(float(w[c])) * Fraction(float(v)) + Fraction(float(a)))
+                            for v, a in zip(flat[c], reverse)], np.float32)
+    assert np.any(unfused != m)
+    assert np.any(reverse != m)
+
+
+def test_single_channel_is_one_rounded_product(orc):
+    """C = 1: the chain is fmaf(w, x, +0) = round32(w*x) (w*x is exact in
+    fp64), then + b in fp32."""
+    rng = np.random.default_rng(3)
+    x = rng.standard_normal((3, 1, 6, 7)).astype(np.float32)
+    w = np.array([rng.standard_normal()], np.float32)
+    b = np.float32(0.125)
+    G, m = orc.mask(x, w, b)
+    prod = np.float32(np.float64(w[0]) * x.astype(np.float64).reshape(-1))
+    want = (prod + b).astype(np.float32)
+    np.testing.assert_array_equal(m, want)
+    np.testing.assert_array_equal(G, (want > 0).astype(np.uint8))
+
+
+def test_integer_inputs_give_exact_sums(orc):
+    """Small integers: every partial sum is exact in fp32, so the logits are
+    the integer dot product plus the bias, whatever the order."""
+    rng = np.random.default_rng(4)
+    N, C, H, W = 2, 16, 5, 5
+    x = rng.integers(-50, 50, (N, C, H, W)).astype(np.float32)
+    w = rng.integers(-20, 20, C).astype(np.float32)
+    b = np.float32(-3.0)
+    G, m = orc.mask(x, w, b)
+    dot = np.einsum("c,nchw->nhw", w.astype(np.int64), x.astype(np.int64)).reshape(-1)
+    np.testing.assert_array_equal(m, (dot - 3).astype(np.float32))
+    np.testing.assert_array_equal(G, (dot - 3 > 0).astype(np.uint8))
+
+
+def test_threshold_is_strict_and_nan_is_inactive(orc):
+    x = np.array([1.0, 2.0, -1.0, np.nan], np.float32).reshape(1, 1, 1, 4)
+    w = np.array([1.0], np.float32)
+    G, m = orc.mask(x, w, -1.0)  # logits 0, 1, -2, nan
+    assert list(G) == [0, 1, 0, 0]
+    assert m[0] == 0.0 and m[1] == 1.0 and m[2] == -2.0 and np.isnan(m[3])
+
+
+@pytest.mark.parametrize("density", [0.0, 0.1, 0.25, 0.5, 0.75, 0.9, 1.0])
+def test_percentile_bias_gives_exact_density(orc, density):
+    """Closed form of the workload recipe: with distinct logits, the bias
+    -s_(k) leaves exactly round(d * NHW) positions with s + b > 0."""
+    rng = np.random.default_rng(11)
+    x = inputs.blob_features(rng, 3, 16, 20, 24)
+    w = rng.normal(0, 0.1, 24).astype(np.float32)
+    xc = _nchw(x)
+    _, s = orc.mask(xc, w, 0.0)
+    assert np.unique(s).size == s.size
+    b = inputs.percentile_bias(s, density)
+    G, _ = orc.mask(xc, w, b)
+    assert int(G.sum()) == inputs.density_count(density, s.size)
