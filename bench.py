@@ -1,0 +1,369 @@
+"""Benchmark: images/sec of the sparse MobileNetV2 block stack at mask density
+0.25, and its speedup over the same kernels run densely, on one MI355X.
+
+Default workload: 8 stacked stride-1 gated inverted-residual blocks at
+32 x 64x64x32 (hidden 192), fp16 storage, synthetic ellipse ("person")
+features, every block's mask bias set so that 25% of the positions are active.
+
+A step is one pass of the whole hot path over the batch: restore the input
+(one device copy, 8 MiB, inside the timed step), then for each block the mask
+unit, the index maps, gather + expansion, depthwise + projection + scatter-add.
+Steps run from a captured HIP graph (--no-graph: eager).  W warm-up steps, then
+exactly K timed steps between two device synchronisations.
+
+Also reported on the same JSON line:
+  dense         the same stack with every block dense (no mask, no lists)
+  kernels       per-kernel average duration from the start/end events the HIP
+                runtime stamps on each launch (eager, separate pass)
+  roofline      the dominant kernel's algorithmic bytes per launch / its
+                average duration, against the 8 TB/s HBM peak
+  cpu_baseline  the CPU oracle (gather/scatter form, fp64, one thread) on a
+                bounded sample of the same workload
+  sweep         per-block latency of the 32 x 56x56x24 (hidden 144) fp16 block
+                at densities 0.1 .. 0.9, sparse and dense
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "images/sec of sparse MobileNetV2 block stack at mask density 0.25; speedup vs dense"
+HBM_PEAK_GBS = 8000.0
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+# ------------------------------------------------------------------ HIP events
+class HipEvents:
+    """Timing events whose raw hipEvent_t handles the library records on its own
+    stream.  They are torch events (so the runtime already loaded in the
+    process creates them), each recorded once up front so the handle exists."""
+
+    def __init__(self, torch, n):
+        self.torch = torch
+        self.events = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
+        for e in self.events:
+            e.record()
+        torch.cuda.synchronize()
+        self.ev = [e.cuda_event for e in self.events]
+
+    def elapsed_ms(self, i, j):
+        self.events[j].synchronize()
+        return self.events[i].elapsed_time(self.events[j])
+
+    def close(self):
+        self.events = []
+        self.ev = []
+
+
+# ------------------------------------------------------------------ setup
+def calibrate(dc, inputs, torch, x0_dev, blocks_np, dt, density):
+    """Per-block mask bias for the target density, from the library's own
+    bias-free logits of each block's input (offline, before timing)."""
+    n, h, w, c = x0_dev.shape
+    npos = n * h * w
+    shape = dc.shape_of(x0_dev)
+    x = x0_dev.clone()
+    logits = torch.empty(npos, dtype=torch.float32, device=x.device)
+    idx = dc.IndexBuffers.alloc(npos, device=x.device)
+    ws_i = torch.empty(dc.indices_workspace_bytes(shape), dtype=torch.uint8, device=x.device)
+    out = []
+    for wts in blocks_np:
+        blk = dc.BlockWeights.from_arrays(wts, dt, device=x.device)
+        dc.mask(x, blk.w_mask, 0.0, logits=logits)
+        torch.cuda.synchronize()
+        blk.b_mask = float(inputs.percentile_bias(logits.cpu().numpy(), density))
+        m = dc.mask(x, blk.w_mask, blk.b_mask)
+        dc.build_indices(m, shape, 1, idx, ws_i)
+        ws = torch.empty(dc.block_workspace_bytes(shape, blk, dt), dtype=torch.uint8, device=x.device)
+        dc.block_forward(x, x, blk, idx, ws)
+        out.append(blk)
+    torch.cuda.synchronize()
+    return out
+
+
+class Runner:
+    """One timed step (restore input + stack call), eager or graph-replayed."""
+
+    def __init__(self, dc, torch, x0, blocks, dense, use_graph, n_blocks):
+        self.torch = torch
+        self.x0 = x0
+        self.x = x0.clone()
+        npos = x0.shape[0] * x0.shape[1] * x0.shape[2]
+        self.masks = None if dense else torch.zeros(n_blocks, npos, dtype=torch.uint8, device=x0.device)
+        self.counts = None if dense else torch.zeros(n_blocks, 2, dtype=torch.int32, device=x0.device)
+        self.stack = dc.Stack(self.x, blocks, dense, masks=self.masks, counts=self.counts)
+        self.graph = None
+        if use_graph:
+            self.graph = self._capture()
+
+    def eager(self):
+        self.x.copy_(self.x0)
+        self.stack()
+
+    def _capture(self):
+        torch = self.torch
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            self.eager()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            self.eager()
+        torch.cuda.synchronize()
+        return g
+
+    def step(self):
+        if self.graph is not None:
+            self.graph.replay()
+        else:
+            self.eager()
+
+    def timed(self, steps, warmup):
+        torch = self.torch
+        for _ in range(warmup):
+            self.step()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            self.step()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) / steps
+
+
+def profile_kernels(dc, torch, runner, names, steps):
+    """Average duration per kernel name from start/end events that the HIP
+    runtime stamps on every launch of the library (profiled stack call)."""
+    ev = HipEvents(torch, 2 * len(names))
+    per_launch = np.zeros(len(names))
+    try:
+        for _ in range(steps):
+            runner.x.copy_(runner.x0)
+            runner.stack.profiled(ev.ev)
+            torch.cuda.synchronize()
+            per_launch += [ev.elapsed_ms(2 * i, 2 * i + 1) for i in range(len(names))]
+    finally:
+        ev.close()
+    per_launch /= steps
+    out = {}
+    for name, t in zip(names, per_launch):
+        d = out.setdefault(name, [0.0, 0])
+        d[0] += t
+        d[1] += 1
+    return {k: {"avg_us": 1000.0 * v[0] / v[1], "launches": v[1], "total_us": 1000.0 * v[0]}
+            for k, v in out.items()}, per_launch
+
+
+def algorithmic_bytes(name, dense, s, C, E, npos, rows, P, Pd):
+    """Bytes one launch must move at minimum (each input read once, each output
+    written once); P, Pd are the block's active and dilated counts."""
+    if dense:
+        if name == "k_expand":
+            return npos * C * s + npos * E * s + E * C * s + 4 * E
+        if name == "k_dw_project":
+            return npos * E * s + 2 * npos * C * s + 9 * E * s + E * C * s + 4 * (E + C)
+    table = {
+        "k_mask": npos * C * s + npos + 4 * C,
+        "k_rowcount": npos + 8 * rows,
+        "k_rowscan": 8 * rows + 8 * (rows + 1) + 8,
+        "k_compact": npos + 8 * rows + 4 * P + 4 * Pd + 36 * P,
+        "k_expand": 4 * Pd + Pd * C * s + Pd * E * s + E * C * s + 4 * E,
+        "k_dw_project": 40 * P + Pd * E * s + 2 * P * C * s + 9 * E * s + E * C * s + 4 * (E + C),
+    }
+    return table[name]
+
+
+def cpu_baseline(inputs, wl, x0_np, blocks_np, density, budget_s=12.0):
+    """The oracle (mask, dilation, index maps, gather/scatter block; fp64; one
+    thread) on the first S images of the batch, biases calibrated on that
+    sample.  S is sized so the timed run takes about budget_s seconds."""
+    import oracle
+
+    def run(x_nhwc, biases=None, timed=False):
+        x = np.ascontiguousarray(x_nhwc.transpose(0, 3, 1, 2)).astype(np.float64)
+        N, C, H, W = x.shape
+        cal = []
+        t = 0.0
+        for b, wts in enumerate(blocks_np):
+            if biases is None:
+                _, s = oracle.mask(x.astype(np.float32), wts["w_m"], 0.0)
+                bias = inputs.percentile_bias(s, density)
+            else:
+                bias = biases[b]
+            cal.append(bias)
+            t0 = time.perf_counter()
+            G, _ = oracle.mask(x.astype(np.float32), wts["w_m"], bias)
+            Gd = oracle.dilate(G, N, H, W, 1)
+            A, D, nbr = oracle.indices(G, Gd, N, H, W)
+            y, _, _ = oracle.block_sparse(x, wts, A, D, nbr)
+            t += time.perf_counter() - t0
+            y_nhwc = inputs.round_to_storage(y.transpose(0, 2, 3, 1), wl.dtype)
+            x = np.ascontiguousarray(y_nhwc.transpose(0, 3, 1, 2)).astype(np.float64)
+        return cal, t
+
+    cal1, _ = run(x0_np[:1])
+    _, t1 = run(x0_np[:1], cal1)
+    S = int(max(1, min(wl.n, round(budget_s / max(t1, 1e-3)))))
+    sample = x0_np[:S]
+    cal, _ = run(sample)
+    _, t = run(sample, cal)
+    return {"value": S / t, "unit": "images/s", "cores": 1, "kind": "oracle",
+            "sample": "%d of %d images through all %d blocks (mask, dilation, index maps, "
+                      "gather/scatter block; fp64 C loops, one thread); %.1f s" % (S, wl.n, len(blocks_np), t)}
+
+
+def density_sweep(dc, inputs, torch, steps, warmup, use_graph):
+    wl = inputs.WORKLOADS["mbv2_stage2_block_56x56x24_f16"]
+    x_np, blocks_np, _ = inputs.make_block_inputs(wl, 0)
+    dt = dc.NAME_TO_DTYPE[wl.dtype]
+    x0 = torch.from_numpy(x_np).cuda().to(dt)
+    dense_blk = [dc.BlockWeights.from_arrays(blocks_np[0], dt)]
+    dense_t = Runner(dc, torch, x0, dense_blk, True, use_graph, 1).timed(steps, warmup)
+    rows = []
+    for d in wl.densities:
+        blks = calibrate(dc, inputs, torch, x0, blocks_np, dt, d)
+        r = Runner(dc, torch, x0, blks, False, use_graph, 1)
+        t = r.timed(steps, warmup)
+        P, Pd = (int(v) for v in r.counts[0].cpu())
+        rows.append({"density": d, "active_frac": P / wl.nhw, "dilated_frac": Pd / wl.nhw,
+                     "sparse_us": 1e6 * t, "dense_us": 1e6 * dense_t, "speedup": dense_t / t,
+                     "sparse_images_per_s": wl.n / t})
+    return {"workload": wl.name, "rows": rows}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="pose_stack8_64x64x32_f16")
+    ap.add_argument("--density", type=float, default=0.25)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-graph", action="store_true")
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--profile-steps", type=int, default=20)
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print("bench.py measures one GPU: the gated-block path runs on a single MI355X "
+              "(batch sharding across GPUs needs no exchange and is not launched here); "
+              "use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_1912_03203_amd import dynconv as dc
+    from paper_1912_03203_amd import inputs
+
+    if not torch.cuda.is_available():
+        print("no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    dc.load()
+    wl = inputs.WORKLOADS[args.workload]
+    dt = dc.NAME_TO_DTYPE[wl.dtype]
+    use_graph = not args.no_graph
+    log("workload %s density %.2f steps %d warmup %d graph %s" % (wl.name, args.density, args.steps,
+                                                                 args.warmup, use_graph))
+    x_np, blocks_np, _ = inputs.make_block_inputs(wl, args.seed)
+    x0 = torch.from_numpy(x_np).cuda().to(dt)
+    sparse_blocks = calibrate(dc, inputs, torch, x0, blocks_np, dt, args.density)
+    dense_blocks = [dc.BlockWeights.from_arrays(w, dt) for w in blocks_np]
+
+    sp = Runner(dc, torch, x0, sparse_blocks, False, use_graph, wl.blocks)
+    dn = Runner(dc, torch, x0, dense_blocks, True, use_graph, wl.blocks)
+    if use_graph:  # replays must reproduce the eager step bit for bit
+        for r in (sp, dn):
+            r.eager()
+            torch.cuda.synchronize()
+            ref = r.x.clone()
+            for _ in range(3):
+                r.step()
+                torch.cuda.synchronize()
+                if not torch.equal(r.x, ref):
+                    raise RuntimeError("graph replay differs from the eager step")
+    log("timing sparse")
+    t_sp = sp.timed(args.steps, args.warmup)
+    log("timing dense")
+    t_dn = dn.timed(args.steps, args.warmup)
+    counts = sp.counts.cpu().numpy()
+    npos = wl.nhw
+    active = (counts[:, 0] / npos).tolist()
+    dilated = (counts[:, 1] / npos).tolist()
+    log("sparse %.1f us/step, dense %.1f us/step, speedup %.2fx" % (1e6 * t_sp, 1e6 * t_dn, t_dn / t_sp))
+
+    # per-kernel profile (events on the library's stream)
+    names_sp = dc.stack_launch_names(wl.blocks, False)
+    names_dn = dc.stack_launch_names(wl.blocks, True)
+    prof_sp, per_sp = profile_kernels(dc, torch, sp, names_sp, args.profile_steps)
+    prof_dn, _ = profile_kernels(dc, torch, dn, names_dn, args.profile_steps)
+    s = 2 if wl.dtype != "f32" else 4
+    rows = wl.n * wl.h
+    dom = max(prof_sp, key=lambda k: prof_sp[k]["total_us"])
+    # algorithmic bytes of the dominant kernel, averaged over its launches
+    per_block = [algorithmic_bytes(dom, False, s, wl.c, wl.e, npos, rows, int(P), int(Pd))
+                 for P, Pd in counts]
+    bytes_per_launch = float(np.mean(per_block))
+    achieved = bytes_per_launch / (prof_sp[dom]["avg_us"] * 1e-6) / 1e9
+    for k, v in prof_sp.items():
+        b = np.mean([algorithmic_bytes(k, False, s, wl.c, wl.e, npos, rows, int(P), int(Pd))
+                     for P, Pd in counts])
+        v["algorithmic_bytes"] = float(b)
+        v["gbs"] = float(b / (v["avg_us"] * 1e-6) / 1e9)
+    for k, v in prof_dn.items():
+        b = algorithmic_bytes(k, True, s, wl.c, wl.e, npos, rows, npos, npos)
+        v["algorithmic_bytes"] = float(b)
+        v["gbs"] = float(b / (v["avg_us"] * 1e-6) / 1e9)
+    kernel_sum_us = float(sum(v["total_us"] for v in prof_sp.values()))
+
+    result = {
+        "metric": METRIC,
+        "value": wl.n / t_sp,
+        "unit": "images/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": 1e3 * t_sp,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic",
+        "config": {"workload": wl.name, "batch": wl.n, "h": wl.h, "w": wl.w, "c": wl.c,
+                   "hidden": wl.e, "blocks": wl.blocks, "density": args.density,
+                   "graph": use_graph, "seed": args.seed},
+        "speedup_vs_dense": t_dn / t_sp,
+        "dense": {"value": wl.n / t_dn, "ms_per_step": 1e3 * t_dn},
+        "per_block_us": {"sparse": 1e6 * t_sp / wl.blocks, "dense": 1e6 * t_dn / wl.blocks},
+        "active_frac": active,
+        "dilated_frac": dilated,
+        "kernels": {"sparse": prof_sp, "dense": prof_dn, "sparse_kernel_sum_us": kernel_sum_us},
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "algorithmic_bytes_per_launch": bytes_per_launch},
+    }
+    if not args.no_sweep:
+        log("density sweep")
+        result["sweep"] = density_sweep(dc, inputs, torch, min(args.steps, 100), min(args.warmup, 10),
+                                        use_graph)
+    if not args.no_cpu:
+        log("cpu baseline (oracle)")
+        result["cpu_baseline"] = cpu_baseline(inputs, wl, x_np, blocks_np, args.density)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

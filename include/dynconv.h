@@ -1,0 +1,237 @@
+/*
+ * dynconv.h -- C ABI of the MI355X (gfx950) library for spatially gated
+ * MobileNetV2 inverted-residual blocks: the inference path of Verelst &
+ * Tuytelaars, "Dynamic Convolutions: Exploiting Spatial Sparsity for Faster
+ * Inference" (CVPR 2020), Sec. 3.1.1 (block and mask unit), Sec. 3.1.2 (hard
+ * decision) and Sec. 3.2 (gather / modified depthwise / scatter execution).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * * Feature maps are NHWC, dense, channel fastest: element (n, h, w, c) sits
+ *   at ((n*H + h)*W + w)*C + c.  Flat positions are raster ordered,
+ *   i = (n*H + h)*W + w, image-major; the paper's "p-th active position of the
+ *   flattened mask" uses this order (Sec. 3.2, masked gather).
+ * * Pointers marked (device) must be device memory of the current HIP device;
+ *   (host) pointers are read during the call only.  The library allocates and
+ *   frees nothing: every buffer, including the workspace, belongs to the
+ *   caller.  It keeps no global state, so calls on different streams may run
+ *   concurrently as long as their buffers are disjoint.
+ * * Every call validates all of its arguments on the host first.  On any
+ *   error it returns a nonzero status and enqueues nothing.  Otherwise the
+ *   work is enqueued asynchronously on `stream` (a hipStream_t; NULL is the
+ *   null stream) and DYNCONV_OK is returned; a failed kernel launch is
+ *   reported as DYNCONV_ERR_HIP (the call clears HIP's last-error state
+ *   before launching).  Nothing synchronises with the host, nothing is
+ *   printed, no exception leaves the library.  No call enqueues a memset or
+ *   a host synchronisation, so the calls may be captured into a HIP graph.
+ * * Sizes that the mask decides (the active count P and the dilated count
+ *   P_d) stay on the device; kernels are sized for the capacity N*H*W and
+ *   read the counts there.
+ * * Data types: fp32, fp16 and bf16 storage.  Arithmetic is fp32 (fp32
+ *   accumulation in the matrix-core products); the expanded and depthwise
+ *   intermediates are rounded to the storage type.
+ * * Supported channel counts: c_in == c_out (the identity path of Eq. 3),
+ *   8 <= c_in <= 256 with c_in % 8 == 0, 16 <= c_hidden <= 1536 with
+ *   c_hidden % 16 == 0.  Other valid shapes return DYNCONV_ERR_UNSUPPORTED.
+ *   N*H*W must stay below 2^31 / 9.  Data pointers must be 16-byte aligned.
+ */
+#ifndef DYNCONV_H_
+#define DYNCONV_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    DYNCONV_F32 = 0,
+    DYNCONV_F16 = 1,
+    DYNCONV_BF16 = 2
+} dynconv_dtype;
+
+typedef enum {
+    DYNCONV_OK = 0,
+    DYNCONV_ERR_NULL = 1,        /* a required pointer is NULL */
+    DYNCONV_ERR_SHAPE = 2,       /* non-positive / overflowing sizes, overlapping buffers */
+    DYNCONV_ERR_DTYPE = 3,       /* unknown dtype */
+    DYNCONV_ERR_UNSUPPORTED = 4, /* well-formed but outside what the kernels implement */
+    DYNCONV_ERR_CAPACITY = 5,    /* index buffers hold fewer than N*H*W entries */
+    DYNCONV_ERR_ALIGN = 6,       /* a data pointer is not 16-byte aligned */
+    DYNCONV_ERR_WORKSPACE = 7,   /* workspace NULL or smaller than required */
+    DYNCONV_ERR_HIP = 8,         /* a HIP launch failed */
+    DYNCONV_ERR_ARG = 9          /* another argument is out of range (dilation, activation, block count) */
+} dynconv_status;
+
+typedef enum {
+    DYNCONV_ACT_NONE = 0,
+    DYNCONV_ACT_RELU = 1,
+    DYNCONV_ACT_RELU6 = 2
+} dynconv_act;
+
+/* Shape of a feature map: n images of h x w positions and c channels. */
+typedef struct {
+    int32_t n, h, w, c;
+} dynconv_shape;
+
+/*
+ * One inverted-residual block with batch norm folded into weights and biases
+ * (Sec. 3.2: pointwise expansion, depthwise 3x3, linear pointwise
+ * projection), plus its 1x1 mask unit (Sec. 3.1.1).  All pointers (device).
+ * Weight layouts are PyTorch's convolution layouts, in the storage dtype:
+ *   w_expand  [c_hidden][c_in]    (from [E, C, 1, 1])
+ *   w_dw      [c_hidden][9]       (from [E, 1, 3, 3]; tap k = 3*(dh+1) + (dw+1))
+ *   w_project [c_out][c_hidden]   (from [Co, E, 1, 1])
+ * Biases are fp32.  The mask unit is an fp32 weight vector w_mask [c_in] and
+ * a scalar b_mask; MobileNetV2 uses act_expand = act_dw = RELU6 and
+ * act_project = NONE.
+ */
+typedef struct {
+    int32_t c_in, c_hidden, c_out;
+    const void *w_expand;
+    const float *b_expand;
+    const void *w_dw;
+    const float *b_dw;
+    const void *w_project;
+    const float *b_project;
+    int32_t act_expand, act_dw, act_project;
+    const float *w_mask;
+    float b_mask;
+} dynconv_block;
+
+/*
+ * Index maps of one hard mask (Sec. 3.2).  All arrays (device), int32, each
+ * with room for `capacity` >= N*H*W positions (nbr: 9*capacity entries):
+ *   active [P]     ascending flat positions with G = 1
+ *   dilated[P_d]   ascending flat positions with G_dilated = 1
+ *   nbr    [P][9]  nbr[p*9 + 3*(dh+1) + (dw+1)] = row of `dilated` holding the
+ *                  neighbour (h+dh, w+dw) of active[p], or -1 when it lies
+ *                  outside the image or outside the dilated mask
+ *   counts [2]     P, P_d
+ * Entries past the counts are left unspecified.
+ */
+typedef struct {
+    int32_t *active;
+    int32_t *dilated;
+    int32_t *nbr;
+    int32_t *counts;
+    int64_t capacity;
+} dynconv_indices;
+
+/* Text for a status code (static storage, never NULL). */
+const char *dynconv_status_str(dynconv_status status);
+
+/* Library identification string (static storage). */
+const char *dynconv_version(void);
+
+/*
+ * Mask unit and hard decision (Sec. 3.1.1, Eq. 2; Sec. 3.1.2, Eq. 8 with the
+ * Gumbel noise fixed to zero at inference):
+ *   m[i] = (sum over c ascending of w_mask[c] * x[i, c], as an fp32 fused
+ *           multiply-add chain starting from +0) + b_mask     (fp32)
+ *   mask[i] = m[i] > 0 ? 1 : 0                                 (ties, NaN -> 0)
+ *   x       (device) NHWC, dtype dt, shape s
+ *   w_mask  (device) fp32 [s.c]
+ *   mask    (device) uint8 [N*H*W], written
+ *   logits  (device) fp32 [N*H*W] or NULL, written when non-NULL
+ * The fp32 operation order is fixed, so masks are reproducible bit for bit.
+ */
+dynconv_status dynconv_mask(const void *x, dynconv_shape s, dynconv_dtype dt,
+                            const float *w_mask, float b_mask,
+                            uint8_t *mask, float *logits, void *stream);
+
+/* Workspace bytes that dynconv_build_indices needs for shape s. */
+size_t dynconv_indices_workspace_bytes(dynconv_shape s);
+
+/*
+ * Mask dilation and index maps, the paper's "bookkeeping" (Sec. 3.2, mask
+ * dilation and masked gather; Table 2): the (2*dilate+1)^2 square dilation
+ * of the mask within each image, then the raster-ordered lists and the
+ * neighbour table described at dynconv_indices.  Output is unique, so it is
+ * bit-exact and deterministic.
+ *   mask    (device) uint8 [N*H*W] (nonzero = active); s.c is ignored
+ *   dilate  0..3; block execution needs 1 (the depthwise kernel is 3x3)
+ *   idx     (host struct, device arrays) outputs, capacity >= N*H*W
+ *   ws      (device) dynconv_indices_workspace_bytes(s) bytes of scratch
+ */
+dynconv_status dynconv_build_indices(const uint8_t *mask, dynconv_shape s, int32_t dilate,
+                                     const dynconv_indices *idx, void *ws, size_t ws_bytes,
+                                     void *stream);
+
+/* Workspace bytes that dynconv_block_forward needs. */
+size_t dynconv_block_workspace_bytes(dynconv_shape s, const dynconv_block *blk,
+                                     dynconv_dtype dt);
+
+/*
+ * One gated residual block (Eq. 3 with r = identity), executed on the
+ * gathered rows only (Sec. 3.2):
+ *   y[i] = x[i] + F(x)[i]  where the mask is active, y[i] = x[i] elsewhere,
+ * with F = project(act_dw(DW3x3(act_expand(expand(x))))).  The expansion runs
+ * on the dilated positions, the depthwise and projection on the active ones.
+ *   x    (device) NHWC input, shape s, dtype dt
+ *   y    (device) NHWC output; y == x runs in place, any other overlap is
+ *        DYNCONV_ERR_SHAPE; when y != x inactive positions are copied
+ *   blk  (host struct, device weights)
+ *   idx  (host struct, device arrays) built by dynconv_build_indices with
+ *        dilate >= 1, or NULL for the dense block (Eq. 1) on all positions
+ *   ws   (device) dynconv_block_workspace_bytes bytes of scratch
+ */
+dynconv_status dynconv_block_forward(const void *x, void *y, dynconv_shape s, dynconv_dtype dt,
+                                     const dynconv_block *blk, const dynconv_indices *idx,
+                                     void *ws, size_t ws_bytes, void *stream);
+
+/* Workspace bytes that dynconv_stack_forward needs (largest block sets it). */
+size_t dynconv_stack_workspace_bytes(dynconv_shape s, const dynconv_block *blks,
+                                     int32_t n_blocks, dynconv_dtype dt);
+
+/*
+ * A stack of gated blocks in place (Sec. 3.1.1: every residual block has its
+ * own mask unit, applied to that block's input), one stream, no host
+ * synchronisation:
+ *   for b in 0..n_blocks-1:
+ *     mask_b = dynconv_mask(x, blks[b].w_mask, blks[b].b_mask)
+ *     idx_b  = dynconv_build_indices(mask_b, dilate = 1)
+ *     x      = dynconv_block_forward(x, x, blks[b], idx_b)
+ * With dense != 0 the mask units are skipped and every block runs densely on
+ * all positions (the baseline of Eq. 1).
+ *   x_inout (device) NHWC, shape s, dtype dt
+ *   blks    (host array of n_blocks, device weights), 1 <= n_blocks <= 1024
+ *   masks   (device) uint8 [n_blocks][N*H*W] or NULL: per-block hard masks
+ *   counts  (device) int32 [n_blocks][2] or NULL: per-block P, P_d
+ *   ws      (device) dynconv_stack_workspace_bytes bytes of scratch
+ */
+dynconv_status dynconv_stack_forward(void *x_inout, dynconv_shape s, dynconv_dtype dt,
+                                     const dynconv_block *blks, int32_t n_blocks, int32_t dense,
+                                     uint8_t *masks, int32_t *counts,
+                                     void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Launch sequence of dynconv_stack_forward, for profiling: stores up to `cap`
+ * kernel names (static strings) in launch order into `names` (may be NULL
+ * when cap is 0) and returns the number of launches, or -1 for an invalid
+ * n_blocks.  The sequence depends only on n_blocks and dense.
+ */
+int32_t dynconv_stack_launch_names(int32_t n_blocks, int32_t dense, const char **names,
+                                   int32_t cap);
+
+/*
+ * dynconv_stack_forward with per-kernel timing: launch i of the sequence that
+ * dynconv_stack_launch_names reports is issued with the event pair
+ * (events[2i], events[2i+1]) (hipEvent_t, created by the caller), which the
+ * runtime stamps when that kernel starts and ends, so
+ * hipEventElapsedTime(events[2i], events[2i+1]) is the kernel's duration.
+ * n_events must be at least 2 * count (else DYNCONV_ERR_ARG).  Results are
+ * identical to dynconv_stack_forward.
+ */
+dynconv_status dynconv_stack_forward_profiled(void *x_inout, dynconv_shape s, dynconv_dtype dt,
+                                              const dynconv_block *blks, int32_t n_blocks,
+                                              int32_t dense, uint8_t *masks, int32_t *counts,
+                                              void *ws, size_t ws_bytes, void *stream,
+                                              void *const *events, int32_t n_events);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DYNCONV_H_ */

@@ -1,0 +1,454 @@
+// dynconv.hip -- host side of the C ABI declared in include/dynconv.h:
+// argument validation, workspace carving and kernel launches.  Every entry
+// point validates everything before it enqueues anything, allocates nothing
+// and never synchronises with the host.
+#include <hip/hip_ext.h>
+#include <hip/hip_runtime.h>
+
+#include <stdint.h>
+#include <string.h>
+
+#include "dynconv.h"
+#include "kernels.h"
+
+using namespace dynconv;
+
+namespace {
+
+constexpr int kMaxC = 256;
+constexpr int kMaxE = 1536;
+constexpr int kMaxDilate = 3;
+constexpr int kMaxBlocks = 1024;
+constexpr int64_t kMaxPositions = (int64_t{1} << 31) / 9 - 1;
+constexpr int kMaxGrid = 2048;  // workgroups of the row-tile kernels (grid-stride beyond)
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+size_t dtype_size(dynconv_dtype dt) { return dt == DYNCONV_F32 ? 4 : 2; }
+
+bool dtype_ok(int dt) { return dt == DYNCONV_F32 || dt == DYNCONV_F16 || dt == DYNCONV_BF16; }
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int64_t positions(dynconv_shape s) {
+    return static_cast<int64_t>(s.n) * s.h * s.w;
+}
+
+dynconv_status check_shape(dynconv_shape s, bool need_c) {
+    if (s.n <= 0 || s.h <= 0 || s.w <= 0) return DYNCONV_ERR_SHAPE;
+    if (need_c && s.c <= 0) return DYNCONV_ERR_SHAPE;
+    if (positions(s) > kMaxPositions) return DYNCONV_ERR_SHAPE;
+    if (s.w > kMaxSeg * kWave) return DYNCONV_ERR_UNSUPPORTED;
+    return DYNCONV_OK;
+}
+
+dynconv_status check_channels(int c) {
+    if (c < 8 || c > kMaxC || c % 8 != 0) return DYNCONV_ERR_UNSUPPORTED;
+    return DYNCONV_OK;
+}
+
+dynconv_status check_block(const dynconv_block *b, dynconv_shape s, bool need_mask) {
+    if (!b) return DYNCONV_ERR_NULL;
+    if (!b->w_expand || !b->b_expand || !b->w_dw || !b->b_dw || !b->w_project || !b->b_project)
+        return DYNCONV_ERR_NULL;
+    if (need_mask && !b->w_mask) return DYNCONV_ERR_NULL;
+    if (b->c_in <= 0 || b->c_hidden <= 0 || b->c_out <= 0) return DYNCONV_ERR_SHAPE;
+    if (b->c_in != s.c) return DYNCONV_ERR_SHAPE;
+    if (b->c_out != b->c_in) return DYNCONV_ERR_UNSUPPORTED;  // identity path of Eq. 3
+    if (dynconv_status st = check_channels(b->c_in)) return st;
+    if (b->c_hidden < 16 || b->c_hidden > kMaxE || b->c_hidden % 16 != 0) return DYNCONV_ERR_UNSUPPORTED;
+    for (int a : {b->act_expand, b->act_dw, b->act_project})
+        if (a < DYNCONV_ACT_NONE || a > DYNCONV_ACT_RELU6) return DYNCONV_ERR_ARG;
+    if (!aligned16(b->w_expand) || !aligned16(b->w_dw) || !aligned16(b->w_project) ||
+        !aligned16(b->b_expand) || !aligned16(b->b_dw) || !aligned16(b->b_project))
+        return DYNCONV_ERR_ALIGN;
+    return DYNCONV_OK;
+}
+
+bool ranges_overlap(const void *a, size_t na, const void *b, size_t nb) {
+    uintptr_t x0 = reinterpret_cast<uintptr_t>(a), y0 = reinterpret_cast<uintptr_t>(b);
+    return x0 < y0 + nb && y0 < x0 + na;
+}
+
+dynconv_status launch_status() {
+    return hipGetLastError() == hipSuccess ? DYNCONV_OK : DYNCONV_ERR_HIP;
+}
+
+int grid_for_rows(int64_t rows) {
+    int64_t tiles = (rows + 15) / 16;
+    int64_t blocks = (tiles + kWavesPerBlock - 1) / kWavesPerBlock;
+    if (blocks < 1) blocks = 1;
+    return static_cast<int>(blocks < kMaxGrid ? blocks : kMaxGrid);
+}
+
+// Optional per-launch timing: launch i gets the event pair (ev[2i], ev[2i+1]),
+// which the runtime stamps at the start and the end of that kernel.
+struct Marks {
+    hipEvent_t const *ev = nullptr;
+    int32_t n = 0;  // number of events
+    int32_t i = 0;  // launches so far
+    void next(hipEvent_t *start, hipEvent_t *stop) {
+        if (ev && 2 * i + 1 < n) {
+            *start = ev[2 * i];
+            *stop = ev[2 * i + 1];
+        }
+        ++i;
+    }
+};
+
+template <typename... KArgs, typename... Args>
+void launch(Marks &mk, void (*kernel)(KArgs...), dim3 grid, dim3 block, size_t lds, hipStream_t st,
+            Args... args) {
+    hipEvent_t start = nullptr, stop = nullptr;
+    mk.next(&start, &stop);
+    hipExtLaunchKernelGGL(kernel, grid, block, static_cast<uint32_t>(lds), st, start, stop, 0u,
+                          static_cast<KArgs>(args)...);
+}
+
+// ------------------------------------------------------------ workspaces
+struct IndexScratch {
+    int2 *rowcnt;
+    int2 *rowoff;
+};
+
+size_t index_scratch_bytes(dynconv_shape s) {
+    int64_t rows = static_cast<int64_t>(s.n) * s.h;
+    return align_up(sizeof(int2) * rows) + align_up(sizeof(int2) * (rows + 1));
+}
+
+IndexScratch carve_index_scratch(void *ws, dynconv_shape s) {
+    int64_t rows = static_cast<int64_t>(s.n) * s.h;
+    char *p = static_cast<char *>(ws);
+    IndexScratch sc;
+    sc.rowcnt = reinterpret_cast<int2 *>(p);
+    p += align_up(sizeof(int2) * rows);
+    sc.rowoff = reinterpret_cast<int2 *>(p);
+    return sc;
+}
+
+size_t hidden_bytes(dynconv_shape s, int E, dynconv_dtype dt) {
+    return align_up(static_cast<size_t>(positions(s)) * E * dtype_size(dt));
+}
+
+// ------------------------------------------------------------ launches
+template <typename T>
+void launch_mask(const void *x, dynconv_shape s, const float *w_m, float b_m, uint8_t *mask,
+                 float *logits, hipStream_t st, Marks &mk) {
+    int64_t n = positions(s);
+    int grid = static_cast<int>((n + kBlock - 1) / kBlock);
+    launch(mk, k_mask<T>, dim3(grid), dim3(kBlock), 0, st, static_cast<const T *>(x), n,
+                       s.c, w_m, b_m, mask, logits);
+}
+
+void launch_indices(const uint8_t *mask, dynconv_shape s, int dilate, const dynconv_indices *idx,
+                    void *ws, hipStream_t st, Marks &mk) {
+    IndexScratch sc = carve_index_scratch(ws, s);
+    int64_t rows = static_cast<int64_t>(s.n) * s.h;
+    int grid = static_cast<int>((rows + kWavesPerBlock - 1) / kWavesPerBlock);
+    launch(mk, k_rowcount, dim3(grid), dim3(kBlock), 0, st, mask, s.n, s.h, s.w, dilate,
+                       sc.rowcnt);
+    launch(mk, k_rowscan, dim3(1), dim3(kScanThreads), 0, st, sc.rowcnt, rows, sc.rowoff,
+                       idx->counts);
+    launch(mk, k_compact, dim3(grid), dim3(kBlock), 0, st, mask, s.n, s.h, s.w, dilate,
+                       sc.rowoff, idx->active, idx->dilated, idx->nbr);
+}
+
+template <typename T, bool DENSE, int MAXKS>
+void launch_expand_k(const void *x, dynconv_shape s, const dynconv_block *b, const int32_t *dil,
+                     const int32_t *counts, void *h1, hipStream_t st, Marks &mk) {
+    int64_t rows = positions(s);
+    launch(mk, k_expand<T, DENSE, MAXKS>, dim3(grid_for_rows(rows)), dim3(kBlock), 0, st,
+                       static_cast<const T *>(x), b->c_in, b->c_hidden,
+                       static_cast<const T *>(b->w_expand), b->b_expand, b->act_expand, dil, counts,
+                       rows, static_cast<T *>(h1));
+}
+
+template <typename T, bool DENSE>
+void launch_expand(const void *x, dynconv_shape s, const dynconv_block *b, const int32_t *dil,
+                   const int32_t *counts, void *h1, hipStream_t st, Marks &mk) {
+    int ks = (b->c_in + 31) / 32;
+    if (ks <= 1) launch_expand_k<T, DENSE, 1>(x, s, b, dil, counts, h1, st, mk);
+    else if (ks <= 2) launch_expand_k<T, DENSE, 2>(x, s, b, dil, counts, h1, st, mk);
+    else if (ks <= 4) launch_expand_k<T, DENSE, 4>(x, s, b, dil, counts, h1, st, mk);
+    else launch_expand_k<T, DENSE, 8>(x, s, b, dil, counts, h1, st, mk);
+}
+
+template <typename T, bool DENSE, int MAXMT>
+void launch_dw_project_k(const void *h1, const void *x, void *y, dynconv_shape s,
+                         const dynconv_block *b, const int32_t *act, const int32_t *nbr,
+                         const int32_t *counts, hipStream_t st, Marks &mk) {
+    int64_t rows = positions(s);
+    size_t lds = sizeof(float) * 10 * static_cast<size_t>(b->c_hidden);
+    launch(mk, k_dw_project<T, DENSE, MAXMT>, dim3(grid_for_rows(rows)), dim3(kBlock), lds,
+                       st, static_cast<const T *>(h1), static_cast<const T *>(x), static_cast<T *>(y),
+                       s.n, s.h, s.w, s.c, b->c_hidden, static_cast<const T *>(b->w_dw), b->b_dw,
+                       b->act_dw, static_cast<const T *>(b->w_project), b->b_project, b->act_project,
+                       act, nbr, counts);
+}
+
+template <typename T, bool DENSE>
+void launch_dw_project(const void *h1, const void *x, void *y, dynconv_shape s,
+                       const dynconv_block *b, const int32_t *act, const int32_t *nbr,
+                       const int32_t *counts, hipStream_t st, Marks &mk) {
+    int mt = (b->c_out + 15) / 16;
+    if (mt <= 2) launch_dw_project_k<T, DENSE, 2>(h1, x, y, s, b, act, nbr, counts, st, mk);
+    else if (mt <= 4) launch_dw_project_k<T, DENSE, 4>(h1, x, y, s, b, act, nbr, counts, st, mk);
+    else if (mt <= 8) launch_dw_project_k<T, DENSE, 8>(h1, x, y, s, b, act, nbr, counts, st, mk);
+    else launch_dw_project_k<T, DENSE, 16>(h1, x, y, s, b, act, nbr, counts, st, mk);
+}
+
+template <typename T>
+void launch_block(const void *x, void *y, dynconv_shape s, const dynconv_block *b,
+                  const dynconv_indices *idx, void *h1, hipStream_t st, Marks &mk) {
+    if (idx) {
+        launch_expand<T, false>(x, s, b, idx->dilated, idx->counts, h1, st, mk);
+        launch_dw_project<T, false>(h1, x, y, s, b, idx->active, idx->nbr, idx->counts, st, mk);
+    } else {
+        launch_expand<T, true>(x, s, b, nullptr, nullptr, h1, st, mk);
+        launch_dw_project<T, true>(h1, x, y, s, b, nullptr, nullptr, nullptr, st, mk);
+    }
+}
+
+void launch_copy(const void *src, void *dst, size_t bytes, hipStream_t st) {
+    int64_t n16 = static_cast<int64_t>(bytes / 16);
+    int64_t blocks = (n16 + kBlock - 1) / kBlock;
+    int grid = static_cast<int>(blocks < 4096 ? (blocks < 1 ? 1 : blocks) : 4096);
+    Marks mk;
+    launch(mk, k_copy16, dim3(grid), dim3(kBlock), 0, st, static_cast<const uint4 *>(src),
+           static_cast<uint4 *>(dst), n16);
+}
+
+void dispatch_mask(dynconv_dtype dt, const void *x, dynconv_shape s, const float *w_m, float b_m,
+                   uint8_t *mask, float *logits, hipStream_t st, Marks &mk) {
+    if (dt == DYNCONV_F32) launch_mask<float>(x, s, w_m, b_m, mask, logits, st, mk);
+    else if (dt == DYNCONV_F16) launch_mask<half_t>(x, s, w_m, b_m, mask, logits, st, mk);
+    else launch_mask<bf16_t>(x, s, w_m, b_m, mask, logits, st, mk);
+}
+
+void dispatch_block(dynconv_dtype dt, const void *x, void *y, dynconv_shape s, const dynconv_block *b,
+                    const dynconv_indices *idx, void *h1, hipStream_t st, Marks &mk) {
+    if (dt == DYNCONV_F32) launch_block<float>(x, y, s, b, idx, h1, st, mk);
+    else if (dt == DYNCONV_F16) launch_block<half_t>(x, y, s, b, idx, h1, st, mk);
+    else launch_block<bf16_t>(x, y, s, b, idx, h1, st, mk);
+}
+
+// ------------------------------------------------------------ stack layout
+struct StackLayout {
+    size_t masks, active, dilated, nbr, counts, scratch, hidden, total;
+};
+
+StackLayout stack_layout(dynconv_shape s, const dynconv_block *blks, int32_t n_blocks,
+                         dynconv_dtype dt) {
+    StackLayout L;
+    size_t npos = static_cast<size_t>(positions(s));
+    int emax = 0;
+    for (int32_t b = 0; b < n_blocks; ++b)
+        if (blks[b].c_hidden > emax) emax = blks[b].c_hidden;
+    size_t off = 0;
+    L.masks = off;   off += align_up(npos);
+    L.active = off;  off += align_up(4 * npos);
+    L.dilated = off; off += align_up(4 * npos);
+    L.nbr = off;     off += align_up(36 * npos);
+    L.counts = off;  off += align_up(8 * static_cast<size_t>(n_blocks));
+    L.scratch = off; off += index_scratch_bytes(s);
+    L.hidden = off;  off += hidden_bytes(s, emax, dt);
+    L.total = off;
+    return L;
+}
+
+// The stack sequence shared by dynconv_stack_forward and its profiled form.
+dynconv_status stack_checked(void *x_inout, dynconv_shape s, dynconv_dtype dt,
+                             const dynconv_block *blks, int32_t n_blocks, int32_t dense,
+                             StackLayout *L) {
+    if (!x_inout || !blks) return DYNCONV_ERR_NULL;
+    if (!dtype_ok(dt)) return DYNCONV_ERR_DTYPE;
+    if (n_blocks < 1 || n_blocks > kMaxBlocks) return DYNCONV_ERR_ARG;
+    if (dynconv_status st = check_shape(s, true)) return st;
+    for (int32_t b = 0; b < n_blocks; ++b)
+        if (dynconv_status st = check_block(&blks[b], s, !dense)) return st;
+    if (!aligned16(x_inout)) return DYNCONV_ERR_ALIGN;
+    *L = stack_layout(s, blks, n_blocks, dt);
+    return DYNCONV_OK;
+}
+
+int32_t stack_launch_count(int32_t n_blocks, int32_t dense) {
+    return n_blocks * (dense ? 2 : 6);
+}
+
+void stack_enqueue(void *x_inout, dynconv_shape s, dynconv_dtype dt, const dynconv_block *blks,
+                   int32_t n_blocks, int32_t dense, uint8_t *masks, int32_t *counts, char *base,
+                   const StackLayout &L, hipStream_t st, Marks &mk) {
+    void *h1 = base + L.hidden;
+    if (dense) {
+        for (int32_t b = 0; b < n_blocks; ++b)
+            dispatch_block(dt, x_inout, x_inout, s, &blks[b], nullptr, h1, st, mk);
+        return;
+    }
+    size_t npos = static_cast<size_t>(positions(s));
+    dynconv_indices idx;
+    idx.active = reinterpret_cast<int32_t *>(base + L.active);
+    idx.dilated = reinterpret_cast<int32_t *>(base + L.dilated);
+    idx.nbr = reinterpret_cast<int32_t *>(base + L.nbr);
+    idx.capacity = static_cast<int64_t>(npos);
+    int32_t *cnt_all = counts ? counts : reinterpret_cast<int32_t *>(base + L.counts);
+    void *scratch = base + L.scratch;
+    for (int32_t b = 0; b < n_blocks; ++b) {
+        uint8_t *mask_b = masks ? masks + static_cast<size_t>(b) * npos
+                                : reinterpret_cast<uint8_t *>(base + L.masks);
+        idx.counts = cnt_all + 2 * b;
+        dispatch_mask(dt, x_inout, s, blks[b].w_mask, blks[b].b_mask, mask_b, nullptr, st, mk);
+        launch_indices(mask_b, s, 1, &idx, scratch, st, mk);
+        dispatch_block(dt, x_inout, x_inout, s, &blks[b], &idx, h1, st, mk);
+    }
+}
+
+const char *const kSparseNames[6] = {"k_mask", "k_rowcount", "k_rowscan", "k_compact", "k_expand",
+                                     "k_dw_project"};
+const char *const kDenseNames[2] = {"k_expand", "k_dw_project"};
+
+}  // namespace
+
+// ================================================================ C ABI
+extern "C" {
+
+const char *dynconv_status_str(dynconv_status status) {
+    switch (status) {
+    case DYNCONV_OK: return "ok";
+    case DYNCONV_ERR_NULL: return "required pointer is NULL";
+    case DYNCONV_ERR_SHAPE: return "invalid shape or overlapping buffers";
+    case DYNCONV_ERR_DTYPE: return "unknown dtype";
+    case DYNCONV_ERR_UNSUPPORTED: return "shape or channel count not supported by the kernels";
+    case DYNCONV_ERR_CAPACITY: return "index buffers smaller than N*H*W";
+    case DYNCONV_ERR_ALIGN: return "data pointer not 16-byte aligned";
+    case DYNCONV_ERR_WORKSPACE: return "workspace missing or too small";
+    case DYNCONV_ERR_HIP: return "HIP launch failed";
+    case DYNCONV_ERR_ARG: return "argument out of range";
+    }
+    return "unknown status";
+}
+
+const char *dynconv_version(void) { return "dynconv-mi355x 0.1 (gfx950)"; }
+
+dynconv_status dynconv_mask(const void *x, dynconv_shape s, dynconv_dtype dt, const float *w_mask,
+                            float b_mask, uint8_t *mask, float *logits, void *stream) {
+    if (!x || !w_mask || !mask) return DYNCONV_ERR_NULL;
+    if (!dtype_ok(dt)) return DYNCONV_ERR_DTYPE;
+    if (dynconv_status st = check_shape(s, true)) return st;
+    if (dynconv_status st = check_channels(s.c)) return st;
+    if (!aligned16(x)) return DYNCONV_ERR_ALIGN;
+    (void)hipGetLastError();
+    Marks mk;
+    dispatch_mask(dt, x, s, w_mask, b_mask, mask, logits, static_cast<hipStream_t>(stream), mk);
+    return launch_status();
+}
+
+size_t dynconv_indices_workspace_bytes(dynconv_shape s) {
+    if (check_shape(s, false) != DYNCONV_OK) return 0;
+    return index_scratch_bytes(s);
+}
+
+dynconv_status dynconv_build_indices(const uint8_t *mask, dynconv_shape s, int32_t dilate,
+                                     const dynconv_indices *idx, void *ws, size_t ws_bytes,
+                                     void *stream) {
+    if (!mask || !idx) return DYNCONV_ERR_NULL;
+    if (!idx->active || !idx->dilated || !idx->nbr || !idx->counts) return DYNCONV_ERR_NULL;
+    if (dynconv_status st = check_shape(s, false)) return st;
+    if (dilate < 0 || dilate > kMaxDilate) return DYNCONV_ERR_ARG;
+    if (idx->capacity < positions(s)) return DYNCONV_ERR_CAPACITY;
+    if (!ws || ws_bytes < index_scratch_bytes(s)) return DYNCONV_ERR_WORKSPACE;
+    if ((reinterpret_cast<uintptr_t>(ws) & 7u) != 0) return DYNCONV_ERR_ALIGN;
+    (void)hipGetLastError();
+    Marks mk;
+    launch_indices(mask, s, dilate, idx, ws, static_cast<hipStream_t>(stream), mk);
+    return launch_status();
+}
+
+size_t dynconv_block_workspace_bytes(dynconv_shape s, const dynconv_block *blk, dynconv_dtype dt) {
+    if (!blk || !dtype_ok(dt) || check_shape(s, true) != DYNCONV_OK || blk->c_hidden <= 0) return 0;
+    return hidden_bytes(s, blk->c_hidden, dt);
+}
+
+dynconv_status dynconv_block_forward(const void *x, void *y, dynconv_shape s, dynconv_dtype dt,
+                                     const dynconv_block *blk, const dynconv_indices *idx, void *ws,
+                                     size_t ws_bytes, void *stream) {
+    if (!x || !y) return DYNCONV_ERR_NULL;
+    if (!dtype_ok(dt)) return DYNCONV_ERR_DTYPE;
+    if (dynconv_status st = check_shape(s, true)) return st;
+    if (dynconv_status st = check_block(blk, s, false)) return st;
+    if (!aligned16(x) || !aligned16(y)) return DYNCONV_ERR_ALIGN;
+    size_t bytes = static_cast<size_t>(positions(s)) * s.c * dtype_size(dt);
+    if (x != y && ranges_overlap(x, bytes, y, bytes)) return DYNCONV_ERR_SHAPE;
+    if (idx) {
+        if (!idx->active || !idx->dilated || !idx->nbr || !idx->counts) return DYNCONV_ERR_NULL;
+        if (idx->capacity < positions(s)) return DYNCONV_ERR_CAPACITY;
+    }
+    if (!ws || ws_bytes < hidden_bytes(s, blk->c_hidden, dt)) return DYNCONV_ERR_WORKSPACE;
+    if (!aligned16(ws)) return DYNCONV_ERR_ALIGN;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    (void)hipGetLastError();
+    if (x != y) launch_copy(x, y, bytes, st);
+    Marks mk;
+    dispatch_block(dt, x, y, s, blk, idx, ws, st, mk);
+    return launch_status();
+}
+
+size_t dynconv_stack_workspace_bytes(dynconv_shape s, const dynconv_block *blks, int32_t n_blocks,
+                                     dynconv_dtype dt) {
+    if (!blks || n_blocks < 1 || n_blocks > kMaxBlocks || !dtype_ok(dt) ||
+        check_shape(s, true) != DYNCONV_OK)
+        return 0;
+    return stack_layout(s, blks, n_blocks, dt).total;
+}
+
+dynconv_status dynconv_stack_forward(void *x_inout, dynconv_shape s, dynconv_dtype dt,
+                                     const dynconv_block *blks, int32_t n_blocks, int32_t dense,
+                                     uint8_t *masks, int32_t *counts, void *ws, size_t ws_bytes,
+                                     void *stream) {
+    StackLayout L;
+    if (dynconv_status st = stack_checked(x_inout, s, dt, blks, n_blocks, dense, &L)) return st;
+    if (!ws || ws_bytes < L.total) return DYNCONV_ERR_WORKSPACE;
+    if (!aligned16(ws)) return DYNCONV_ERR_ALIGN;
+    (void)hipGetLastError();
+    Marks mk;
+    stack_enqueue(x_inout, s, dt, blks, n_blocks, dense, masks, counts, static_cast<char *>(ws), L,
+                  static_cast<hipStream_t>(stream), mk);
+    return launch_status();
+}
+
+int32_t dynconv_stack_launch_names(int32_t n_blocks, int32_t dense, const char **names,
+                                   int32_t cap) {
+    if (n_blocks < 1 || n_blocks > kMaxBlocks) return -1;
+    int32_t per = dense ? 2 : 6;
+    int32_t total = stack_launch_count(n_blocks, dense);
+    if (names)
+        for (int32_t i = 0; i < total && i < cap; ++i)
+            names[i] = dense ? kDenseNames[i % per] : kSparseNames[i % per];
+    return total;
+}
+
+dynconv_status dynconv_stack_forward_profiled(void *x_inout, dynconv_shape s, dynconv_dtype dt,
+                                              const dynconv_block *blks, int32_t n_blocks,
+                                              int32_t dense, uint8_t *masks, int32_t *counts,
+                                              void *ws, size_t ws_bytes, void *stream,
+                                              void *const *events, int32_t n_events) {
+    StackLayout L;
+    if (dynconv_status st = stack_checked(x_inout, s, dt, blks, n_blocks, dense, &L)) return st;
+    if (!ws || ws_bytes < L.total) return DYNCONV_ERR_WORKSPACE;
+    if (!aligned16(ws)) return DYNCONV_ERR_ALIGN;
+    if (!events) return DYNCONV_ERR_NULL;
+    int32_t total = stack_launch_count(n_blocks, dense);
+    if (n_events < 2 * total) return DYNCONV_ERR_ARG;
+    for (int32_t i = 0; i < 2 * total; ++i)
+        if (!events[i]) return DYNCONV_ERR_NULL;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    (void)hipGetLastError();
+    Marks mk;
+    mk.ev = reinterpret_cast<hipEvent_t const *>(events);
+    mk.n = 2 * total;
+    stack_enqueue(x_inout, s, dt, blks, n_blocks, dense, masks, counts, static_cast<char *>(ws), L,
+                  st, mk);
+    return launch_status();
+}
+
+}  // extern "C"

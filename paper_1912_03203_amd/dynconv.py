@@ -1,0 +1,295 @@
+"""Python binding of the C ABI in include/dynconv.h (argument marshalling only).
+
+Every computation happens in the HIP library ``libdynconv.so`` built next to
+this file; this module passes device pointers of torch tensors, sizes and the
+current HIP stream through ctypes.  There is no fallback: if the library is
+missing or a call fails, an exception is raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libdynconv.so")
+
+F32, F16, BF16 = 0, 1, 2
+ACT_NONE, ACT_RELU, ACT_RELU6 = 0, 1, 2
+
+_TORCH_DTYPE = {F32: torch.float32, F16: torch.float16, BF16: torch.bfloat16}
+_CODE = {torch.float32: F32, torch.float16: F16, torch.bfloat16: BF16}
+NAME_TO_DTYPE = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}
+
+EXPORTED = (
+    "dynconv_status_str", "dynconv_version", "dynconv_mask", "dynconv_indices_workspace_bytes",
+    "dynconv_build_indices", "dynconv_block_workspace_bytes", "dynconv_block_forward",
+    "dynconv_stack_workspace_bytes", "dynconv_stack_forward", "dynconv_stack_launch_names",
+    "dynconv_stack_forward_profiled",
+)
+
+
+class Shape(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int32), ("h", ctypes.c_int32), ("w", ctypes.c_int32),
+                ("c", ctypes.c_int32)]
+
+
+class Block(ctypes.Structure):
+    _fields_ = [
+        ("c_in", ctypes.c_int32), ("c_hidden", ctypes.c_int32), ("c_out", ctypes.c_int32),
+        ("w_expand", ctypes.c_void_p), ("b_expand", ctypes.c_void_p),
+        ("w_dw", ctypes.c_void_p), ("b_dw", ctypes.c_void_p),
+        ("w_project", ctypes.c_void_p), ("b_project", ctypes.c_void_p),
+        ("act_expand", ctypes.c_int32), ("act_dw", ctypes.c_int32), ("act_project", ctypes.c_int32),
+        ("w_mask", ctypes.c_void_p), ("b_mask", ctypes.c_float),
+    ]
+
+
+class Indices(ctypes.Structure):
+    _fields_ = [("active", ctypes.c_void_p), ("dilated", ctypes.c_void_p),
+                ("nbr", ctypes.c_void_p), ("counts", ctypes.c_void_p),
+                ("capacity", ctypes.c_int64)]
+
+
+class DynconvError(RuntimeError):
+    pass
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load the HIP library; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise DynconvError("libdynconv.so is not built (%s); run __graft_entry__.build()" % path)
+    lib = ctypes.CDLL(path)
+    vp, sz, i32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32
+    lib.dynconv_status_str.argtypes = [ctypes.c_int]
+    lib.dynconv_status_str.restype = ctypes.c_char_p
+    lib.dynconv_version.argtypes = []
+    lib.dynconv_version.restype = ctypes.c_char_p
+    lib.dynconv_mask.argtypes = [vp, Shape, ctypes.c_int, vp, ctypes.c_float, vp, vp, vp]
+    lib.dynconv_mask.restype = ctypes.c_int
+    lib.dynconv_indices_workspace_bytes.argtypes = [Shape]
+    lib.dynconv_indices_workspace_bytes.restype = sz
+    lib.dynconv_build_indices.argtypes = [vp, Shape, i32, ctypes.POINTER(Indices), vp, sz, vp]
+    lib.dynconv_build_indices.restype = ctypes.c_int
+    lib.dynconv_block_workspace_bytes.argtypes = [Shape, ctypes.POINTER(Block), ctypes.c_int]
+    lib.dynconv_block_workspace_bytes.restype = sz
+    lib.dynconv_block_forward.argtypes = [vp, vp, Shape, ctypes.c_int, ctypes.POINTER(Block),
+                                          ctypes.POINTER(Indices), vp, sz, vp]
+    lib.dynconv_block_forward.restype = ctypes.c_int
+    lib.dynconv_stack_workspace_bytes.argtypes = [Shape, ctypes.POINTER(Block), i32, ctypes.c_int]
+    lib.dynconv_stack_workspace_bytes.restype = sz
+    lib.dynconv_stack_forward.argtypes = [vp, Shape, ctypes.c_int, ctypes.POINTER(Block), i32, i32,
+                                          vp, vp, vp, sz, vp]
+    lib.dynconv_stack_forward.restype = ctypes.c_int
+    lib.dynconv_stack_launch_names.argtypes = [i32, i32, ctypes.POINTER(ctypes.c_char_p), i32]
+    lib.dynconv_stack_launch_names.restype = i32
+    lib.dynconv_stack_forward_profiled.argtypes = [vp, Shape, ctypes.c_int, ctypes.POINTER(Block),
+                                                   i32, i32, vp, vp, vp, sz, vp,
+                                                   ctypes.POINTER(ctypes.c_void_p), i32]
+    lib.dynconv_stack_forward_profiled.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def status_str(code: int) -> str:
+    return load().dynconv_status_str(code).decode()
+
+
+def _check(code: int, what: str):
+    if code != 0:
+        raise DynconvError("%s failed: %s (status %d)" % (what, status_str(code), code))
+
+
+def _stream(stream=None):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def dtype_code(dtype) -> int:
+    return _CODE[dtype]
+
+
+def shape_of(x: torch.Tensor) -> Shape:
+    n, h, w, c = x.shape
+    return Shape(n, h, w, c)
+
+
+# ------------------------------------------------------------------ weights
+@dataclass
+class BlockWeights:
+    """Device copies of one block's folded weights plus the C struct that
+    points at them (the tensors must outlive every call that uses it)."""
+
+    w_expand: torch.Tensor
+    b_expand: torch.Tensor
+    w_dw: torch.Tensor
+    b_dw: torch.Tensor
+    w_project: torch.Tensor
+    b_project: torch.Tensor
+    w_mask: torch.Tensor
+    b_mask: float
+    acts: tuple = (ACT_RELU6, ACT_RELU6, ACT_NONE)
+
+    @classmethod
+    def from_arrays(cls, wts: dict, dtype, device="cuda", b_mask=0.0, acts=None):
+        def dev(a, dt):
+            return torch.as_tensor(a).to(device=device, dtype=dt).contiguous()
+
+        return cls(dev(wts["w1"], dtype), dev(wts["b1"], torch.float32),
+                   dev(wts["w2"], dtype).reshape(-1, 9).contiguous(), dev(wts["b2"], torch.float32),
+                   dev(wts["w3"], dtype), dev(wts["b3"], torch.float32),
+                   dev(wts["w_m"], torch.float32), float(b_mask),
+                   tuple(acts) if acts is not None else tuple(wts.get("acts", (2, 2, 0))))
+
+    def struct(self) -> Block:
+        E, C = self.w_expand.shape
+        Co = self.w_project.shape[0]
+        return Block(C, E, Co, self.w_expand.data_ptr(), self.b_expand.data_ptr(),
+                     self.w_dw.data_ptr(), self.b_dw.data_ptr(), self.w_project.data_ptr(),
+                     self.b_project.data_ptr(), self.acts[0], self.acts[1], self.acts[2],
+                     self.w_mask.data_ptr(), float(self.b_mask))
+
+
+@dataclass
+class IndexBuffers:
+    active: torch.Tensor
+    dilated: torch.Tensor
+    nbr: torch.Tensor
+    counts: torch.Tensor
+
+    @classmethod
+    def alloc(cls, npos: int, device="cuda"):
+        z = dict(device=device, dtype=torch.int32)
+        return cls(torch.empty(max(npos, 1), **z), torch.empty(max(npos, 1), **z),
+                   torch.empty(max(npos, 1) * 9, **z), torch.zeros(2, **z))
+
+    def struct(self) -> Indices:
+        return Indices(self.active.data_ptr(), self.dilated.data_ptr(), self.nbr.data_ptr(),
+                       self.counts.data_ptr(), self.active.numel())
+
+
+# ------------------------------------------------------------------ calls
+def mask(x: torch.Tensor, w_mask: torch.Tensor, b_mask: float, out=None, logits=None, stream=None):
+    """Hard mask of one block (uint8 [N*H*W]); optional fp32 logits."""
+    lib = load()
+    n, h, w, _ = x.shape
+    if out is None:
+        out = torch.empty(n * h * w, dtype=torch.uint8, device=x.device)
+    _check(lib.dynconv_mask(_ptr(x), shape_of(x), dtype_code(x.dtype), _ptr(w_mask),
+                            ctypes.c_float(b_mask), _ptr(out), _ptr(logits), _stream(stream)),
+           "dynconv_mask")
+    return out
+
+
+def indices_workspace_bytes(shape: Shape) -> int:
+    return load().dynconv_indices_workspace_bytes(shape)
+
+
+def build_indices(mask_t: torch.Tensor, shape: Shape, dilate: int, idx: IndexBuffers,
+                  ws: torch.Tensor, stream=None):
+    lib = load()
+    s = idx.struct()
+    _check(lib.dynconv_build_indices(_ptr(mask_t), shape, int(dilate), ctypes.byref(s), _ptr(ws),
+                                     ws.numel() * ws.element_size(), _stream(stream)),
+           "dynconv_build_indices")
+
+
+def block_workspace_bytes(shape: Shape, blk: BlockWeights, dtype) -> int:
+    s = blk.struct()
+    return load().dynconv_block_workspace_bytes(shape, ctypes.byref(s), dtype_code(dtype))
+
+
+def block_forward(x: torch.Tensor, y: torch.Tensor, blk: BlockWeights, idx, ws: torch.Tensor,
+                  stream=None):
+    lib = load()
+    s = blk.struct()
+    ids = idx.struct() if idx is not None else None
+    _check(lib.dynconv_block_forward(_ptr(x), _ptr(y), shape_of(x), dtype_code(x.dtype),
+                                     ctypes.byref(s), ctypes.byref(ids) if ids is not None else None,
+                                     _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)),
+           "dynconv_block_forward")
+    return y
+
+
+def _blocks_array(blocks):
+    arr = (Block * len(blocks))()
+    for i, b in enumerate(blocks):
+        arr[i] = b.struct()
+    return arr
+
+
+def stack_workspace_bytes(shape: Shape, blocks, dtype) -> int:
+    arr = _blocks_array(blocks)
+    return load().dynconv_stack_workspace_bytes(shape, arr, len(blocks), dtype_code(dtype))
+
+
+class Stack:
+    """A prepared stack call: the block array and pointers are marshalled once,
+    so repeated launches (e.g. inside a timed loop or a graph capture) cost a
+    single ctypes call."""
+
+    def __init__(self, x: torch.Tensor, blocks, dense: bool, masks=None, counts=None, ws=None):
+        self.lib = load()
+        self.x = x
+        self.blocks = list(blocks)
+        self.arr = _blocks_array(self.blocks)
+        self.shape = shape_of(x)
+        self.dtype = dtype_code(x.dtype)
+        need = self.lib.dynconv_stack_workspace_bytes(self.shape, self.arr, len(self.blocks),
+                                                      self.dtype)
+        if need == 0:
+            raise DynconvError("dynconv_stack_workspace_bytes rejected the stack")
+        if ws is None:
+            ws = torch.empty(need, dtype=torch.uint8, device=x.device)
+        self.ws = ws
+        self.masks = masks
+        self.counts = counts
+        self.dense = 1 if dense else 0
+
+    def __call__(self, stream=None):
+        _check(self.lib.dynconv_stack_forward(_ptr(self.x), self.shape, self.dtype, self.arr,
+                                              len(self.blocks), self.dense, _ptr(self.masks),
+                                              _ptr(self.counts), _ptr(self.ws),
+                                              self.ws.numel() * self.ws.element_size(),
+                                              _stream(stream)),
+               "dynconv_stack_forward")
+        return self.x
+
+    def profiled(self, events, stream=None):
+        """Same call, with launch i timed by the raw HIP events
+        (events[2i], events[2i+1]); len(events) >= 2 * number of launches."""
+        arr = (ctypes.c_void_p * len(events))(*events)
+        _check(self.lib.dynconv_stack_forward_profiled(
+            _ptr(self.x), self.shape, self.dtype, self.arr, len(self.blocks), self.dense,
+            _ptr(self.masks), _ptr(self.counts), _ptr(self.ws),
+            self.ws.numel() * self.ws.element_size(), _stream(stream), arr, len(events)),
+            "dynconv_stack_forward_profiled")
+        return self.x
+
+
+def stack_launch_names(n_blocks: int, dense: bool):
+    lib = load()
+    total = lib.dynconv_stack_launch_names(n_blocks, 1 if dense else 0, None, 0)
+    if total < 0:
+        raise DynconvError("invalid block count %d" % n_blocks)
+    arr = (ctypes.c_char_p * total)()
+    lib.dynconv_stack_launch_names(n_blocks, 1 if dense else 0, arr, total)
+    return [a.decode() for a in arr]
+
+
+def stack_forward(x: torch.Tensor, blocks, dense=False, masks=None, counts=None, ws=None,
+                  stream=None):
+    return Stack(x, blocks, dense, masks, counts, ws)(stream)

@@ -147,16 +147,18 @@ def ellipse_mask_weights(rng, x_nhwc, labels, blocks, jitter=0.02):
 
 
 def round_to_storage(a, dtype):
-    """Round float values once to the storage dtype; returns float32 values that
-    are exactly representable in it (fp16 / bf16 round to nearest even)."""
-    a32 = np.ascontiguousarray(a, np.float32)
+    """Round float values to the storage dtype (nearest even); returns float32
+    values exactly representable in it.  fp32 and fp16 round once from the
+    input precision; bf16 rounds through fp32."""
+    a = np.asarray(a)
     if dtype == "f32":
-        return a32.copy()
+        return np.ascontiguousarray(a, np.float32).copy()
     if dtype == "f16":
-        return a32.astype(np.float16).astype(np.float32)
+        return np.ascontiguousarray(a.astype(np.float16).astype(np.float32))
     if dtype == "bf16":
         import torch
 
+        a32 = np.ascontiguousarray(a, np.float32)
         return torch.from_numpy(a32).to(torch.bfloat16).to(torch.float32).numpy()
     raise ValueError("unknown dtype %r" % (dtype,))
 

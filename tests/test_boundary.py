@@ -1,0 +1,146 @@
+"""The C-ABI library: it loads, exports every entry point that
+include/dynconv.h declares, sizes workspaces on the host, and rejects invalid
+arguments before anything is enqueued.  Runs without a GPU: every call here
+fails host-side validation, so no HIP call is made."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_1912_03203_amd import dynconv as dc
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dynconv.h")
+
+OK, ERR_NULL, ERR_SHAPE, ERR_DTYPE, ERR_UNSUPPORTED, ERR_CAPACITY, ERR_ALIGN, ERR_WORKSPACE, \
+    ERR_HIP, ERR_ARG = range(10)
+
+FAKE = 0x7F0000000000  # 16-byte aligned, never dereferenced: validation fails first
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dynconv_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(dc.LIB_PATH):
+        from paper_1912_03203_amd import build
+
+        build.build()
+    return dc.load()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = declared_functions()
+    assert set(dc.EXPORTED) == set(names)
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def test_status_strings_and_version(lib):
+    for code in range(10):
+        s = dc.status_str(code)
+        assert s and s != "unknown status"
+    assert dc.status_str(99) == "unknown status"
+    assert b"gfx950" in lib.dynconv_version()
+
+
+def fake_block(C=32, E=192, Co=None, acts=(2, 2, 0), **over):
+    Co = C if Co is None else Co
+    b = dc.Block(C, E, Co, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, acts[0], acts[1], acts[2], FAKE, 0.0)
+    for k, v in over.items():
+        setattr(b, k, v)
+    return b
+
+
+def test_mask_validation(lib):
+    s = dc.Shape(2, 8, 8, 32)
+    f = lib.dynconv_mask
+    assert f(None, s, 1, FAKE, 0.0, FAKE, None, None) == ERR_NULL
+    assert f(FAKE, s, 1, None, 0.0, FAKE, None, None) == ERR_NULL
+    assert f(FAKE, s, 1, FAKE, 0.0, None, None, None) == ERR_NULL
+    assert f(FAKE, s, 7, FAKE, 0.0, FAKE, None, None) == ERR_DTYPE
+    assert f(FAKE, dc.Shape(0, 8, 8, 32), 1, FAKE, 0.0, FAKE, None, None) == ERR_SHAPE
+    assert f(FAKE, dc.Shape(2, -1, 8, 32), 1, FAKE, 0.0, FAKE, None, None) == ERR_SHAPE
+    assert f(FAKE, dc.Shape(2, 8, 8, 0), 1, FAKE, 0.0, FAKE, None, None) == ERR_SHAPE
+    assert f(FAKE, dc.Shape(2, 8, 8, 12), 1, FAKE, 0.0, FAKE, None, None) == ERR_UNSUPPORTED
+    assert f(FAKE, dc.Shape(2, 8, 8, 264), 1, FAKE, 0.0, FAKE, None, None) == ERR_UNSUPPORTED
+    assert f(FAKE, dc.Shape(1, 1, 4097, 32), 1, FAKE, 0.0, FAKE, None, None) == ERR_UNSUPPORTED
+    # N*H*W*9 would overflow int32 indices
+    assert f(FAKE, dc.Shape(4096, 4096, 16, 8), 1, FAKE, 0.0, FAKE, None, None) == ERR_SHAPE
+    assert f(FAKE + 8, s, 1, FAKE, 0.0, FAKE, None, None) == ERR_ALIGN
+
+
+def test_build_indices_validation(lib):
+    s = dc.Shape(2, 8, 8, 0)
+    need = lib.dynconv_indices_workspace_bytes(s)
+    assert need == 256 + 256  # 16 rows of int2 counts, 17 of offsets, each 256-aligned
+    idx = dc.Indices(FAKE, FAKE, FAKE, FAKE, 128)
+    f = lib.dynconv_build_indices
+    assert f(None, s, 1, ctypes.byref(idx), FAKE, need, None) == ERR_NULL
+    assert f(FAKE, s, 1, None, FAKE, need, None) == ERR_NULL
+    bad = dc.Indices(FAKE, None, FAKE, FAKE, 128)
+    assert f(FAKE, s, 1, ctypes.byref(bad), FAKE, need, None) == ERR_NULL
+    assert f(FAKE, s, -1, ctypes.byref(idx), FAKE, need, None) == ERR_ARG
+    assert f(FAKE, s, 4, ctypes.byref(idx), FAKE, need, None) == ERR_ARG
+    small = dc.Indices(FAKE, FAKE, FAKE, FAKE, 127)
+    assert f(FAKE, s, 1, ctypes.byref(small), FAKE, need, None) == ERR_CAPACITY
+    assert f(FAKE, s, 1, ctypes.byref(idx), FAKE, need - 1, None) == ERR_WORKSPACE
+    assert f(FAKE, s, 1, ctypes.byref(idx), None, need, None) == ERR_WORKSPACE
+    assert f(FAKE, dc.Shape(2, 0, 8, 0), 1, ctypes.byref(idx), FAKE, need, None) == ERR_SHAPE
+
+
+def test_block_validation(lib):
+    s = dc.Shape(2, 8, 8, 32)
+    b = fake_block()
+    need = lib.dynconv_block_workspace_bytes(s, ctypes.byref(b), 1)
+    assert need == 2 * 8 * 8 * 192 * 2  # hidden rows x channels x fp16, already 256-aligned
+    f = lib.dynconv_block_forward
+
+    def call(x=FAKE, y=FAKE, shape=s, dt=1, blk=b, idx=None, ws=FAKE, nbytes=need):
+        return f(x, y, shape, dt, ctypes.byref(blk) if blk is not None else None,
+                 ctypes.byref(idx) if idx is not None else None, ws, nbytes, None)
+
+    assert call(x=None) == ERR_NULL
+    assert call(blk=None) == ERR_NULL
+    assert call(blk=fake_block(w_dw=None)) == ERR_NULL
+    assert call(dt=3) == ERR_DTYPE
+    assert call(blk=fake_block(C=24)) == ERR_SHAPE  # block channels differ from the map's
+    assert call(blk=fake_block(Co=16)) == ERR_UNSUPPORTED  # no identity path
+    assert call(blk=fake_block(E=152)) == ERR_UNSUPPORTED
+    assert call(blk=fake_block(E=1552)) == ERR_UNSUPPORTED
+    assert call(blk=fake_block(acts=(2, 3, 0))) == ERR_ARG
+    assert call(blk=fake_block(w_project=FAKE + 4)) == ERR_ALIGN
+    assert call(y=FAKE + 64) == ERR_SHAPE  # partial overlap with x
+    assert call(idx=dc.Indices(FAKE, FAKE, FAKE, FAKE, 127)) == ERR_CAPACITY
+    assert call(idx=dc.Indices(FAKE, FAKE, None, FAKE, 128)) == ERR_NULL
+    assert call(nbytes=need - 1) == ERR_WORKSPACE
+    assert call(ws=None) == ERR_WORKSPACE
+
+
+def test_stack_validation(lib):
+    s = dc.Shape(4, 16, 16, 32)
+    blocks = (dc.Block * 3)(fake_block(), fake_block(E=96), fake_block())
+    need = lib.dynconv_stack_workspace_bytes(s, blocks, 3, 1)
+    npos = 4 * 16 * 16
+    rows = 4 * 16
+
+    def up(v):
+        return (v + 255) // 256 * 256
+
+    expect = (npos + 4 * npos + 4 * npos + 36 * npos + up(8 * 3) + up(8 * rows)
+              + up(8 * (rows + 1)) + npos * 192 * 2)
+    assert need == expect
+    f = lib.dynconv_stack_forward
+    assert f(None, s, 1, blocks, 3, 0, None, None, FAKE, need, None) == ERR_NULL
+    assert f(FAKE, s, 1, blocks, 0, 0, None, None, FAKE, need, None) == ERR_ARG
+    assert f(FAKE, s, 1, blocks, 1025, 0, None, None, FAKE, need, None) == ERR_ARG
+    assert f(FAKE, s, 1, blocks, 3, 0, None, None, FAKE, need - 1, None) == ERR_WORKSPACE
+    nomask = (dc.Block * 1)(fake_block(w_mask=None))
+    need1 = lib.dynconv_stack_workspace_bytes(s, nomask, 1, 1)
+    assert f(FAKE, s, 1, nomask, 1, 0, None, None, FAKE, need1, None) == ERR_NULL
+    assert lib.dynconv_stack_workspace_bytes(s, blocks, 0, 1) == 0

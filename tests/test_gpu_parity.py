@@ -1,0 +1,349 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Masks, logits and index maps must match bit for bit; block outputs within the
+normwise relative error max|g - o| / max|o| of 1e-5 (fp32) or 2e-2 (fp16,
+bf16), checked both on y and on the residual branch F = y - x at active
+positions; inactive positions must keep x bit for bit.  Inputs are seeded
+synthetic workloads; the mask bias always comes from the oracle's logits."""
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_1912_03203_amd import dynconv as dc
+from paper_1912_03203_amd import inputs
+from tests import util
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    dc.load()
+
+
+def to_dev(x_f32, dtype):
+    return torch.from_numpy(np.ascontiguousarray(x_f32)).to(DEV).to(dc.NAME_TO_DTYPE[dtype])
+
+
+def host(t):
+    return t.detach().float().cpu().numpy() if t.dtype != torch.float32 else t.detach().cpu().numpy()
+
+
+def log(msg):
+    print(msg, flush=True)
+
+
+def gpu_mask(x_dev, w_m, b_m):
+    n, h, w, _ = x_dev.shape
+    wm = torch.from_numpy(np.asarray(w_m, np.float32)).to(DEV)
+    logits = torch.empty(n * h * w, dtype=torch.float32, device=DEV)
+    m = dc.mask(x_dev, wm, float(b_m), logits=logits)
+    return m, logits
+
+
+def gpu_indices(mask_dev, shape, dilate=1):
+    npos = shape.n * shape.h * shape.w
+    idx = dc.IndexBuffers.alloc(npos)
+    ws = torch.empty(max(dc.indices_workspace_bytes(shape), 1), dtype=torch.uint8, device=DEV)
+    dc.build_indices(mask_dev, shape, dilate, idx, ws)
+    torch.cuda.synchronize()
+    P, Pd = (int(v) for v in idx.counts.cpu())
+    return idx, P, Pd
+
+
+def check_indices(idx, P, Pd, A, D, nbr):
+    assert (P, Pd) == (A.size, D.size)
+    np.testing.assert_array_equal(idx.active[:P].cpu().numpy(), A)
+    np.testing.assert_array_equal(idx.dilated[:Pd].cpu().numpy(), D)
+    np.testing.assert_array_equal(idx.nbr[:P * 9].cpu().numpy().reshape(P, 9), nbr)
+
+
+def run_gpu_block(x_f32, wts, b_m, dtype, dense=False, out_of_place=False):
+    """mask -> indices -> block through the C ABI; returns dict of host arrays."""
+    x_dev = to_dev(x_f32, dtype)
+    shape = dc.shape_of(x_dev)
+    blk = dc.BlockWeights.from_arrays(wts, dc.NAME_TO_DTYPE[dtype], b_mask=b_m)
+    mask_dev, logits = gpu_mask(x_dev, wts["w_m"], b_m)
+    idx = None
+    P = Pd = None
+    if not dense:
+        idx, P, Pd = gpu_indices(mask_dev, shape)
+    ws = torch.empty(dc.block_workspace_bytes(shape, blk, x_dev.dtype), dtype=torch.uint8, device=DEV)
+    if out_of_place:
+        y_dev = torch.full_like(x_dev, float("nan"))
+        dc.block_forward(x_dev, y_dev, blk, idx, ws)
+    else:
+        y_dev = x_dev.clone()
+        dc.block_forward(y_dev, y_dev, blk, idx, ws)
+    torch.cuda.synchronize()
+    return {"mask": mask_dev.cpu().numpy(), "logits": logits.cpu().numpy(), "idx": idx, "P": P,
+            "Pd": Pd, "y": host(y_dev), "x_dev": x_dev, "y_dev": y_dev}
+
+
+def check_block_output(y_gpu, x_f32, y_oracle, G, dtype):
+    tol = util.TOL[dtype]
+    G = np.asarray(G).reshape(-1).astype(bool)
+    yg = y_gpu.reshape(-1, y_gpu.shape[-1])
+    xo = np.asarray(x_f32, np.float32).reshape(-1, y_gpu.shape[-1])
+    yo = y_oracle.reshape(-1, y_gpu.shape[-1])
+    # inactive positions keep x bit for bit
+    assert yg[~G].tobytes() == xo[~G].tobytes()
+    e_y = util.normwise(yg, yo)
+    e_f = util.normwise(yg[G].astype(np.float64) - xo[G], yo[G] - xo[G]) if G.any() else 0.0
+    log("  normwise err: y %.3e  F %.3e  (tol %.0e)" % (e_y, e_f, tol))
+    assert e_y <= tol
+    assert e_f <= tol
+
+
+# ------------------------------------------------------------------ mask
+@pytest.mark.parametrize("dtype,shape", [
+    ("f32", (1, 32, 32, 32)), ("f16", (32, 56, 56, 24)), ("bf16", (2, 7, 13, 24)),
+    ("f16", (3, 5, 70, 16)), ("f32", (1, 1, 1, 8)), ("bf16", (32, 64, 64, 32)),
+])
+def test_mask_bit_exact(dtype, shape):
+    N, H, W, C = shape
+    log("mask %s %s" % (dtype, shape))
+    rng = inputs.rng_for(sum(shape))
+    x = inputs.round_to_storage(inputs.blob_features(rng, N, H, W, C), dtype)
+    w_m = rng.normal(0, 0.1, C).astype(np.float32)
+    _, s = util.oracle_mask_chunked(util.nchw(x), w_m, 0.0)
+    b_m = inputs.percentile_bias(s, 0.3)
+    G, m = util.oracle_mask_chunked(util.nchw(x), w_m, b_m)
+    mask_dev, logits = gpu_mask(to_dev(x, dtype), w_m, b_m)
+    torch.cuda.synchronize()
+    assert logits.cpu().numpy().view(np.uint32).tobytes() == m.view(np.uint32).tobytes()
+    assert mask_dev.cpu().numpy().tobytes() == G.tobytes()
+    assert abs(int(G.sum()) - inputs.density_count(0.3, G.size)) <= 8  # ties only
+
+
+# ------------------------------------------------------------------ indices
+def _pattern(kind, N, H, W, rng):
+    if kind == "zeros":
+        return np.zeros(N * H * W, np.uint8)
+    if kind == "ones":
+        return np.ones(N * H * W, np.uint8)
+    if kind == "single":
+        g = np.zeros(N * H * W, np.uint8)
+        g[rng.integers(0, g.size)] = 1
+        return g
+    if kind == "corners":
+        g = np.zeros((N, H, W), np.uint8)
+        g[:, 0, 0] = g[:, -1, -1] = g[:, 0, -1] = g[:, -1, 0] = 1
+        return g.reshape(-1)
+    d = float(kind)
+    return (rng.random(N * H * W) < d).astype(np.uint8)
+
+
+@pytest.mark.parametrize("shape", [(2, 9, 13), (1, 1, 1), (3, 1, 40), (2, 40, 1), (4, 8, 64),
+                                   (2, 6, 65), (1, 5, 130), (2, 3, 200), (1, 2, 4096)])
+@pytest.mark.parametrize("kind", ["zeros", "ones", "single", "corners", "0.05", "0.3", "0.8"])
+def test_indices_bit_exact(shape, kind):
+    N, H, W = shape
+    rng = np.random.default_rng(zlib.crc32(repr((shape, kind)).encode()))
+    G = _pattern(kind, N, H, W, rng)
+    for r in (0, 1, 2, 3) if kind in ("0.05", "single") else (1,):
+        Gd = oracle.dilate(G, N, H, W, r)
+        A, D, nbr = oracle.indices(G, Gd, N, H, W)
+        idx, P, Pd = gpu_indices(torch.from_numpy(G).to(DEV), dc.Shape(N, H, W, 0), r)
+        check_indices(idx, P, Pd, A, D, nbr)
+
+
+# ------------------------------------------------------------------ block
+BLOCK_CASES = [
+    # name, dtype, (N, H, W, C, E), density, seed
+    ("fp32_parity_block", "f32", (1, 32, 32, 32, 192), 0.5, 0),
+    ("stage2_d0.10", "f16", (32, 56, 56, 24, 144), 0.10, 0),
+    ("stage2_d0.25", "f16", (32, 56, 56, 24, 144), 0.25, 0),
+    ("stage2_d0.50", "f16", (32, 56, 56, 24, 144), 0.50, 1),
+    ("stage2_d0.75", "f16", (32, 56, 56, 24, 144), 0.75, 2),
+    ("stage2_d0.90", "f16", (32, 56, 56, 24, 144), 0.90, 3),
+    ("ragged_bf16", "bf16", (3, 7, 11, 40, 80), 0.3, 4),
+    ("ragged_f16_wide", "f16", (2, 5, 100, 16, 48), 0.4, 5),
+    ("ragged_f32", "f32", (2, 9, 5, 8, 16), 0.6, 6),
+    ("max_channels_f16", "f16", (1, 6, 7, 256, 1536), 0.5, 7),
+    ("wide_hidden_bf16", "bf16", (2, 14, 14, 160, 960), 0.3, 8),
+]
+
+
+@pytest.mark.parametrize("case", BLOCK_CASES, ids=[c[0] for c in BLOCK_CASES])
+def test_block_parity(case):
+    name, dtype, (N, H, W, C, E), density, seed = case
+    log("block %s" % name)
+    rng = inputs.rng_for(1000 + seed)
+    x = inputs.round_to_storage(inputs.blob_features(rng, N, H, W, C), dtype)
+    wts = inputs.block_weights(rng, C, E, dtype=dtype)
+    o = util.oracle_calibrated_block(x, wts, density, dtype)
+    g = run_gpu_block(x, wts, o["b_m"], dtype)
+    assert g["mask"].tobytes() == o["G"].tobytes()
+    assert g["logits"].view(np.uint32).tobytes() == o["logits"].view(np.uint32).tobytes()
+    check_indices(g["idx"], g["P"], g["Pd"], o["A"], o["D"], o["nbr"])
+    check_block_output(g["y"], x, o["y"], o["G"], dtype)
+
+
+@pytest.mark.parametrize("dtype,shape", [("f16", (32, 64, 64, 32, 192)), ("f32", (1, 32, 32, 32, 192)),
+                                         ("bf16", (2, 10, 9, 24, 144))])
+def test_dense_block_parity(dtype, shape):
+    N, H, W, C, E = shape
+    log("dense block %s %s" % (dtype, shape))
+    rng = inputs.rng_for(77)
+    x = inputs.round_to_storage(inputs.blob_features(rng, N, H, W, C), dtype)
+    wts = inputs.block_weights(rng, C, E, dtype=dtype)
+    y_o = util.nhwc(util.oracle_block_dense_chunked(util.nchw(x).astype(np.float64), wts, None))
+    g = run_gpu_block(x, wts, 0.0, dtype, dense=True)
+    check_block_output(g["y"], x, y_o, np.ones(N * H * W, np.uint8), dtype)
+
+
+def test_out_of_place_matches_in_place():
+    rng = inputs.rng_for(5)
+    N, H, W, C, E = 4, 20, 24, 32, 192
+    x = inputs.round_to_storage(inputs.blob_features(rng, N, H, W, C), "f16")
+    wts = inputs.block_weights(rng, C, E, dtype="f16")
+    _, s = util.oracle_mask_chunked(util.nchw(x), wts["w_m"], 0.0)
+    b_m = inputs.percentile_bias(s, 0.25)
+    a = run_gpu_block(x, wts, b_m, "f16")
+    b = run_gpu_block(x, wts, b_m, "f16", out_of_place=True)
+    assert a["y"].tobytes() == b["y"].tobytes()
+    assert host(b["x_dev"]).tobytes() == x.tobytes()  # input untouched
+
+
+def test_zero_mask_is_identity_and_all_ones_is_dense():
+    rng = inputs.rng_for(6)
+    N, H, W, C, E = 3, 16, 18, 24, 144
+    x = inputs.round_to_storage(inputs.blob_features(rng, N, H, W, C), "f16")
+    wts = inputs.block_weights(rng, C, E, dtype="f16")
+    z = run_gpu_block(x, wts, -np.inf, "f16")
+    assert z["P"] == 0 and z["Pd"] == 0
+    assert z["y"].tobytes() == x.tobytes()
+    z2 = run_gpu_block(x, wts, -np.inf, "f16", out_of_place=True)
+    assert z2["y"].tobytes() == x.tobytes()
+    ones = run_gpu_block(x, wts, np.inf, "f16")
+    assert ones["P"] == ones["Pd"] == N * H * W
+    dense = run_gpu_block(x, wts, 0.0, "f16", dense=True)
+    assert ones["y"].tobytes() == dense["y"].tobytes()
+
+
+def test_repeat_runs_are_bitwise_identical():
+    rng = inputs.rng_for(8)
+    N, H, W, C, E = 32, 56, 56, 24, 144
+    x = inputs.round_to_storage(inputs.blob_features(rng, N, H, W, C), "f16")
+    wts = inputs.block_weights(rng, C, E, dtype="f16")
+    _, s = util.oracle_mask_chunked(util.nchw(x), wts["w_m"], 0.0)
+    b_m = inputs.percentile_bias(s, 0.25)
+    a = run_gpu_block(x, wts, b_m, "f16")
+    b = run_gpu_block(x, wts, b_m, "f16")
+    assert a["y"].tobytes() == b["y"].tobytes()
+    for k in ("active", "dilated", "nbr", "counts"):
+        assert torch.equal(getattr(a["idx"], k)[: a["P"]], getattr(b["idx"], k)[: b["P"]])
+
+
+# ------------------------------------------------------------------ stack
+def oracle_stack(x0, blocks, density, dtype):
+    """Oracle stack: each block's bias from its own input's logits; each
+    output rounded to the storage dtype before it enters the next block."""
+    xs, outs = [x0], []
+    for wts in blocks:
+        o = util.oracle_calibrated_block(xs[-1], wts, density, dtype)
+        outs.append(o)
+        xs.append(o["y_store"])
+    return xs, outs
+
+
+@pytest.fixture(scope="module")
+def pose_stack():
+    wl = inputs.WORKLOADS["pose_stack8_64x64x32_f16"]
+    x0, blocks, _ = inputs.make_block_inputs(wl, 0)
+    log("oracle stack %s (8 blocks)" % wl.name)
+    xs, outs = oracle_stack(x0, blocks, 0.25, wl.dtype)
+    return wl, blocks, xs, outs
+
+
+def test_stack_blocks_teacher_forced(pose_stack):
+    """Block b on the GPU fed the oracle's input of block b: masks and lists
+    bit-exact, output within tolerance, for all 8 blocks at full size."""
+    wl, blocks, xs, outs = pose_stack
+    for b, (wts, o) in enumerate(zip(blocks, outs)):
+        log("stack block %d" % b)
+        g = run_gpu_block(xs[b], wts, o["b_m"], wl.dtype)
+        assert g["mask"].tobytes() == o["G"].tobytes()
+        check_indices(g["idx"], g["P"], g["Pd"], o["A"], o["D"], o["nbr"])
+        # the recipe's exact count assumes distinct logits; fp32 ties at the
+        # threshold may remove a few positions (the mask itself matched above)
+        assert abs(g["P"] - inputs.density_count(0.25, wl.nhw)) <= 8
+        check_block_output(g["y"], xs[b], o["y"], o["G"], wl.dtype)
+
+
+def test_stack_call_matches_block_calls(pose_stack):
+    """dynconv_stack_forward sequences the same kernels as the per-block calls:
+    bitwise equal results, masks and counts."""
+    wl, blocks, xs, outs = pose_stack
+    dt = dc.NAME_TO_DTYPE[wl.dtype]
+    bw = [dc.BlockWeights.from_arrays(w, dt, b_mask=o["b_m"]) for w, o in zip(blocks, outs)]
+    x_dev = to_dev(xs[0], wl.dtype)
+    masks = torch.zeros(wl.blocks, wl.nhw, dtype=torch.uint8, device=DEV)
+    counts = torch.zeros(wl.blocks, 2, dtype=torch.int32, device=DEV)
+    y_stack = x_dev.clone()
+    dc.stack_forward(y_stack, bw, dense=False, masks=masks, counts=counts)
+    y_seq = x_dev.clone()
+    shape = dc.shape_of(x_dev)
+    for b, blk in enumerate(bw):
+        m, _ = gpu_mask(y_seq, blocks[b]["w_m"], outs[b]["b_m"])
+        idx, P, Pd = gpu_indices(m, shape)
+        assert torch.equal(m, masks[b])
+        assert (P, Pd) == tuple(int(v) for v in counts[b].cpu())
+        ws = torch.empty(dc.block_workspace_bytes(shape, blk, dt), dtype=torch.uint8, device=DEV)
+        dc.block_forward(y_seq, y_seq, blk, idx, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(y_stack, y_seq)
+    # End to end against the oracle (no teacher forcing).  Block 0 sees the same
+    # input, so its mask is exact.  Later inputs differ by the accumulated
+    # rounding of b blocks, at most about b * tol * max|x_b| per element, so a
+    # mask can only flip where |m| <= ||w_m||_1 * b * tol * max|x_b| -- unless an
+    # earlier flip at block b' lies within Chebyshev distance b - b' (a flip
+    # changes that position's output, and each block's 3x3 depthwise spreads it
+    # by one position).  Flips must also stay rare.
+    from scipy import ndimage
+
+    N, H, W = wl.n, wl.h, wl.w
+    tol = util.TOL[wl.dtype]
+    flip_maps = [(masks[b].cpu().numpy() != outs[b]["G"]).reshape(N, H, W) for b in range(wl.blocks)]
+    flips = [int(f.sum()) for f in flip_maps]
+    log("  end-to-end mask flips per block: %s" % flips)
+    assert flips[0] == 0
+    assert sum(flips) <= 1e-3 * wl.nhw * wl.blocks
+    for b in range(1, wl.blocks):
+        reach = np.zeros((N, H, W), bool)
+        for bp in range(b):
+            if flip_maps[bp].any():
+                st = np.ones((1, 2 * (b - bp) + 1, 2 * (b - bp) + 1), bool)
+                reach |= ndimage.binary_dilation(flip_maps[bp], structure=st)
+        primary = flip_maps[b] & ~reach
+        if primary.any():
+            bound = np.abs(blocks[b]["w_m"]).sum() * b * tol * np.max(np.abs(xs[b]))
+            m = np.abs(outs[b]["logits"]).reshape(N, H, W)[primary]
+            log("  block %d: %d primary flips, max |m| %.3e, bound %.3e" % (b, primary.sum(), m.max(), bound))
+            assert np.max(m) <= bound
+
+
+def test_dense_stack_matches_oracle():
+    wl = inputs.WORKLOADS["pose_stack8_64x64x32_f16"]
+    x0, blocks, _ = inputs.make_block_inputs(wl, 1)
+    x0 = x0[:4]  # four images: the dense stack has no batch-wide statistic
+    dt = dc.NAME_TO_DTYPE[wl.dtype]
+    bw = [dc.BlockWeights.from_arrays(w, dt) for w in blocks]
+    x_dev = to_dev(x0, wl.dtype)
+    dc.stack_forward(x_dev, bw, dense=True)
+    torch.cuda.synchronize()
+    xb = x0
+    for wts in blocks:
+        y = util.nhwc(util.oracle_block_dense_chunked(util.nchw(xb).astype(np.float64), wts, None))
+        xb = inputs.round_to_storage(y, wl.dtype)
+    err = util.normwise(host(x_dev), xb)
+    log("  dense stack normwise err %.3e" % err)
+    assert err <= util.TOL[wl.dtype]
