@@ -5,11 +5,13 @@ Default workload: 8 stacked stride-1 gated inverted-residual blocks at
 32 x 64x64x32 (hidden 192), fp16 storage, synthetic ellipse ("person")
 features, every block's mask bias set so that 25% of the positions are active.
 
-A step is one pass of the whole hot path over the batch: restore the input
-(one device copy, 8 MiB, inside the timed step), then for each block the mask
-unit, the index maps, gather + expansion, depthwise + projection + scatter-add.
-Steps run from a captured HIP graph (--no-graph: eager).  W warm-up steps, then
-exactly K timed steps between two device synchronisations.
+A step is one pass of the whole hot path over the batch: for each block the
+mask unit, the active / halo lists, gather + expansion, depthwise + projection
++ scatter-add into the identity path.  The input stays resident in HBM and is
+not modified; the stack writes a separate output buffer.  Steps run from a
+captured HIP graph (--no-graph: eager).  W warm-up steps, then exactly K timed
+steps between two device synchronisations.  --unfused times the multi-kernel
+chain instead of the one-launch blocks.
 
 Also reported on the same JSON line:
   dense         the same stack with every block dense (no mask, no lists)
@@ -94,22 +96,24 @@ def calibrate(dc, inputs, torch, x0_dev, blocks_np, dt, density):
 
 
 class Runner:
-    """One timed step (restore input + stack call), eager or graph-replayed."""
+    """One timed step (the stack call, input -> output buffer), eager or
+    graph-replayed."""
 
-    def __init__(self, dc, torch, x0, blocks, dense, use_graph, n_blocks):
+    def __init__(self, dc, torch, x0, blocks, flags, use_graph, n_blocks):
         self.torch = torch
         self.x0 = x0
-        self.x = x0.clone()
+        self.y = torch.empty_like(x0)
         npos = x0.shape[0] * x0.shape[1] * x0.shape[2]
+        dense = flags & dc.STACK_DENSE
         self.masks = None if dense else torch.zeros(n_blocks, npos, dtype=torch.uint8, device=x0.device)
         self.counts = None if dense else torch.zeros(n_blocks, 2, dtype=torch.int32, device=x0.device)
-        self.stack = dc.Stack(self.x, blocks, dense, masks=self.masks, counts=self.counts)
+        self.stack = dc.Stack(x0, self.y, blocks, flags=flags, masks=self.masks, counts=self.counts)
+        self.names = self.stack.launch_names()
         self.graph = None
         if use_graph:
             self.graph = self._capture()
 
     def eager(self):
-        self.x.copy_(self.x0)
         self.stack()
 
     def _capture(self):
@@ -144,14 +148,14 @@ class Runner:
         return (time.perf_counter() - t0) / steps
 
 
-def profile_kernels(dc, torch, runner, names, steps):
+def profile_kernels(dc, torch, runner, steps):
     """Average duration per kernel name from start/end events that the HIP
     runtime stamps on every launch of the library (profiled stack call)."""
+    names = runner.names
     ev = HipEvents(torch, 2 * len(names))
     per_launch = np.zeros(len(names))
     try:
         for _ in range(steps):
-            runner.x.copy_(runner.x0)
             runner.stack.profiled(ev.ev)
             torch.cuda.synchronize()
             per_launch += [ev.elapsed_ms(2 * i, 2 * i + 1) for i in range(len(names))]
@@ -167,9 +171,17 @@ def profile_kernels(dc, torch, runner, names, steps):
             for k, v in out.items()}, per_launch
 
 
-def algorithmic_bytes(name, dense, s, C, E, npos, rows, P, Pd):
+def algorithmic_bytes(name, dense, s, C, E, npos, rows, P, Pd, last=False):
     """Bytes one launch must move at minimum (each input read once, each output
-    written once); P, Pd are the block's active and dilated counts."""
+    written once); P, Pd are the block's active and dilated counts.  The
+    one-launch block reads x and writes y at every position (its output is a
+    separate buffer), reads this block's mask and writes the next one's."""
+    weights = 2 * E * C * s + 9 * E * s + 4 * (2 * E + C)
+    if name == "k_block_fused":
+        masks = 0 if dense else npos + (0 if last else npos)
+        return 2 * npos * C * s + masks + weights
+    if name == "k_copy16":
+        return 2 * npos * C * s
     if dense:
         if name == "k_expand":
             return npos * C * s + npos * E * s + E * C * s + 4 * E
@@ -225,17 +237,17 @@ def cpu_baseline(inputs, wl, x0_np, blocks_np, density, budget_s=12.0):
                       "gather/scatter block; fp64 C loops, one thread); %.1f s" % (S, wl.n, len(blocks_np), t)}
 
 
-def density_sweep(dc, inputs, torch, steps, warmup, use_graph):
+def density_sweep(dc, inputs, torch, steps, warmup, use_graph, flags):
     wl = inputs.WORKLOADS["mbv2_stage2_block_56x56x24_f16"]
     x_np, blocks_np, _ = inputs.make_block_inputs(wl, 0)
     dt = dc.NAME_TO_DTYPE[wl.dtype]
     x0 = torch.from_numpy(x_np).cuda().to(dt)
     dense_blk = [dc.BlockWeights.from_arrays(blocks_np[0], dt)]
-    dense_t = Runner(dc, torch, x0, dense_blk, True, use_graph, 1).timed(steps, warmup)
+    dense_t = Runner(dc, torch, x0, dense_blk, flags | dc.STACK_DENSE, use_graph, 1).timed(steps, warmup)
     rows = []
     for d in wl.densities:
         blks = calibrate(dc, inputs, torch, x0, blocks_np, dt, d)
-        r = Runner(dc, torch, x0, blks, False, use_graph, 1)
+        r = Runner(dc, torch, x0, blks, flags, use_graph, 1)
         t = r.timed(steps, warmup)
         P, Pd = (int(v) for v in r.counts[0].cpu())
         rows.append({"density": d, "active_frac": P / wl.nhw, "dilated_frac": Pd / wl.nhw,
@@ -253,6 +265,7 @@ def main():
     ap.add_argument("--density", type=float, default=0.25)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-graph", action="store_true")
+    ap.add_argument("--unfused", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--profile-steps", type=int, default=20)
@@ -283,19 +296,21 @@ def main():
     sparse_blocks = calibrate(dc, inputs, torch, x0, blocks_np, dt, args.density)
     dense_blocks = [dc.BlockWeights.from_arrays(w, dt) for w in blocks_np]
 
-    sp = Runner(dc, torch, x0, sparse_blocks, False, use_graph, wl.blocks)
-    dn = Runner(dc, torch, x0, dense_blocks, True, use_graph, wl.blocks)
+    base_flags = dc.STACK_UNFUSED if args.unfused else 0
+    sp = Runner(dc, torch, x0, sparse_blocks, base_flags, use_graph, wl.blocks)
+    dn = Runner(dc, torch, x0, dense_blocks, base_flags | dc.STACK_DENSE, use_graph, wl.blocks)
     if use_graph:  # replays must reproduce the eager step bit for bit
         for r in (sp, dn):
             r.eager()
             torch.cuda.synchronize()
-            ref = r.x.clone()
+            ref = r.y.clone()
             for _ in range(3):
+                r.y.zero_()
                 r.step()
                 torch.cuda.synchronize()
-                if not torch.equal(r.x, ref):
+                if not torch.equal(r.y, ref):
                     raise RuntimeError("graph replay differs from the eager step")
-    log("timing sparse")
+    log("timing sparse (%s)" % " ".join(sorted(set(sp.names))))
     t_sp = sp.timed(args.steps, args.warmup)
     log("timing dense")
     t_dn = dn.timed(args.steps, args.warmup)
@@ -305,28 +320,26 @@ def main():
     dilated = (counts[:, 1] / npos).tolist()
     log("sparse %.1f us/step, dense %.1f us/step, speedup %.2fx" % (1e6 * t_sp, 1e6 * t_dn, t_dn / t_sp))
 
-    # per-kernel profile (events on the library's stream)
-    names_sp = dc.stack_launch_names(wl.blocks, False)
-    names_dn = dc.stack_launch_names(wl.blocks, True)
-    prof_sp, per_sp = profile_kernels(dc, torch, sp, names_sp, args.profile_steps)
-    prof_dn, _ = profile_kernels(dc, torch, dn, names_dn, args.profile_steps)
+    # per-kernel profile (runtime-stamped events on each launch)
+    prof_sp, _ = profile_kernels(dc, torch, sp, args.profile_steps)
+    prof_dn, _ = profile_kernels(dc, torch, dn, args.profile_steps)
     s = 2 if wl.dtype != "f32" else 4
     rows = wl.n * wl.h
+
+    def avg_bytes(name, dense):
+        if dense:
+            return float(algorithmic_bytes(name, True, s, wl.c, wl.e, npos, rows, npos, npos))
+        per = [algorithmic_bytes(name, False, s, wl.c, wl.e, npos, rows, int(P), int(Pd),
+                                 last=(b == wl.blocks - 1)) for b, (P, Pd) in enumerate(counts)]
+        return float(np.mean(per))
+
+    for prof, dense in ((prof_sp, False), (prof_dn, True)):
+        for k, v in prof.items():
+            v["algorithmic_bytes"] = avg_bytes(k, dense)
+            v["gbs"] = v["algorithmic_bytes"] / (v["avg_us"] * 1e-6) / 1e9
     dom = max(prof_sp, key=lambda k: prof_sp[k]["total_us"])
-    # algorithmic bytes of the dominant kernel, averaged over its launches
-    per_block = [algorithmic_bytes(dom, False, s, wl.c, wl.e, npos, rows, int(P), int(Pd))
-                 for P, Pd in counts]
-    bytes_per_launch = float(np.mean(per_block))
-    achieved = bytes_per_launch / (prof_sp[dom]["avg_us"] * 1e-6) / 1e9
-    for k, v in prof_sp.items():
-        b = np.mean([algorithmic_bytes(k, False, s, wl.c, wl.e, npos, rows, int(P), int(Pd))
-                     for P, Pd in counts])
-        v["algorithmic_bytes"] = float(b)
-        v["gbs"] = float(b / (v["avg_us"] * 1e-6) / 1e9)
-    for k, v in prof_dn.items():
-        b = algorithmic_bytes(k, True, s, wl.c, wl.e, npos, rows, npos, npos)
-        v["algorithmic_bytes"] = float(b)
-        v["gbs"] = float(b / (v["avg_us"] * 1e-6) / 1e9)
+    bytes_per_launch = prof_sp[dom]["algorithmic_bytes"]
+    achieved = prof_sp[dom]["gbs"]
     kernel_sum_us = float(sum(v["total_us"] for v in prof_sp.values()))
 
     result = {
@@ -344,7 +357,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "batch": wl.n, "h": wl.h, "w": wl.w, "c": wl.c,
                    "hidden": wl.e, "blocks": wl.blocks, "density": args.density,
-                   "graph": use_graph, "seed": args.seed},
+                   "graph": use_graph, "seed": args.seed,
+                   "execution": "kernel chain" if args.unfused else "one launch per block"},
         "speedup_vs_dense": t_dn / t_sp,
         "dense": {"value": wl.n / t_dn, "ms_per_step": 1e3 * t_dn},
         "per_block_us": {"sparse": 1e6 * t_sp / wl.blocks, "dense": 1e6 * t_dn / wl.blocks},
@@ -358,7 +372,7 @@ def main():
     if not args.no_sweep:
         log("density sweep")
         result["sweep"] = density_sweep(dc, inputs, torch, min(args.steps, 100), min(args.warmup, 10),
-                                        use_graph)
+                                        use_graph, base_flags)
     if not args.no_cpu:
         log("cpu baseline (oracle)")
         result["cpu_baseline"] = cpu_baseline(inputs, wl, x_np, blocks_np, args.density)

@@ -181,39 +181,58 @@ dynconv_status dynconv_block_forward(const void *x, void *y, dynconv_shape s, dy
                                      const dynconv_block *blk, const dynconv_indices *idx,
                                      void *ws, size_t ws_bytes, void *stream);
 
-/* Workspace bytes that dynconv_stack_forward needs (largest block sets it). */
+/* Flags of dynconv_stack_forward. */
+#define DYNCONV_STACK_DENSE 1   /* every block on all positions (Eq. 1), no mask units */
+#define DYNCONV_STACK_UNFUSED 2 /* force the multi-kernel chain (mask, index maps, block) */
+
+/* Workspace bytes that dynconv_stack_forward needs for these blocks and flags. */
 size_t dynconv_stack_workspace_bytes(dynconv_shape s, const dynconv_block *blks,
-                                     int32_t n_blocks, dynconv_dtype dt);
+                                     int32_t n_blocks, dynconv_dtype dt, int32_t flags);
 
 /*
- * A stack of gated blocks in place (Sec. 3.1.1: every residual block has its
- * own mask unit, applied to that block's input), one stream, no host
- * synchronisation:
+ * A stack of gated blocks (Sec. 3.1.1: every residual block has its own mask
+ * unit, applied to that block's input), one stream, no host synchronisation.
+ * The result is that of
+ *   x_0 = x
  *   for b in 0..n_blocks-1:
- *     mask_b = dynconv_mask(x, blks[b].w_mask, blks[b].b_mask)
- *     idx_b  = dynconv_build_indices(mask_b, dilate = 1)
- *     x      = dynconv_block_forward(x, x, blks[b], idx_b)
- * With dense != 0 the mask units are skipped and every block runs densely on
+ *     mask_b  = dynconv_mask(x_b, blks[b].w_mask, blks[b].b_mask)
+ *     idx_b   = dynconv_build_indices(mask_b, dilate = 1)
+ *     x_{b+1} = dynconv_block_forward(x_b, blks[b], idx_b)
+ *   y = x_{n_blocks}
+ * With DYNCONV_STACK_DENSE the mask units are skipped and every block runs on
  * all positions (the baseline of Eq. 1).
- *   x_inout (device) NHWC, shape s, dtype dt
- *   blks    (host array of n_blocks, device weights), 1 <= n_blocks <= 1024
- *   masks   (device) uint8 [n_blocks][N*H*W] or NULL: per-block hard masks
- *   counts  (device) int32 [n_blocks][2] or NULL: per-block P, P_d
- *   ws      (device) dynconv_stack_workspace_bytes bytes of scratch
+ *
+ * Execution: when s.w <= 64 and s.c <= 64 (s.c <= 32 for fp32) and
+ * DYNCONV_STACK_UNFUSED is not set, each block is ONE kernel that builds the active and halo lists of a
+ * band of image rows on chip (ballot ranks in raster order), gathers,
+ * expands, runs the depthwise and the projection, adds the identity path and
+ * computes the next block's mask; blocks alternate between y and a workspace
+ * copy.  Otherwise the block runs the kernel chain of the per-block calls,
+ * in place on y.  Both give identical masks and counts; outputs agree
+ * within rounding of the same arithmetic.
+ *   x      (device) NHWC input, shape s, dtype dt; read only unless y == x
+ *   y      (device) NHWC output; y == x runs in place, other overlap is
+ *          DYNCONV_ERR_SHAPE
+ *   blks   (host array of n_blocks, device weights), 1 <= n_blocks <= 1024
+ *   flags  0 or DYNCONV_STACK_DENSE / DYNCONV_STACK_UNFUSED (others: ERR_ARG)
+ *   masks  (device) uint8 [n_blocks][N*H*W] or NULL: per-block hard masks
+ *   counts (device) int32 [n_blocks][2] or NULL: per-block P, P_d
+ *   ws     (device) dynconv_stack_workspace_bytes bytes of scratch
  */
-dynconv_status dynconv_stack_forward(void *x_inout, dynconv_shape s, dynconv_dtype dt,
-                                     const dynconv_block *blks, int32_t n_blocks, int32_t dense,
-                                     uint8_t *masks, int32_t *counts,
-                                     void *ws, size_t ws_bytes, void *stream);
+dynconv_status dynconv_stack_forward(const void *x, void *y, dynconv_shape s, dynconv_dtype dt,
+                                     const dynconv_block *blks, int32_t n_blocks, int32_t flags,
+                                     uint8_t *masks, int32_t *counts, void *ws, size_t ws_bytes,
+                                     void *stream);
 
 /*
  * Launch sequence of dynconv_stack_forward, for profiling: stores up to `cap`
  * kernel names (static strings) in launch order into `names` (may be NULL
- * when cap is 0) and returns the number of launches, or -1 for an invalid
- * n_blocks.  The sequence depends only on n_blocks and dense.
+ * when cap is 0) and returns the number of launches, or -1 for invalid
+ * arguments.  in_place says whether the call will have y == x.
  */
-int32_t dynconv_stack_launch_names(int32_t n_blocks, int32_t dense, const char **names,
-                                   int32_t cap);
+int32_t dynconv_stack_launch_names(dynconv_shape s, const dynconv_block *blks, int32_t n_blocks,
+                                   dynconv_dtype dt, int32_t flags, int32_t in_place,
+                                   const char **names, int32_t cap);
 
 /*
  * dynconv_stack_forward with per-kernel timing: launch i of the sequence that
@@ -224,11 +243,12 @@ int32_t dynconv_stack_launch_names(int32_t n_blocks, int32_t dense, const char *
  * n_events must be at least 2 * count (else DYNCONV_ERR_ARG).  Results are
  * identical to dynconv_stack_forward.
  */
-dynconv_status dynconv_stack_forward_profiled(void *x_inout, dynconv_shape s, dynconv_dtype dt,
-                                              const dynconv_block *blks, int32_t n_blocks,
-                                              int32_t dense, uint8_t *masks, int32_t *counts,
-                                              void *ws, size_t ws_bytes, void *stream,
-                                              void *const *events, int32_t n_events);
+dynconv_status dynconv_stack_forward_profiled(const void *x, void *y, dynconv_shape s,
+                                              dynconv_dtype dt, const dynconv_block *blks,
+                                              int32_t n_blocks, int32_t flags, uint8_t *masks,
+                                              int32_t *counts, void *ws, size_t ws_bytes,
+                                              void *stream, void *const *events,
+                                              int32_t n_events);
 
 #ifdef __cplusplus
 }

@@ -9,6 +9,7 @@
 #include <string.h>
 
 #include "dynconv.h"
+#include "fused.h"
 #include "kernels.h"
 
 using namespace dynconv;
@@ -127,18 +128,19 @@ IndexScratch carve_index_scratch(void *ws, dynconv_shape s) {
     return sc;
 }
 
+// the expanded tensor: N*H*W rows plus one all-zero row for missing neighbours
 size_t hidden_bytes(dynconv_shape s, int E, dynconv_dtype dt) {
-    return align_up(static_cast<size_t>(positions(s)) * E * dtype_size(dt));
+    return align_up((static_cast<size_t>(positions(s)) + 1) * E * dtype_size(dt));
 }
 
 // ------------------------------------------------------------ launches
 template <typename T>
 void launch_mask(const void *x, dynconv_shape s, const float *w_m, float b_m, uint8_t *mask,
-                 float *logits, hipStream_t st, Marks &mk) {
+                 float *logits, int32_t *zero, int nzero, hipStream_t st, Marks &mk) {
     int64_t n = positions(s);
     int grid = static_cast<int>((n + kBlock - 1) / kBlock);
-    launch(mk, k_mask<T>, dim3(grid), dim3(kBlock), 0, st, static_cast<const T *>(x), n,
-                       s.c, w_m, b_m, mask, logits);
+    launch(mk, k_mask<T>, dim3(grid), dim3(kBlock), 0, st, static_cast<const T *>(x), n, s.c, w_m,
+           b_m, mask, logits, zero, nzero);
 }
 
 void launch_indices(const uint8_t *mask, dynconv_shape s, int dilate, const dynconv_indices *idx,
@@ -220,10 +222,59 @@ void launch_copy(const void *src, void *dst, size_t bytes, hipStream_t st) {
 }
 
 void dispatch_mask(dynconv_dtype dt, const void *x, dynconv_shape s, const float *w_m, float b_m,
-                   uint8_t *mask, float *logits, hipStream_t st, Marks &mk) {
-    if (dt == DYNCONV_F32) launch_mask<float>(x, s, w_m, b_m, mask, logits, st, mk);
-    else if (dt == DYNCONV_F16) launch_mask<half_t>(x, s, w_m, b_m, mask, logits, st, mk);
-    else launch_mask<bf16_t>(x, s, w_m, b_m, mask, logits, st, mk);
+                   uint8_t *mask, float *logits, hipStream_t st, Marks &mk, int32_t *zero = nullptr,
+                   int nzero = 0) {
+    if (dt == DYNCONV_F32) launch_mask<float>(x, s, w_m, b_m, mask, logits, zero, nzero, st, mk);
+    else if (dt == DYNCONV_F16) launch_mask<half_t>(x, s, w_m, b_m, mask, logits, zero, nzero, st, mk);
+    else launch_mask<bf16_t>(x, s, w_m, b_m, mask, logits, zero, nzero, st, mk);
+}
+
+// ------------------------------------------------------------ fused block
+// Band size of the one-launch block kernel: at most kFusedBandPos positions
+// (R*W) per workgroup.
+constexpr int kFusedBandPos = 256;
+
+template <typename T, bool DENSE, int MAXKS, int MAXMT, int MAXC>
+void launch_fused_k(const void *src, void *dst, dynconv_shape s, const dynconv_block *b,
+                    const uint8_t *mask_in, const dynconv_block *next, uint8_t *mask_next,
+                    int32_t *counts, hipStream_t st, Marks &mk) {
+    constexpr int MAXPOS = kFusedBandPos;
+    const int R = fused_rows(MAXPOS, s.w, s.h);
+    const int nbands = s.n * ((s.h + R - 1) / R);
+    const int grid = (nbands + 7) / 8 * 8;  // whole groups of 8 (one per XCD)
+    launch(mk, k_block_fused<T, DENSE, MAXKS, MAXMT, MAXC, MAXPOS>, dim3(grid), dim3(kBlock), 0, st,
+           static_cast<const T *>(src), static_cast<T *>(dst), s.n, s.h, s.w, s.c, b->c_hidden, R,
+           mask_in, static_cast<const T *>(b->w_expand), b->b_expand, b->act_expand,
+           static_cast<const T *>(b->w_dw), b->b_dw, b->act_dw,
+           static_cast<const T *>(b->w_project), b->b_project, b->act_project,
+           next ? next->w_mask : nullptr, next ? next->b_mask : 0.0f,
+           next ? mask_next : nullptr, counts);
+}
+
+template <typename T, bool DENSE>
+void launch_fused(const void *src, void *dst, dynconv_shape s, const dynconv_block *b,
+                  const uint8_t *mask_in, const dynconv_block *next, uint8_t *mask_next,
+                  int32_t *counts, hipStream_t st, Marks &mk) {
+    if constexpr (sizeof(T) == 4) {  // fp32: LDS holds at most 32 channels (use_fused)
+        launch_fused_k<T, DENSE, 1, 2, 32>(src, dst, s, b, mask_in, next, mask_next, counts, st, mk);
+    } else {
+        if (s.c <= 32)
+            launch_fused_k<T, DENSE, 1, 2, 32>(src, dst, s, b, mask_in, next, mask_next, counts, st, mk);
+        else
+            launch_fused_k<T, DENSE, 2, 4, 64>(src, dst, s, b, mask_in, next, mask_next, counts, st, mk);
+    }
+}
+
+void dispatch_fused(dynconv_dtype dt, bool dense, const void *src, void *dst, dynconv_shape s,
+                    const dynconv_block *b, const uint8_t *mask_in, const dynconv_block *next,
+                    uint8_t *mask_next, int32_t *counts, hipStream_t st, Marks &mk) {
+#define DC_FUSED(T)                                                                          \
+    (dense ? launch_fused<T, true>(src, dst, s, b, nullptr, nullptr, nullptr, nullptr, st, mk) \
+           : launch_fused<T, false>(src, dst, s, b, mask_in, next, mask_next, counts, st, mk))
+    if (dt == DYNCONV_F32) DC_FUSED(float);
+    else if (dt == DYNCONV_F16) DC_FUSED(half_t);
+    else DC_FUSED(bf16_t);
+#undef DC_FUSED
 }
 
 void dispatch_block(dynconv_dtype dt, const void *x, void *y, dynconv_shape s, const dynconv_block *b,
@@ -233,79 +284,145 @@ void dispatch_block(dynconv_dtype dt, const void *x, void *y, dynconv_shape s, c
     else launch_block<bf16_t>(x, y, s, b, idx, h1, st, mk);
 }
 
-// ------------------------------------------------------------ stack layout
+// ------------------------------------------------------------ stacks
+constexpr int32_t kStackDense = 1;
+constexpr int32_t kStackUnfused = 2;
+
+// The one-launch block kernel covers widths up to one wave and at most 64
+// channels (32 in fp32, whose slices and band rows fill the LDS at 32);
+// other shapes run the unfused kernel chain.
+bool use_fused(dynconv_shape s, dynconv_dtype dt, int32_t flags) {
+    const int cmax = (dt == DYNCONV_F32) ? 32 : kMaxFusedC;
+    return !(flags & kStackUnfused) && s.w <= kWave && s.c <= cmax;
+}
+
 struct StackLayout {
-    size_t masks, active, dilated, nbr, counts, scratch, hidden, total;
+    bool fused;
+    size_t masks, mask2, tbuf, active, dilated, nbr, counts, scratch, hidden, total;
 };
 
 StackLayout stack_layout(dynconv_shape s, const dynconv_block *blks, int32_t n_blocks,
-                         dynconv_dtype dt) {
-    StackLayout L;
+                         dynconv_dtype dt, int32_t flags) {
+    StackLayout L{};
+    L.fused = use_fused(s, dt, flags);
     size_t npos = static_cast<size_t>(positions(s));
-    int emax = 0;
-    for (int32_t b = 0; b < n_blocks; ++b)
-        if (blks[b].c_hidden > emax) emax = blks[b].c_hidden;
     size_t off = 0;
-    L.masks = off;   off += align_up(npos);
-    L.active = off;  off += align_up(4 * npos);
-    L.dilated = off; off += align_up(4 * npos);
-    L.nbr = off;     off += align_up(36 * npos);
-    L.counts = off;  off += align_up(8 * static_cast<size_t>(n_blocks));
-    L.scratch = off; off += index_scratch_bytes(s);
-    L.hidden = off;  off += hidden_bytes(s, emax, dt);
+    if (L.fused) {
+        L.tbuf = off;   off += align_up(npos * s.c * dtype_size(dt));
+        L.masks = off;  off += align_up(npos);
+        L.mask2 = off;  off += align_up(npos);
+        L.counts = off; off += align_up(8 * static_cast<size_t>(n_blocks));
+    } else {
+        int emax = 0;
+        for (int32_t b = 0; b < n_blocks; ++b)
+            if (blks[b].c_hidden > emax) emax = blks[b].c_hidden;
+        L.masks = off;   off += align_up(npos);
+        L.active = off;  off += align_up(4 * npos);
+        L.dilated = off; off += align_up(4 * npos);
+        L.nbr = off;     off += align_up(36 * npos);
+        L.counts = off;  off += align_up(8 * static_cast<size_t>(n_blocks));
+        L.scratch = off; off += index_scratch_bytes(s);
+        L.hidden = off;  off += hidden_bytes(s, emax, dt);
+    }
     L.total = off;
     return L;
 }
 
-// The stack sequence shared by dynconv_stack_forward and its profiled form.
-dynconv_status stack_checked(void *x_inout, dynconv_shape s, dynconv_dtype dt,
-                             const dynconv_block *blks, int32_t n_blocks, int32_t dense,
-                             StackLayout *L) {
-    if (!x_inout || !blks) return DYNCONV_ERR_NULL;
+dynconv_status stack_checked(const void *x, void *y, dynconv_shape s, dynconv_dtype dt,
+                             const dynconv_block *blks, int32_t n_blocks, int32_t flags) {
+    if (!x || !y || !blks) return DYNCONV_ERR_NULL;
     if (!dtype_ok(dt)) return DYNCONV_ERR_DTYPE;
     if (n_blocks < 1 || n_blocks > kMaxBlocks) return DYNCONV_ERR_ARG;
+    if (flags & ~(kStackDense | kStackUnfused)) return DYNCONV_ERR_ARG;
     if (dynconv_status st = check_shape(s, true)) return st;
     for (int32_t b = 0; b < n_blocks; ++b)
-        if (dynconv_status st = check_block(&blks[b], s, !dense)) return st;
-    if (!aligned16(x_inout)) return DYNCONV_ERR_ALIGN;
-    *L = stack_layout(s, blks, n_blocks, dt);
+        if (dynconv_status st = check_block(&blks[b], s, !(flags & kStackDense))) return st;
+    if (!aligned16(x) || !aligned16(y)) return DYNCONV_ERR_ALIGN;
+    size_t bytes = static_cast<size_t>(positions(s)) * s.c * dtype_size(dt);
+    if (x != y && ranges_overlap(x, bytes, y, bytes)) return DYNCONV_ERR_SHAPE;
     return DYNCONV_OK;
 }
 
-int32_t stack_launch_count(int32_t n_blocks, int32_t dense) {
-    return n_blocks * (dense ? 2 : 6);
-}
+// Walks the launch sequence of a stack.  With exec == false it only records
+// the kernel names (what dynconv_stack_launch_names reports).
+struct Plan {
+    bool exec;
+    const char **names;
+    int32_t cap;
+    int32_t count = 0;
+    bool note(const char *name) {
+        if (names && count < cap) names[count] = name;
+        ++count;
+        return exec;
+    }
+};
 
-void stack_enqueue(void *x_inout, dynconv_shape s, dynconv_dtype dt, const dynconv_block *blks,
-                   int32_t n_blocks, int32_t dense, uint8_t *masks, int32_t *counts, char *base,
-                   const StackLayout &L, hipStream_t st, Marks &mk) {
-    void *h1 = base + L.hidden;
-    if (dense) {
-        for (int32_t b = 0; b < n_blocks; ++b)
-            dispatch_block(dt, x_inout, x_inout, s, &blks[b], nullptr, h1, st, mk);
+void stack_walk(const void *x, void *y, dynconv_shape s, dynconv_dtype dt, const dynconv_block *blks,
+                int32_t n_blocks, int32_t flags, uint8_t *masks, int32_t *counts, char *base,
+                const StackLayout &L, hipStream_t st, Marks &mk, Plan &plan, bool in_place) {
+    const bool dense = flags & kStackDense;
+    const size_t npos = static_cast<size_t>(positions(s));
+    const size_t bytes = npos * s.c * dtype_size(dt);
+    int32_t *cnt_all = counts ? counts : reinterpret_cast<int32_t *>(base + L.counts);
+    if (L.fused) {
+        // Ping-pong between y and a scratch copy so that the last block writes y.
+        void *tb = base + L.tbuf;
+        const void *src = x;
+        if (in_place && (n_blocks % 2 == 1)) {
+            if (plan.note("k_copy16")) launch_copy(x, tb, bytes, st);  // keeps y free for block 0
+            src = tb;
+        }
+        auto mask_of = [&](int32_t b) -> uint8_t * {
+            if (masks) return masks + static_cast<size_t>(b) * npos;
+            return reinterpret_cast<uint8_t *>(base + ((b % 2) ? L.mask2 : L.masks));
+        };
+        if (!dense && plan.note("k_mask"))
+            dispatch_mask(dt, src, s, blks[0].w_mask, blks[0].b_mask, mask_of(0), nullptr, st, mk,
+                          cnt_all, 2 * n_blocks);
+        for (int32_t b = 0; b < n_blocks; ++b) {
+            void *dst = ((n_blocks - 1 - b) % 2 == 0) ? y : tb;
+            const dynconv_block *next = (b + 1 < n_blocks) ? &blks[b + 1] : nullptr;
+            if (plan.note("k_block_fused"))
+                dispatch_fused(dt, dense, src, dst, s, &blks[b], mask_of(b), next,
+                               next ? mask_of(b + 1) : nullptr, cnt_all + 2 * b, st, mk);
+            src = dst;
+        }
         return;
     }
-    size_t npos = static_cast<size_t>(positions(s));
+    // Unfused chain, in place on y.
+    if (!in_place && plan.note("k_copy16")) launch_copy(x, y, bytes, st);
+    void *h1 = base + L.hidden;
+    if (dense) {
+        for (int32_t b = 0; b < n_blocks; ++b) {
+            bool run = plan.note("k_expand");
+            plan.note("k_dw_project");
+            if (run) dispatch_block(dt, y, y, s, &blks[b], nullptr, h1, st, mk);
+        }
+        return;
+    }
     dynconv_indices idx;
     idx.active = reinterpret_cast<int32_t *>(base + L.active);
     idx.dilated = reinterpret_cast<int32_t *>(base + L.dilated);
     idx.nbr = reinterpret_cast<int32_t *>(base + L.nbr);
     idx.capacity = static_cast<int64_t>(npos);
-    int32_t *cnt_all = counts ? counts : reinterpret_cast<int32_t *>(base + L.counts);
     void *scratch = base + L.scratch;
     for (int32_t b = 0; b < n_blocks; ++b) {
         uint8_t *mask_b = masks ? masks + static_cast<size_t>(b) * npos
                                 : reinterpret_cast<uint8_t *>(base + L.masks);
         idx.counts = cnt_all + 2 * b;
-        dispatch_mask(dt, x_inout, s, blks[b].w_mask, blks[b].b_mask, mask_b, nullptr, st, mk);
-        launch_indices(mask_b, s, 1, &idx, scratch, st, mk);
-        dispatch_block(dt, x_inout, x_inout, s, &blks[b], &idx, h1, st, mk);
+        bool run = plan.note("k_mask");
+        plan.note("k_rowcount");
+        plan.note("k_rowscan");
+        plan.note("k_compact");
+        plan.note("k_expand");
+        plan.note("k_dw_project");
+        if (run) {
+            dispatch_mask(dt, y, s, blks[b].w_mask, blks[b].b_mask, mask_b, nullptr, st, mk);
+            launch_indices(mask_b, s, 1, &idx, scratch, st, mk);
+            dispatch_block(dt, y, y, s, &blks[b], &idx, h1, st, mk);
+        }
     }
 }
-
-const char *const kSparseNames[6] = {"k_mask", "k_rowcount", "k_rowscan", "k_compact", "k_expand",
-                                     "k_dw_project"};
-const char *const kDenseNames[2] = {"k_expand", "k_dw_project"};
 
 }  // namespace
 
@@ -394,61 +511,73 @@ dynconv_status dynconv_block_forward(const void *x, void *y, dynconv_shape s, dy
 }
 
 size_t dynconv_stack_workspace_bytes(dynconv_shape s, const dynconv_block *blks, int32_t n_blocks,
-                                     dynconv_dtype dt) {
+                                     dynconv_dtype dt, int32_t flags) {
     if (!blks || n_blocks < 1 || n_blocks > kMaxBlocks || !dtype_ok(dt) ||
         check_shape(s, true) != DYNCONV_OK)
         return 0;
-    return stack_layout(s, blks, n_blocks, dt).total;
+    return stack_layout(s, blks, n_blocks, dt, flags).total;
 }
 
-dynconv_status dynconv_stack_forward(void *x_inout, dynconv_shape s, dynconv_dtype dt,
-                                     const dynconv_block *blks, int32_t n_blocks, int32_t dense,
+static dynconv_status stack_common(const void *x, void *y, dynconv_shape s, dynconv_dtype dt,
+                                   const dynconv_block *blks, int32_t n_blocks, int32_t flags,
+                                   uint8_t *masks, int32_t *counts, void *ws, size_t ws_bytes,
+                                   void *stream, void *const *events, int32_t n_events,
+                                   bool profiled) {
+    if (dynconv_status st = stack_checked(x, y, s, dt, blks, n_blocks, flags)) return st;
+    StackLayout L = stack_layout(s, blks, n_blocks, dt, flags);
+    if (!ws || ws_bytes < L.total) return DYNCONV_ERR_WORKSPACE;
+    if (!aligned16(ws)) return DYNCONV_ERR_ALIGN;
+    const bool in_place = x == y;
+    Marks mk;
+    if (profiled) {
+        Plan count{false, nullptr, 0};
+        StackLayout L0 = L;
+        Marks none;
+        stack_walk(x, y, s, dt, blks, n_blocks, flags, masks, counts, nullptr, L0, nullptr, none,
+                   count, in_place);
+        if (!events) return DYNCONV_ERR_NULL;
+        if (n_events < 2 * count.count) return DYNCONV_ERR_ARG;
+        for (int32_t i = 0; i < 2 * count.count; ++i)
+            if (!events[i]) return DYNCONV_ERR_NULL;
+        mk.ev = reinterpret_cast<hipEvent_t const *>(events);
+        mk.n = 2 * count.count;
+    }
+    (void)hipGetLastError();
+    Plan run{true, nullptr, 0};
+    stack_walk(x, y, s, dt, blks, n_blocks, flags, masks, counts, static_cast<char *>(ws), L,
+               static_cast<hipStream_t>(stream), mk, run, in_place);
+    return launch_status();
+}
+
+dynconv_status dynconv_stack_forward(const void *x, void *y, dynconv_shape s, dynconv_dtype dt,
+                                     const dynconv_block *blks, int32_t n_blocks, int32_t flags,
                                      uint8_t *masks, int32_t *counts, void *ws, size_t ws_bytes,
                                      void *stream) {
-    StackLayout L;
-    if (dynconv_status st = stack_checked(x_inout, s, dt, blks, n_blocks, dense, &L)) return st;
-    if (!ws || ws_bytes < L.total) return DYNCONV_ERR_WORKSPACE;
-    if (!aligned16(ws)) return DYNCONV_ERR_ALIGN;
-    (void)hipGetLastError();
-    Marks mk;
-    stack_enqueue(x_inout, s, dt, blks, n_blocks, dense, masks, counts, static_cast<char *>(ws), L,
-                  static_cast<hipStream_t>(stream), mk);
-    return launch_status();
+    return stack_common(x, y, s, dt, blks, n_blocks, flags, masks, counts, ws, ws_bytes, stream,
+                        nullptr, 0, false);
 }
 
-int32_t dynconv_stack_launch_names(int32_t n_blocks, int32_t dense, const char **names,
-                                   int32_t cap) {
-    if (n_blocks < 1 || n_blocks > kMaxBlocks) return -1;
-    int32_t per = dense ? 2 : 6;
-    int32_t total = stack_launch_count(n_blocks, dense);
-    if (names)
-        for (int32_t i = 0; i < total && i < cap; ++i)
-            names[i] = dense ? kDenseNames[i % per] : kSparseNames[i % per];
-    return total;
+int32_t dynconv_stack_launch_names(dynconv_shape s, const dynconv_block *blks, int32_t n_blocks,
+                                   dynconv_dtype dt, int32_t flags, int32_t in_place,
+                                   const char **names, int32_t cap) {
+    if (!blks || n_blocks < 1 || n_blocks > kMaxBlocks || !dtype_ok(dt) ||
+        check_shape(s, true) != DYNCONV_OK || (flags & ~(kStackDense | kStackUnfused)))
+        return -1;
+    StackLayout L = stack_layout(s, blks, n_blocks, dt, flags);
+    Plan plan{false, names, names ? cap : 0};
+    Marks none;
+    stack_walk(nullptr, nullptr, s, dt, blks, n_blocks, flags, nullptr, nullptr, nullptr, L,
+               nullptr, none, plan, in_place != 0);
+    return plan.count;
 }
 
-dynconv_status dynconv_stack_forward_profiled(void *x_inout, dynconv_shape s, dynconv_dtype dt,
-                                              const dynconv_block *blks, int32_t n_blocks,
-                                              int32_t dense, uint8_t *masks, int32_t *counts,
-                                              void *ws, size_t ws_bytes, void *stream,
-                                              void *const *events, int32_t n_events) {
-    StackLayout L;
-    if (dynconv_status st = stack_checked(x_inout, s, dt, blks, n_blocks, dense, &L)) return st;
-    if (!ws || ws_bytes < L.total) return DYNCONV_ERR_WORKSPACE;
-    if (!aligned16(ws)) return DYNCONV_ERR_ALIGN;
-    if (!events) return DYNCONV_ERR_NULL;
-    int32_t total = stack_launch_count(n_blocks, dense);
-    if (n_events < 2 * total) return DYNCONV_ERR_ARG;
-    for (int32_t i = 0; i < 2 * total; ++i)
-        if (!events[i]) return DYNCONV_ERR_NULL;
-    hipStream_t st = static_cast<hipStream_t>(stream);
-    (void)hipGetLastError();
-    Marks mk;
-    mk.ev = reinterpret_cast<hipEvent_t const *>(events);
-    mk.n = 2 * total;
-    stack_enqueue(x_inout, s, dt, blks, n_blocks, dense, masks, counts, static_cast<char *>(ws), L,
-                  st, mk);
-    return launch_status();
+dynconv_status dynconv_stack_forward_profiled(const void *x, void *y, dynconv_shape s,
+                                              dynconv_dtype dt, const dynconv_block *blks,
+                                              int32_t n_blocks, int32_t flags, uint8_t *masks,
+                                              int32_t *counts, void *ws, size_t ws_bytes,
+                                              void *stream, void *const *events, int32_t n_events) {
+    return stack_common(x, y, s, dt, blks, n_blocks, flags, masks, counts, ws, ws_bytes, stream,
+                        events, n_events, true);
 }
 
 }  // extern "C"

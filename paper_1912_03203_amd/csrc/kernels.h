@@ -40,6 +40,15 @@ constexpr int kMaxSeg = 64;          // image width limit: 64 segments of 64 col
 template <typename T> struct io;
 
 template <> struct io<float> {
+    struct vec8 {
+        float v[8];
+        __device__ __forceinline__ float operator[](int i) const { return v[i]; }
+    };
+    static __device__ __forceinline__ vec8 raw8(const float *p) {
+        vec8 r;
+        load8(p, r.v);
+        return r;
+    }
     static __device__ __forceinline__ void load8(const float *p, float v[8]) {
         float4 a = *reinterpret_cast<const float4 *>(p);
         float4 b = *reinterpret_cast<const float4 *>(p + 4);
@@ -56,6 +65,10 @@ template <> struct io<float> {
 };
 
 template <> struct io<half_t> {
+    typedef half8 vec8;  // 8 values packed in 4 registers
+    static __device__ __forceinline__ vec8 raw8(const half_t *p) {
+        return *reinterpret_cast<const half8 *>(p);
+    }
     static __device__ __forceinline__ void load8(const half_t *p, float v[8]) {
         half8 h = *reinterpret_cast<const half8 *>(p);
 #pragma unroll
@@ -75,6 +88,10 @@ template <> struct io<half_t> {
 };
 
 template <> struct io<bf16_t> {
+    typedef bf16x8 vec8;
+    static __device__ __forceinline__ vec8 raw8(const bf16_t *p) {
+        return *reinterpret_cast<const bf16x8 *>(p);
+    }
     static __device__ __forceinline__ void load8(const bf16_t *p, float v[8]) {
         bf16x8 h = *reinterpret_cast<const bf16x8 *>(p);
 #pragma unroll
@@ -167,13 +184,15 @@ template <> struct mma<float> {
     }
 };
 
+// Activation as one clamp: kind 0 none, 1 ReLU, 2 ReLU6.  act_lo / act_hi
+// are uniform, so activate() is a single branch-free v_med3.
+__device__ __forceinline__ float act_lo(int kind) { return kind == 0 ? -__builtin_huge_valf() : 0.0f; }
+__device__ __forceinline__ float act_hi(int kind) { return kind == 2 ? 6.0f : __builtin_huge_valf(); }
+__device__ __forceinline__ float clamp_act(float v, float lo, float hi) {
+    return __builtin_amdgcn_fmed3f(v, lo, hi);
+}
 __device__ __forceinline__ float activate(float v, int kind) {
-    // kind: 0 none, 1 ReLU, 2 ReLU6 (uniform across the wave)
-    if (kind != 0) {
-        v = fmaxf(v, 0.0f);
-        if (kind == 2) v = fminf(v, 6.0f);
-    }
-    return v;
+    return clamp_act(v, act_lo(kind), act_hi(kind));
 }
 
 // ------------------------------------------------------------------- K1 mask
@@ -182,8 +201,12 @@ __device__ __forceinline__ float activate(float v, int kind) {
 template <typename T>
 __global__ void __launch_bounds__(kBlock)
 k_mask(const T *__restrict__ x, int64_t npix, int C, const float *__restrict__ w_m, float b_m,
-       uint8_t *__restrict__ mask, float *__restrict__ logits) {
+       uint8_t *__restrict__ mask, float *__restrict__ logits, int32_t *__restrict__ zero,
+       int nzero) {
     int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    // optional: clear a small counter array for the kernels that follow
+    if (zero && blockIdx.x == 0)
+        for (int z = threadIdx.x; z < nzero; z += kBlock) zero[z] = 0;
     if (i >= npix) return;
     const T *row = x + i * C;
     float acc = 0.0f;
@@ -377,6 +400,10 @@ k_expand(const T *__restrict__ x, int C, int E, const T *__restrict__ w1,
     const int64_t ntiles = (nrows + 15) / 16;
     const int nks = (C + 31) / 32;
     const int nmt = E / 16;
+    // row dense_rows (one past the capacity) stays zero: the depthwise reads it
+    // for neighbours outside the image or the dilated list
+    if (blockIdx.x == 0)
+        for (int e = threadIdx.x; e < E; e += kBlock) h1[dense_rows * E + e] = static_cast<T>(0.0f);
     for (int64_t t = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + wave; t < ntiles;
          t += static_cast<int64_t>(gridDim.x) * kWavesPerBlock) {
         const int64_t j = t * 16 + r;
@@ -389,21 +416,23 @@ k_expand(const T *__restrict__ x, int C, int E, const T *__restrict__ w1,
             b[ks] = (ks < nks && valid && c0 < C) ? M::load(x + pix * C + c0) : M::zero();
         }
         for (int mt = 0; mt < nmt; ++mt) {
-            floatx4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
             const int e = mt * 16 + r;
+            const int e0 = mt * 16 + 4 * g;
+            floatx4 acc = {b1[e0], b1[e0 + 1], b1[e0 + 2], b1[e0 + 3]};  // bias first
+            // Every MFMA is issued unconditionally (slices past C get zero
+            // fragments): a branch around an MFMA whose result is read at the
+            // join has been compiled without the wait states the read needs.
 #pragma unroll
             for (int ks = 0; ks < MAXKS; ++ks) {
-                if (ks < nks) {
-                    const int c0 = ks * 32 + g * 8;
-                    typename M::frag a = (c0 < C) ? M::load(w1 + static_cast<int64_t>(e) * C + c0) : M::zero();
-                    acc = M::run(a, b[ks], acc);
-                }
+                const int c0 = ks * 32 + g * 8;
+                typename M::frag a = (ks < nks && c0 < C)
+                    ? M::load(w1 + static_cast<int64_t>(e) * C + c0) : M::zero();
+                acc = M::run(a, b[ks], acc);
             }
             if (valid) {
-                const int e0 = mt * 16 + 4 * g;
                 float o[4];
 #pragma unroll
-                for (int v = 0; v < 4; ++v) o[v] = activate(acc[v] + b1[e0 + v], act1);
+                for (int v = 0; v < 4; ++v) o[v] = activate(acc[v], act1);
                 io<T>::store4(h1 + j * E + e0, o);
             }
         }
@@ -414,7 +443,8 @@ k_expand(const T *__restrict__ x, int C, int E, const T *__restrict__ w1,
 // Each wave owns tiles of 16 active rows.  Lane (r, g) computes the depthwise
 // output of row r for the 8 hidden channels it supplies to the projection's B
 // operand: 9 taps, each a 16-byte load of an expanded row found through the
-// neighbour table (missing neighbours contribute 0), fp32 accumulation with the
+// neighbour table (missing neighbours read the all-zero row N*H*W of the
+// expanded tensor, so the loads carry no branch), fp32 accumulation with the
 // folded depthwise weights staged transposed in LDS, bias, activation, rounding
 // to the storage type.  The projection (F^T = W3 H2^T) accumulates over the
 // hidden channels on the matrix cores; the epilogue adds bias and the identity
@@ -457,16 +487,23 @@ k_dw_project(const T *__restrict__ h1, const T *x, T *y, int N, int H, int W, in
             for (int k = 0; k < 9; ++k) {
                 const int dh = k / 3 - 1, dw = k % 3 - 1;
                 const bool in = valid && hh0 + dh >= 0 && hh0 + dh < H && ww0 + dw >= 0 && ww0 + dw < W;
-                nb[k] = in ? static_cast<int32_t>(pix + dh * W + dw) : -1;
+                nb[k] = in ? static_cast<int32_t>(pix + dh * W + dw) : static_cast<int32_t>(npos);
             }
         } else {
             pix = valid ? static_cast<int64_t>(act_list[p]) : 0;
 #pragma unroll
-            for (int k = 0; k < 9; ++k) nb[k] = valid ? nbr[p * 9 + k] : -1;
+            for (int k = 0; k < 9; ++k) {
+                const int32_t q = valid ? nbr[p * 9 + k] : -1;
+                nb[k] = (q >= 0) ? q : static_cast<int32_t>(npos);  // missing: the zero row
+            }
         }
-        floatx4 acc[MAXMT];
+        floatx4 acc[MAXMT];  // projection bias first
 #pragma unroll
-        for (int mt = 0; mt < MAXMT; ++mt) acc[mt] = floatx4{0.0f, 0.0f, 0.0f, 0.0f};
+        for (int mt = 0; mt < MAXMT; ++mt) {
+            const int c0 = mt * 16 + 4 * g;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) acc[mt][v] = (mt < nmt && c0 < C) ? b3[c0 + v] : 0.0f;
+        }
 
         for (int ks = 0; ks < nks; ++ks) {
             const int e0 = ks * 32 + g * 8;
@@ -475,30 +512,27 @@ k_dw_project(const T *__restrict__ h1, const T *x, T *y, int N, int H, int W, in
 #pragma unroll
             for (int u = 0; u < 8; ++u) hv[u] = 0.0f;
             if (ein && valid) {
-                float s[8];
+                float s[8];  // depthwise bias first, then the taps in order
 #pragma unroll
-                for (int u = 0; u < 8; ++u) s[u] = 0.0f;
+                for (int u = 0; u < 8; ++u) s[u] = lds[9 * E + e0 + u];
 #pragma unroll
-                for (int k = 0; k < 9; ++k) {
-                    if (nb[k] >= 0) {
-                        float v[8];
-                        io<T>::load8(h1 + static_cast<int64_t>(nb[k]) * E + e0, v);
-                        const float *wk = lds + k * E + e0;
+                for (int k = 0; k < 9; ++k) {  // branch free: missing taps read zeros
+                    float v[8];
+                    io<T>::load8(h1 + static_cast<int64_t>(nb[k]) * E + e0, v);
+                    const float *wk = lds + k * E + e0;
 #pragma unroll
-                        for (int u = 0; u < 8; ++u) s[u] = __builtin_fmaf(wk[u], v[u], s[u]);
-                    }
+                    for (int u = 0; u < 8; ++u) s[u] = __builtin_fmaf(wk[u], v[u], s[u]);
                 }
 #pragma unroll
-                for (int u = 0; u < 8; ++u) hv[u] = activate(s[u] + lds[9 * E + e0 + u], act2);
+                for (int u = 0; u < 8; ++u) hv[u] = activate(s[u], act2);
             }
             const typename M::frag bf = M::pack(hv);
 #pragma unroll
-            for (int mt = 0; mt < MAXMT; ++mt) {
-                if (mt < nmt) {
-                    const int c = mt * 16 + r;
-                    typename M::frag a = (ein && c < C) ? M::load(w3 + static_cast<int64_t>(c) * E + e0) : M::zero();
-                    acc[mt] = M::run(a, bf, acc[mt]);
-                }
+            for (int mt = 0; mt < MAXMT; ++mt) {  // unconditional MFMAs, as in k_expand
+                const int c = mt * 16 + r;
+                typename M::frag a = (mt < nmt && ein && c < C)
+                    ? M::load(w3 + static_cast<int64_t>(c) * E + e0) : M::zero();
+                acc[mt] = M::run(a, bf, acc[mt]);
             }
         }
         if (valid) {
@@ -509,7 +543,7 @@ k_dw_project(const T *__restrict__ h1, const T *x, T *y, int N, int H, int W, in
                     float xv[4], o[4];
                     io<T>::load4(x + pix * C + c0, xv);
 #pragma unroll
-                    for (int v = 0; v < 4; ++v) o[v] = xv[v] + activate(acc[mt][v] + b3[c0 + v], act3);
+                    for (int v = 0; v < 4; ++v) o[v] = xv[v] + activate(acc[mt][v], act3);
                     io<T>::store4(y + pix * C + c0, o);
                 }
             }

@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libdynconv.so")
 
 F32, F16, BF16 = 0, 1, 2
 ACT_NONE, ACT_RELU, ACT_RELU6 = 0, 1, 2
+STACK_DENSE, STACK_UNFUSED = 1, 2
 
 _TORCH_DTYPE = {F32: torch.float32, F16: torch.float16, BF16: torch.bfloat16}
 _CODE = {torch.float32: F32, torch.float16: F16, torch.bfloat16: BF16}
@@ -84,16 +85,18 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.dynconv_block_forward.argtypes = [vp, vp, Shape, ctypes.c_int, ctypes.POINTER(Block),
                                           ctypes.POINTER(Indices), vp, sz, vp]
     lib.dynconv_block_forward.restype = ctypes.c_int
-    lib.dynconv_stack_workspace_bytes.argtypes = [Shape, ctypes.POINTER(Block), i32, ctypes.c_int]
+    lib.dynconv_stack_workspace_bytes.argtypes = [Shape, ctypes.POINTER(Block), i32, ctypes.c_int,
+                                                  i32]
     lib.dynconv_stack_workspace_bytes.restype = sz
-    lib.dynconv_stack_forward.argtypes = [vp, Shape, ctypes.c_int, ctypes.POINTER(Block), i32, i32,
-                                          vp, vp, vp, sz, vp]
+    lib.dynconv_stack_forward.argtypes = [vp, vp, Shape, ctypes.c_int, ctypes.POINTER(Block), i32,
+                                          i32, vp, vp, vp, sz, vp]
     lib.dynconv_stack_forward.restype = ctypes.c_int
-    lib.dynconv_stack_launch_names.argtypes = [i32, i32, ctypes.POINTER(ctypes.c_char_p), i32]
+    lib.dynconv_stack_launch_names.argtypes = [Shape, ctypes.POINTER(Block), i32, ctypes.c_int, i32,
+                                               i32, ctypes.POINTER(ctypes.c_char_p), i32]
     lib.dynconv_stack_launch_names.restype = i32
-    lib.dynconv_stack_forward_profiled.argtypes = [vp, Shape, ctypes.c_int, ctypes.POINTER(Block),
-                                                   i32, i32, vp, vp, vp, sz, vp,
-                                                   ctypes.POINTER(ctypes.c_void_p), i32]
+    lib.dynconv_stack_forward_profiled.argtypes = [vp, vp, Shape, ctypes.c_int,
+                                                   ctypes.POINTER(Block), i32, i32, vp, vp, vp, sz,
+                                                   vp, ctypes.POINTER(ctypes.c_void_p), i32]
     lib.dynconv_stack_forward_profiled.restype = ctypes.c_int
     _lib = lib
     return lib
@@ -231,25 +234,27 @@ def _blocks_array(blocks):
     return arr
 
 
-def stack_workspace_bytes(shape: Shape, blocks, dtype) -> int:
+def stack_workspace_bytes(shape: Shape, blocks, dtype, flags=0) -> int:
     arr = _blocks_array(blocks)
-    return load().dynconv_stack_workspace_bytes(shape, arr, len(blocks), dtype_code(dtype))
+    return load().dynconv_stack_workspace_bytes(shape, arr, len(blocks), dtype_code(dtype), flags)
 
 
 class Stack:
-    """A prepared stack call: the block array and pointers are marshalled once,
-    so repeated launches (e.g. inside a timed loop or a graph capture) cost a
-    single ctypes call."""
+    """A prepared stack call y = blocks(x): the block array and pointers are
+    marshalled once, so repeated launches (a timed loop, a graph capture) cost
+    a single ctypes call.  y may be x (in place)."""
 
-    def __init__(self, x: torch.Tensor, blocks, dense: bool, masks=None, counts=None, ws=None):
+    def __init__(self, x: torch.Tensor, y: torch.Tensor, blocks, flags=0, masks=None, counts=None,
+                 ws=None):
         self.lib = load()
-        self.x = x
+        self.x, self.y = x, y
         self.blocks = list(blocks)
         self.arr = _blocks_array(self.blocks)
         self.shape = shape_of(x)
         self.dtype = dtype_code(x.dtype)
+        self.flags = int(flags)
         need = self.lib.dynconv_stack_workspace_bytes(self.shape, self.arr, len(self.blocks),
-                                                      self.dtype)
+                                                      self.dtype, self.flags)
         if need == 0:
             raise DynconvError("dynconv_stack_workspace_bytes rejected the stack")
         if ws is None:
@@ -257,39 +262,36 @@ class Stack:
         self.ws = ws
         self.masks = masks
         self.counts = counts
-        self.dense = 1 if dense else 0
+
+    def launch_names(self):
+        lib = self.lib
+        args = (self.shape, self.arr, len(self.blocks), self.dtype, self.flags,
+                1 if self.x.data_ptr() == self.y.data_ptr() else 0)
+        total = lib.dynconv_stack_launch_names(*args, None, 0)
+        if total < 0:
+            raise DynconvError("dynconv_stack_launch_names rejected the stack")
+        names = (ctypes.c_char_p * total)()
+        lib.dynconv_stack_launch_names(*args, names, total)
+        return [n.decode() for n in names]
+
+    def _args(self, stream):
+        return (_ptr(self.x), _ptr(self.y), self.shape, self.dtype, self.arr, len(self.blocks),
+                self.flags, _ptr(self.masks), _ptr(self.counts), _ptr(self.ws),
+                self.ws.numel() * self.ws.element_size(), _stream(stream))
 
     def __call__(self, stream=None):
-        _check(self.lib.dynconv_stack_forward(_ptr(self.x), self.shape, self.dtype, self.arr,
-                                              len(self.blocks), self.dense, _ptr(self.masks),
-                                              _ptr(self.counts), _ptr(self.ws),
-                                              self.ws.numel() * self.ws.element_size(),
-                                              _stream(stream)),
-               "dynconv_stack_forward")
-        return self.x
+        _check(self.lib.dynconv_stack_forward(*self._args(stream)), "dynconv_stack_forward")
+        return self.y
 
     def profiled(self, events, stream=None):
         """Same call, with launch i timed by the raw HIP events
         (events[2i], events[2i+1]); len(events) >= 2 * number of launches."""
         arr = (ctypes.c_void_p * len(events))(*events)
-        _check(self.lib.dynconv_stack_forward_profiled(
-            _ptr(self.x), self.shape, self.dtype, self.arr, len(self.blocks), self.dense,
-            _ptr(self.masks), _ptr(self.counts), _ptr(self.ws),
-            self.ws.numel() * self.ws.element_size(), _stream(stream), arr, len(events)),
-            "dynconv_stack_forward_profiled")
-        return self.x
+        _check(self.lib.dynconv_stack_forward_profiled(*self._args(stream), arr, len(events)),
+               "dynconv_stack_forward_profiled")
+        return self.y
 
 
-def stack_launch_names(n_blocks: int, dense: bool):
-    lib = load()
-    total = lib.dynconv_stack_launch_names(n_blocks, 1 if dense else 0, None, 0)
-    if total < 0:
-        raise DynconvError("invalid block count %d" % n_blocks)
-    arr = (ctypes.c_char_p * total)()
-    lib.dynconv_stack_launch_names(n_blocks, 1 if dense else 0, arr, total)
-    return [a.decode() for a in arr]
-
-
-def stack_forward(x: torch.Tensor, blocks, dense=False, masks=None, counts=None, ws=None,
-                  stream=None):
-    return Stack(x, blocks, dense, masks, counts, ws)(stream)
+def stack_forward(x: torch.Tensor, y: torch.Tensor, blocks, flags=0, masks=None, counts=None,
+                  ws=None, stream=None):
+    return Stack(x, y, blocks, flags, masks, counts, ws)(stream)

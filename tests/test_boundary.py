@@ -98,7 +98,8 @@ def test_block_validation(lib):
     s = dc.Shape(2, 8, 8, 32)
     b = fake_block()
     need = lib.dynconv_block_workspace_bytes(s, ctypes.byref(b), 1)
-    assert need == 2 * 8 * 8 * 192 * 2  # hidden rows x channels x fp16, already 256-aligned
+    # hidden tensor: N*H*W rows plus one zero row, x 192 channels x fp16, 256-aligned
+    assert need == (2 * 8 * 8 * 192 * 2 + 192 * 2 + 255) // 256 * 256
     f = lib.dynconv_block_forward
 
     def call(x=FAKE, y=FAKE, shape=s, dt=1, blk=b, idx=None, ws=FAKE, nbytes=need):
@@ -125,22 +126,59 @@ def test_block_validation(lib):
 def test_stack_validation(lib):
     s = dc.Shape(4, 16, 16, 32)
     blocks = (dc.Block * 3)(fake_block(), fake_block(E=96), fake_block())
-    need = lib.dynconv_stack_workspace_bytes(s, blocks, 3, 1)
     npos = 4 * 16 * 16
     rows = 4 * 16
 
     def up(v):
         return (v + 255) // 256 * 256
 
-    expect = (npos + 4 * npos + 4 * npos + 36 * npos + up(8 * 3) + up(8 * rows)
-              + up(8 * (rows + 1)) + npos * 192 * 2)
-    assert need == expect
+    # one-launch blocks: ping-pong copy of x, two masks, counts
+    fused = lib.dynconv_stack_workspace_bytes(s, blocks, 3, 1, 0)
+    assert fused == up(npos * 32 * 2) + 2 * up(npos) + up(8 * 3)
+    # kernel chain: mask, lists, counts, row scratch, hidden tensor of the widest block
+    need = lib.dynconv_stack_workspace_bytes(s, blocks, 3, 1, 2)
+    assert need == (npos + 4 * npos + 4 * npos + 36 * npos + up(8 * 3) + up(8 * rows)
+                    + up(8 * (rows + 1)) + up((npos + 1) * 192 * 2))
+    # widths beyond one wave always take the kernel chain
+    wide = dc.Shape(1, 4, 100, 32)
+    assert lib.dynconv_stack_workspace_bytes(wide, blocks, 3, 1, 0) == \
+        lib.dynconv_stack_workspace_bytes(wide, blocks, 3, 1, 2)
     f = lib.dynconv_stack_forward
-    assert f(None, s, 1, blocks, 3, 0, None, None, FAKE, need, None) == ERR_NULL
-    assert f(FAKE, s, 1, blocks, 0, 0, None, None, FAKE, need, None) == ERR_ARG
-    assert f(FAKE, s, 1, blocks, 1025, 0, None, None, FAKE, need, None) == ERR_ARG
-    assert f(FAKE, s, 1, blocks, 3, 0, None, None, FAKE, need - 1, None) == ERR_WORKSPACE
+    assert f(None, FAKE, s, 1, blocks, 3, 0, None, None, FAKE, need, None) == ERR_NULL
+    assert f(FAKE, None, s, 1, blocks, 3, 0, None, None, FAKE, need, None) == ERR_NULL
+    assert f(FAKE, FAKE, s, 1, blocks, 0, 0, None, None, FAKE, need, None) == ERR_ARG
+    assert f(FAKE, FAKE, s, 1, blocks, 1025, 0, None, None, FAKE, need, None) == ERR_ARG
+    assert f(FAKE, FAKE, s, 1, blocks, 3, 4, None, None, FAKE, need, None) == ERR_ARG
+    assert f(FAKE, FAKE, s, 1, blocks, 3, 2, None, None, FAKE, need - 1, None) == ERR_WORKSPACE
+    assert f(FAKE, FAKE, s, 1, blocks, 3, 0, None, None, FAKE, fused - 1, None) == ERR_WORKSPACE
+    assert f(FAKE, FAKE + 64, s, 1, blocks, 3, 0, None, None, FAKE, fused, None) == ERR_SHAPE
     nomask = (dc.Block * 1)(fake_block(w_mask=None))
-    need1 = lib.dynconv_stack_workspace_bytes(s, nomask, 1, 1)
-    assert f(FAKE, s, 1, nomask, 1, 0, None, None, FAKE, need1, None) == ERR_NULL
-    assert lib.dynconv_stack_workspace_bytes(s, blocks, 0, 1) == 0
+    need1 = lib.dynconv_stack_workspace_bytes(s, nomask, 1, 1, 0)
+    assert f(FAKE, FAKE, s, 1, nomask, 1, 0, None, None, FAKE, need1, None) == ERR_NULL
+    assert lib.dynconv_stack_workspace_bytes(s, blocks, 0, 1, 0) == 0
+    pf = lib.dynconv_stack_forward_profiled
+    ev = (ctypes.c_void_p * 8)(*([FAKE] * 8))
+    # 1 mask launch + 3 block launches need 8 events
+    assert pf(FAKE, FAKE, s, 1, blocks, 3, 0, None, None, FAKE, fused, None, ev, 7) == ERR_ARG
+    assert pf(FAKE, FAKE, s, 1, blocks, 3, 0, None, None, FAKE, fused, None, None, 8) == ERR_NULL
+
+
+def test_stack_launch_plans(lib):
+    s = dc.Shape(32, 64, 64, 32)
+    arr = (dc.Block * 8)(*([fake_block()] * 8))
+
+    def names(flags, in_place, shape=s, n=8):
+        total = lib.dynconv_stack_launch_names(shape, arr, n, 1, flags, in_place, None, 0)
+        out = (ctypes.c_char_p * total)()
+        lib.dynconv_stack_launch_names(shape, arr, n, 1, flags, in_place, out, total)
+        return [x.decode() for x in out]
+
+    assert names(0, 0) == ["k_mask"] + ["k_block_fused"] * 8
+    assert names(1, 1) == ["k_block_fused"] * 8
+    assert names(0, 1, n=3) == ["k_copy16", "k_mask"] + ["k_block_fused"] * 3
+    assert names(2, 1) == ["k_mask", "k_rowcount", "k_rowscan", "k_compact", "k_expand",
+                           "k_dw_project"] * 8
+    assert names(3, 0) == ["k_copy16"] + ["k_expand", "k_dw_project"] * 8
+    assert names(0, 1, shape=dc.Shape(2, 8, 65, 32))[:7] == [
+        "k_mask", "k_rowcount", "k_rowscan", "k_compact", "k_expand", "k_dw_project", "k_mask"]
+    assert lib.dynconv_stack_launch_names(s, arr, 0, 1, 0, 0, None, 0) == -1

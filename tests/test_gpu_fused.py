@@ -1,0 +1,166 @@
+"""Parity of the one-launch block kernel (the stack's execution for widths up
+to 64 and at most 64 channels) with the CPU oracle, and its agreement with the
+multi-kernel chain.  Same tolerances as the per-block calls: masks and counts
+bit-exact, outputs within 1e-5 (fp32) / 2e-2 (fp16, bf16) normwise, inactive
+positions untouched."""
+import numpy as np
+import pytest
+import torch
+
+from paper_1912_03203_amd import dynconv as dc
+from paper_1912_03203_amd import inputs
+from tests import util
+from tests.test_gpu_parity import DEV, check_block_output, host, log, oracle_stack, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _lib():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    dc.load()
+
+
+def run_stack(x_np, blocks_np, biases, dtype, flags=0, in_place=False):
+    dt = dc.NAME_TO_DTYPE[dtype]
+    bw = [dc.BlockWeights.from_arrays(w, dt, b_mask=b) for w, b in zip(blocks_np, biases)]
+    x = to_dev(x_np, dtype)
+    n, h, w, _ = x.shape
+    nb = len(bw)
+    masks = torch.full((nb, n * h * w), 7, dtype=torch.uint8, device=DEV)
+    counts = torch.full((nb, 2), -5, dtype=torch.int32, device=DEV)
+    y = x if in_place else torch.full_like(x, float("nan"))
+    stack = dc.Stack(x, y, bw, flags=flags, masks=masks, counts=counts)
+    stack()
+    torch.cuda.synchronize()
+    if not in_place:
+        assert host(x).tobytes() == np.asarray(x_np, np.float32).tobytes()  # input untouched
+    return {"y": y, "masks": masks, "counts": counts, "names": stack.launch_names()}
+
+
+FUSED_CASES = [
+    # name, dtype, (N, H, W, C, E), density, seed
+    ("fp32_parity_block", "f32", (1, 32, 32, 32, 192), 0.5, 0),
+    ("stage2_d0.10", "f16", (32, 56, 56, 24, 144), 0.10, 0),
+    ("stage2_d0.25", "f16", (32, 56, 56, 24, 144), 0.25, 0),
+    ("stage2_d0.50", "f16", (32, 56, 56, 24, 144), 0.50, 1),
+    ("stage2_d0.90", "f16", (32, 56, 56, 24, 144), 0.90, 3),
+    ("pose_d0.25", "f16", (32, 64, 64, 32, 192), 0.25, 2),
+    ("ragged_bf16_c40", "bf16", (3, 7, 11, 40, 80), 0.3, 4),
+    ("c64_e384_f16", "f16", (2, 9, 64, 64, 384), 0.4, 5),
+    ("width1_f16", "f16", (2, 300, 1, 16, 48), 0.3, 6),
+    ("width7_f32", "f32", (3, 20, 7, 8, 16), 0.6, 7),
+    ("height1_bf16", "bf16", (5, 1, 50, 24, 96), 0.5, 8),
+]
+
+
+@pytest.mark.parametrize("case", FUSED_CASES, ids=[c[0] for c in FUSED_CASES])
+def test_fused_block_parity(case):
+    name, dtype, (N, H, W, C, E), density, seed = case
+    log("fused block %s" % name)
+    rng = inputs.rng_for(2000 + seed)
+    x = inputs.round_to_storage(inputs.blob_features(rng, N, H, W, C), dtype)
+    wts = inputs.block_weights(rng, C, E, dtype=dtype)
+    o = util.oracle_calibrated_block(x, wts, density, dtype)
+    g = run_stack(x, [wts], [o["b_m"]], dtype)
+    assert g["names"] == ["k_mask", "k_block_fused"]
+    assert g["masks"][0].cpu().numpy().tobytes() == o["G"].tobytes()
+    assert tuple(int(v) for v in g["counts"][0].cpu()) == (o["A"].size, o["D"].size)
+    check_block_output(host(g["y"]), x, o["y"], o["G"], dtype)
+
+
+@pytest.mark.parametrize("bias", [-np.inf, np.inf])
+def test_fused_empty_and_full_masks(bias):
+    rng = inputs.rng_for(9)
+    N, H, W, C, E = 4, 12, 40, 24, 144
+    x = inputs.round_to_storage(inputs.blob_features(rng, N, H, W, C), "f16")
+    wts = inputs.block_weights(rng, C, E, dtype="f16")
+    g = run_stack(x, [wts], [bias], "f16")
+    P, Pd = (int(v) for v in g["counts"][0].cpu())
+    if bias < 0:
+        assert (P, Pd) == (0, 0)
+        assert host(g["y"]).tobytes() == x.tobytes()
+    else:
+        assert (P, Pd) == (N * H * W, N * H * W)
+        dense = run_stack(x, [wts], [0.0], "f16", flags=dc.STACK_DENSE)
+        assert torch.equal(g["y"], dense["y"])
+
+
+@pytest.mark.parametrize("dtype,shape,nb", [("f16", (32, 64, 64, 32, 192), 8),
+                                            ("bf16", (4, 20, 28, 48, 96), 3),
+                                            ("f32", (2, 16, 16, 16, 96), 2)])
+def test_fused_stack_matches_kernel_chain(dtype, shape, nb):
+    """One-launch blocks (out of place and in place, which takes the extra copy
+    for an odd block count) and the multi-kernel chain give the same masks,
+    counts and outputs bit for bit: same operand fragments, same summation
+    order, same roundings."""
+    N, H, W, C, E = shape
+    rng = inputs.rng_for(31)
+    x = inputs.round_to_storage(inputs.blob_features(rng, N, H, W, C), dtype)
+    blocks = [inputs.block_weights(rng, C, E, dtype=dtype) for _ in range(nb)]
+    _, s = util.oracle_mask_chunked(util.nchw(x), blocks[0]["w_m"], 0.0)
+    b0 = inputs.percentile_bias(s, 0.3)
+    biases = [b0] + [b0 * 0.5] * (nb - 1)  # later densities drift; not calibrated here
+    ref = run_stack(x, blocks, biases, dtype, flags=dc.STACK_UNFUSED, in_place=True)
+    assert ref["names"][0] == "k_mask" and "k_block_fused" not in ref["names"]
+    for in_place in (False, True):
+        g = run_stack(x, blocks, biases, dtype, in_place=in_place)
+        assert "k_block_fused" in g["names"]
+        assert torch.equal(g["masks"], ref["masks"])
+        assert torch.equal(g["counts"], ref["counts"])
+        assert torch.equal(g["y"], ref["y"])
+
+
+def test_fused_pose_stack_teacher_forced_and_end_to_end():
+    """Every block of the 8-block pose stack as a one-launch block fed the
+    oracle's input; then the whole fused stack end to end."""
+    wl = inputs.WORKLOADS["pose_stack8_64x64x32_f16"]
+    x0, blocks, _ = inputs.make_block_inputs(wl, 0)
+    xs, outs = oracle_stack(x0, blocks, 0.25, wl.dtype)
+    for b in range(wl.blocks):
+        g = run_stack(xs[b], [blocks[b]], [outs[b]["b_m"]], wl.dtype)
+        assert g["masks"][0].cpu().numpy().tobytes() == outs[b]["G"].tobytes()
+        check_block_output(host(g["y"]), xs[b], outs[b]["y"], outs[b]["G"], wl.dtype)
+    g = run_stack(x0, blocks, [o["b_m"] for o in outs], wl.dtype)
+    flips = [int((g["masks"][b].cpu().numpy() != outs[b]["G"]).sum()) for b in range(wl.blocks)]
+    log("  fused end-to-end mask flips per block: %s" % flips)
+    assert flips[0] == 0
+    assert sum(flips) <= 1e-3 * wl.nhw * wl.blocks
+
+
+def test_fused_stack_in_graph_replays():
+    """The stack captured in a HIP graph: several replays, with eager work and
+    synchronisation between them, each equal to the eager result."""
+    wl = inputs.WORKLOADS["pose_stack8_64x64x32_f16"]
+    x0, blocks, _ = inputs.make_block_inputs(wl, 3)
+    dt = dc.NAME_TO_DTYPE[wl.dtype]
+    _, s = util.oracle_mask_chunked(util.nchw(x0), blocks[0]["w_m"], 0.0)
+    b0 = float(inputs.percentile_bias(s, 0.25))
+    bw = [dc.BlockWeights.from_arrays(w, dt, b_mask=b0) for w in blocks]
+    x = to_dev(x0, wl.dtype)
+    counts = torch.zeros(wl.blocks, 2, dtype=torch.int32, device=DEV)
+    for flags in (0, dc.STACK_DENSE):
+        y = torch.empty_like(x)
+        stack = dc.Stack(x, y, bw, flags=flags, counts=counts)
+        stack()
+        torch.cuda.synchronize()
+        eager = y.clone()
+        eager_counts = counts.clone()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            stack()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            stack()
+        for _ in range(4):
+            y.fill_(0)
+            torch.cuda.synchronize()
+            graph.replay()
+            torch.cuda.synchronize()
+            assert torch.equal(y, eager)
+            if flags == 0:
+                assert torch.equal(counts, eager_counts)

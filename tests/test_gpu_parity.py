@@ -289,7 +289,7 @@ def test_stack_call_matches_block_calls(pose_stack):
     masks = torch.zeros(wl.blocks, wl.nhw, dtype=torch.uint8, device=DEV)
     counts = torch.zeros(wl.blocks, 2, dtype=torch.int32, device=DEV)
     y_stack = x_dev.clone()
-    dc.stack_forward(y_stack, bw, dense=False, masks=masks, counts=counts)
+    dc.stack_forward(y_stack, y_stack, bw, flags=dc.STACK_UNFUSED, masks=masks, counts=counts)
     y_seq = x_dev.clone()
     shape = dc.shape_of(x_dev)
     for b, blk in enumerate(bw):
@@ -337,13 +337,19 @@ def test_dense_stack_matches_oracle():
     x0 = x0[:4]  # four images: the dense stack has no batch-wide statistic
     dt = dc.NAME_TO_DTYPE[wl.dtype]
     bw = [dc.BlockWeights.from_arrays(w, dt) for w in blocks]
-    x_dev = to_dev(x0, wl.dtype)
-    dc.stack_forward(x_dev, bw, dense=True)
-    torch.cuda.synchronize()
     xb = x0
     for wts in blocks:
         y = util.nhwc(util.oracle_block_dense_chunked(util.nchw(xb).astype(np.float64), wts, None))
         xb = inputs.round_to_storage(y, wl.dtype)
-    err = util.normwise(host(x_dev), xb)
-    log("  dense stack normwise err %.3e" % err)
-    assert err <= util.TOL[wl.dtype]
+    outs = []
+    for flags in (dc.STACK_DENSE, dc.STACK_DENSE | dc.STACK_UNFUSED):
+        x_dev = to_dev(x0, wl.dtype)
+        y_dev = torch.empty_like(x_dev)
+        dc.stack_forward(x_dev, y_dev, bw, flags=flags)
+        torch.cuda.synchronize()
+        assert host(x_dev).tobytes() == x0.tobytes()  # input untouched
+        err = util.normwise(host(y_dev), xb)
+        log("  dense stack (flags %d) normwise err %.3e" % (flags, err))
+        assert err <= util.TOL[wl.dtype]
+        outs.append(y_dev)
+    assert torch.equal(outs[0], outs[1])  # one-launch and multi-kernel blocks agree bitwise
