@@ -171,7 +171,7 @@ def profile_kernels(dc, torch, runner, steps):
             for k, v in out.items()}, per_launch
 
 
-def algorithmic_bytes(name, dense, s, C, E, npos, rows, P, Pd, last=False):
+def algorithmic_bytes(name, dense, s, C, E, npos, rows, P, Pd, last=False, bands=0):
     """Bytes one launch must move at minimum (each input read once, each output
     written once); P, Pd are the block's active and dilated counts.  The
     one-launch block reads x and writes y at every position (its output is a
@@ -182,6 +182,8 @@ def algorithmic_bytes(name, dense, s, C, E, npos, rows, P, Pd, last=False):
         return 2 * npos * C * s + masks + weights
     if name == "k_copy16":
         return 2 * npos * C * s
+    if name == "k_band_counts":  # per-band (P, P_d) pairs in, the block's sums out
+        return 8 * bands + 8
     if dense:
         if name == "k_expand":
             return npos * C * s + npos * E * s + E * C * s + 4 * E
@@ -325,12 +327,15 @@ def main():
     prof_dn, _ = profile_kernels(dc, torch, dn, args.profile_steps)
     s = 2 if wl.dtype != "f32" else 4
     rows = wl.n * wl.h
+    band_rows = max(1, min(256 // wl.w, 62, wl.h))  # rows per band of the one-launch block
+    bands = wl.n * -(-wl.h // band_rows)
 
     def avg_bytes(name, dense):
         if dense:
             return float(algorithmic_bytes(name, True, s, wl.c, wl.e, npos, rows, npos, npos))
         per = [algorithmic_bytes(name, False, s, wl.c, wl.e, npos, rows, int(P), int(Pd),
-                                 last=(b == wl.blocks - 1)) for b, (P, Pd) in enumerate(counts)]
+                                 last=(b == wl.blocks - 1), bands=bands)
+               for b, (P, Pd) in enumerate(counts)]
         return float(np.mean(per))
 
     for prof, dense in ((prof_sp, False), (prof_dn, True)):

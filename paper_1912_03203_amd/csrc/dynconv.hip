@@ -136,11 +136,11 @@ size_t hidden_bytes(dynconv_shape s, int E, dynconv_dtype dt) {
 // ------------------------------------------------------------ launches
 template <typename T>
 void launch_mask(const void *x, dynconv_shape s, const float *w_m, float b_m, uint8_t *mask,
-                 float *logits, int32_t *zero, int nzero, hipStream_t st, Marks &mk) {
+                 float *logits, hipStream_t st, Marks &mk) {
     int64_t n = positions(s);
     int grid = static_cast<int>((n + kBlock - 1) / kBlock);
     launch(mk, k_mask<T>, dim3(grid), dim3(kBlock), 0, st, static_cast<const T *>(x), n, s.c, w_m,
-           b_m, mask, logits, zero, nzero);
+           b_m, mask, logits);
 }
 
 void launch_indices(const uint8_t *mask, dynconv_shape s, int dilate, const dynconv_indices *idx,
@@ -222,17 +222,24 @@ void launch_copy(const void *src, void *dst, size_t bytes, hipStream_t st) {
 }
 
 void dispatch_mask(dynconv_dtype dt, const void *x, dynconv_shape s, const float *w_m, float b_m,
-                   uint8_t *mask, float *logits, hipStream_t st, Marks &mk, int32_t *zero = nullptr,
-                   int nzero = 0) {
-    if (dt == DYNCONV_F32) launch_mask<float>(x, s, w_m, b_m, mask, logits, zero, nzero, st, mk);
-    else if (dt == DYNCONV_F16) launch_mask<half_t>(x, s, w_m, b_m, mask, logits, zero, nzero, st, mk);
-    else launch_mask<bf16_t>(x, s, w_m, b_m, mask, logits, zero, nzero, st, mk);
+                   uint8_t *mask, float *logits, hipStream_t st, Marks &mk) {
+    if (dt == DYNCONV_F32) launch_mask<float>(x, s, w_m, b_m, mask, logits, st, mk);
+    else if (dt == DYNCONV_F16) launch_mask<half_t>(x, s, w_m, b_m, mask, logits, st, mk);
+    else launch_mask<bf16_t>(x, s, w_m, b_m, mask, logits, st, mk);
 }
 
 // ------------------------------------------------------------ fused block
 // Band size of the one-launch block kernel: at most kFusedBandPos positions
-// (R*W) per workgroup.
+// (R*W) per workgroup of kFusedWaves waves, register budget for
+// kFusedWavesPerSimd waves per SIMD.
 constexpr int kFusedBandPos = 256;
+constexpr int kFusedWaves = 4;
+constexpr int kFusedWavesPerSimd = 2;
+
+int fused_band_count(dynconv_shape s) {
+    const int R = fused_rows(kFusedBandPos, s.w, s.h);
+    return s.n * ((s.h + R - 1) / R);
+}
 
 template <typename T, bool DENSE, int MAXKS, int MAXMT, int MAXC>
 void launch_fused_k(const void *src, void *dst, dynconv_shape s, const dynconv_block *b,
@@ -240,9 +247,10 @@ void launch_fused_k(const void *src, void *dst, dynconv_shape s, const dynconv_b
                     int32_t *counts, hipStream_t st, Marks &mk) {
     constexpr int MAXPOS = kFusedBandPos;
     const int R = fused_rows(MAXPOS, s.w, s.h);
-    const int nbands = s.n * ((s.h + R - 1) / R);
+    const int nbands = fused_band_count(s);
     const int grid = (nbands + 7) / 8 * 8;  // whole groups of 8 (one per XCD)
-    launch(mk, k_block_fused<T, DENSE, MAXKS, MAXMT, MAXC, MAXPOS>, dim3(grid), dim3(kBlock), 0, st,
+    launch(mk, k_block_fused<T, DENSE, MAXKS, MAXMT, MAXC, MAXPOS, kFusedWaves, kFusedWavesPerSimd>,
+           dim3(grid), dim3(kFusedWaves * kWave), 0, st,
            static_cast<const T *>(src), static_cast<T *>(dst), s.n, s.h, s.w, s.c, b->c_hidden, R,
            mask_in, static_cast<const T *>(b->w_expand), b->b_expand, b->act_expand,
            static_cast<const T *>(b->w_dw), b->b_dw, b->act_dw,
@@ -298,7 +306,7 @@ bool use_fused(dynconv_shape s, dynconv_dtype dt, int32_t flags) {
 
 struct StackLayout {
     bool fused;
-    size_t masks, mask2, tbuf, active, dilated, nbr, counts, scratch, hidden, total;
+    size_t masks, mask2, tbuf, active, dilated, nbr, counts, bands, scratch, hidden, total;
 };
 
 StackLayout stack_layout(dynconv_shape s, const dynconv_block *blks, int32_t n_blocks,
@@ -312,6 +320,7 @@ StackLayout stack_layout(dynconv_shape s, const dynconv_block *blks, int32_t n_b
         L.masks = off;  off += align_up(npos);
         L.mask2 = off;  off += align_up(npos);
         L.counts = off; off += align_up(8 * static_cast<size_t>(n_blocks));
+        L.bands = off;  off += align_up(8 * static_cast<size_t>(n_blocks) * fused_band_count(s));
     } else {
         int emax = 0;
         for (int32_t b = 0; b < n_blocks; ++b)
@@ -376,17 +385,22 @@ void stack_walk(const void *x, void *y, dynconv_shape s, dynconv_dtype dt, const
             if (masks) return masks + static_cast<size_t>(b) * npos;
             return reinterpret_cast<uint8_t *>(base + ((b % 2) ? L.mask2 : L.masks));
         };
+        const int nbands = fused_band_count(s);
+        int32_t *band_counts = reinterpret_cast<int32_t *>(base + L.bands);
         if (!dense && plan.note("k_mask"))
-            dispatch_mask(dt, src, s, blks[0].w_mask, blks[0].b_mask, mask_of(0), nullptr, st, mk,
-                          cnt_all, 2 * n_blocks);
+            dispatch_mask(dt, src, s, blks[0].w_mask, blks[0].b_mask, mask_of(0), nullptr, st, mk);
         for (int32_t b = 0; b < n_blocks; ++b) {
             void *dst = ((n_blocks - 1 - b) % 2 == 0) ? y : tb;
             const dynconv_block *next = (b + 1 < n_blocks) ? &blks[b + 1] : nullptr;
             if (plan.note("k_block_fused"))
                 dispatch_fused(dt, dense, src, dst, s, &blks[b], mask_of(b), next,
-                               next ? mask_of(b + 1) : nullptr, cnt_all + 2 * b, st, mk);
+                               next ? mask_of(b + 1) : nullptr,
+                               band_counts + static_cast<size_t>(2) * nbands * b, st, mk);
             src = dst;
         }
+        if (!dense && plan.note("k_band_counts"))
+            launch(mk, k_band_counts, dim3(n_blocks), dim3(kBlock), 0, st,
+                   static_cast<const int32_t *>(band_counts), nbands, cnt_all);
         return;
     }
     // Unfused chain, in place on y.

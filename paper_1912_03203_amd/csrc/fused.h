@@ -26,8 +26,8 @@
 // The arithmetic of every output element is the one of the kernel chain
 // (k_expand, k_dw_project): same operand fragments, same summation order.
 // Input and output must be different buffers: neighbouring bands read the
-// rows next to this band as their halo.  The active and dilated counts are
-// added to counts[0..1] with integer atomics (order independent).
+// rows next to this band as their halo.  Band i writes its active and
+// dilated counts to band_counts[2i], [2i+1]; k_band_counts sums them.
 #pragma once
 
 #include "kernels.h"
@@ -57,18 +57,19 @@ __host__ __device__ constexpr int fused_max_region(int maxpos) {
     return m;
 }
 
-template <int MAXPOS>
+template <int MAXPOS, int NW>
 struct BandShape {
+    static constexpr int kThreads = NW * kWave;                // workgroup size
     static constexpr int kMaxNeed = MAXPOS + 2 * kWave;       // region positions (R+2)*W
     static constexpr int kMaxRegion = fused_max_region(MAXPOS);
-    static constexpr int kNeedTiles = (kMaxNeed / 16 + kWavesPerBlock - 1) / kWavesPerBlock;
-    static constexpr int kActTiles = (MAXPOS / 16 + kWavesPerBlock - 1) / kWavesPerBlock;
+    static constexpr int kNeedTiles = (kMaxNeed / 16 + NW - 1) / NW;   // 16-row tiles per wave
+    static constexpr int kActTiles = (MAXPOS / 16 + NW - 1) / NW;
 };
 
 // Weights of one 32-channel slice of the hidden layer.
 template <typename T, int MAXC>
 struct SliceWeights {
-    alignas(16) T w1[kChunk][MAXC];        // expansion rows e (slice-local), c fastest
+    alignas(16) T w1[kChunk][MAXC + 8];    // expansion rows e (slice-local), c fastest, padded
     alignas(16) T w3[MAXC][kChunkPad];     // projection rows c, slice channels fastest
     alignas(16) T w2[9][kChunk];           // depthwise taps, transposed
     alignas(16) float b1[kChunk];
@@ -77,7 +78,7 @@ struct SliceWeights {
 
 template <typename T, int MAXC, int MAXPOS>
 struct FusedLds {
-    typedef BandShape<MAXPOS> B;
+    typedef BandShape<MAXPOS, 1> B;
     uint64_t nw[kFusedMaxRegionRows];   // dilated positions (of the band's actives) per region row
     uint64_t aw[kFusedMaxRegionRows];   // active positions (own rows only)
     uint64_t gw[kFusedMaxRegionRows];   // mask words of region rows (image rows h0-1+rr)
@@ -87,17 +88,18 @@ struct FusedLds {
     int16_t act[MAXPOS];
     alignas(16) float b3[MAXC];
     SliceWeights<T, MAXC> wt[2];        // double-buffered slice weights
-    alignas(16) T xs[B::kMaxNeed * MAXC];  // x of the region rows (rr*W + w); own rows become y
+    alignas(16) T xs[B::kMaxNeed][MAXC + 8];  // x of the region rows (rr*W + w), padded rows;
+                                              // the band's own rows become y
     alignas(16) T h1r[B::kMaxRegion][kChunkPad];  // the slice, zero-bordered region layout
 };
 
 // Cooperative global -> register -> LDS staging of one slice's weights: each
 // thread owns kStageSlots 16-byte pieces (zero beyond E).
-template <typename T, int MAXC>
+template <typename T, int MAXC, int NT>
 struct SliceStager {
     static constexpr int kPer16 = 16 / static_cast<int>(sizeof(T));
     static constexpr int kPieces = 2 * kChunk * MAXC / kPer16 + kChunk * 9 / kPer16 + 2 * kChunk / 4;
-    static constexpr int kStageSlots = (kPieces + kBlock - 1) / kBlock;
+    static constexpr int kStageSlots = (kPieces + NT - 1) / NT;
     uint4 v[kStageSlots];
     // piece index p enumerates, in order: w1 rows (32 x C), w3 rows (C x 32),
     // w2 (32 channels x 9 taps, read as [e][9]), b1, b2
@@ -108,7 +110,7 @@ struct SliceStager {
         const int e_base = ec * kChunk;
 #pragma unroll
         for (int sl = 0; sl < kStageSlots; ++sl) {
-            const int p = tid + sl * kBlock;
+            const int p = tid + sl * NT;
             uint4 val = make_uint4(0, 0, 0, 0);
             if (p < n1) {
                 const int e = p / (C / per16), c = (p % (C / per16)) * per16;
@@ -142,7 +144,7 @@ struct SliceStager {
         const int e_lim = E - ec * kChunk;
 #pragma unroll
         for (int sl = 0; sl < kStageSlots; ++sl) {
-            const int p = tid + sl * kBlock;
+            const int p = tid + sl * NT;
             if (p < n1) {
                 const int e = p / (C / per16), c = (p % (C / per16)) * per16;
                 *reinterpret_cast<uint4 *>(&dst.w1[e][c]) = v[sl];
@@ -168,18 +170,19 @@ struct SliceStager {
     }
 };
 
-template <typename T, bool DENSE, int MAXKS, int MAXMT, int MAXC, int MAXPOS>
-__global__ void __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(2)))
+template <typename T, bool DENSE, int MAXKS, int MAXMT, int MAXC, int MAXPOS, int NW, int WPE>
+__global__ void __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(WPE)))
 k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int W, int C, int E,
               int R, const uint8_t *__restrict__ mask_in,
               const T *__restrict__ w1, const float *__restrict__ b1, int act1,
               const T *__restrict__ w2, const float *__restrict__ b2, int act2,
               const T *__restrict__ w3, const float *__restrict__ b3, int act3,
               const float *__restrict__ wm_next, float bm_next, uint8_t *__restrict__ mask_next,
-              int32_t *__restrict__ counts) {
+              int32_t *__restrict__ band_counts) {
     typedef mma<T> M;
-    typedef BandShape<MAXPOS> BS;
+    typedef BandShape<MAXPOS, NW> BS;
     constexpr int kNeedTiles = BS::kNeedTiles, kActTiles = BS::kActTiles;
+    constexpr int NT = BS::kThreads;
     __shared__ FusedLds<T, MAXC, MAXPOS> L;
     const int tid = threadIdx.x;
     const int wave = tid / kWave, lane = tid % kWave;
@@ -208,25 +211,26 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
     // All of these only depend on the arguments, so their loads overlap:
     // the first slice's weights, the projection bias, and x of every region
     // row inside the image (rows h0-1 .. h0+R: one contiguous NHWC stretch).
-    SliceStager<T, MAXC> stage;
+    SliceStager<T, MAXC, NT> stage;
     stage.load(w1, w2, w3, b1, b2, C, E, 0, tid);
-    for (int c = tid; c < C; c += kBlock) L.b3[c] = b3[c];
+    for (int c = tid; c < C; c += NT) L.b3[c] = b3[c];
     {
         const int r_first = (h0 == 0) ? 1 : 0;          // region row of image row max(h0-1, 0)
         const int r_last = (h0 + rows_out < H) ? nreg - 1 : nreg - 2;
-        const int nvec = (r_last - r_first + 1) * W * C / per16;
+        const int vpr = C / per16;                      // 16-byte pieces per position
+        const int nvec = (r_last - r_first + 1) * W * vpr;
         const uint4 *src = reinterpret_cast<const uint4 *>(xin + (img + h0 - 1 + r_first) * W * C);
-        uint4 *dst = reinterpret_cast<uint4 *>(&L.xs[r_first * W * C]);
-        for (int i = tid; i < nvec; i += kBlock) dst[i] = src[i];
+        for (int i = tid; i < nvec; i += NT)
+            *reinterpret_cast<uint4 *>(&L.xs[r_first * W + i / vpr][(i % vpr) * per16]) = src[i];
     }
     {   // zero region: its border and out-of-image rows are never written again
         uint4 *z = reinterpret_cast<uint4 *>(&L.h1r[0][0]);
         constexpr int nz = BS::kMaxRegion * kChunkPad * static_cast<int>(sizeof(T)) / 16;
-        for (int i = tid; i < nz; i += kBlock) z[i] = make_uint4(0, 0, 0, 0);
+        for (int i = tid; i < nz; i += NT) z[i] = make_uint4(0, 0, 0, 0);
     }
 
     // ---- 1. mask words, dilation, lists
-    for (int rr = wave; rr < nreg; rr += kWavesPerBlock) {
+    for (int rr = wave; rr < nreg; rr += NW) {
         const int hh = h0 - 1 + rr;
         bool bit = false;
         if (hh >= 0 && hh < H && lane < W)
@@ -273,21 +277,20 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
             L.need_off[nreg] = sn;
             L.act_off[nreg] = sa;
         }
-        if (!DENSE && counts) {
+        if (!DENSE && band_counts) {
+            // this band's active and dilated counts (a plain store per band:
+            // atomics on one address from every XCD serialise)
             int pa = ca, pd = __popcll(dil_own);
             for (int off = 32; off > 0; off >>= 1) {
                 pa += __shfl_down(pa, off);
                 pd += __shfl_down(pd, off);
             }
-            if (lane == 0) {
-                atomicAdd(counts + 0, pa);
-                atomicAdd(counts + 1, pd);
-            }
+            if (lane == 0) *reinterpret_cast<int2 *>(band_counts + 2 * band) = make_int2(pa, pd);
         }
     }
     __syncthreads();
     const uint64_t lt = lanemask_lt(lane);
-    for (int rr = wave; rr < nreg; rr += kWavesPerBlock) {
+    for (int rr = wave; rr < nreg; rr += NW) {
         if (lane < W) {
             const uint64_t nwd = L.nw[rr], awd = L.aw[rr];
             const int16_t q = static_cast<int16_t>(rr * WP + lane + 1);
@@ -299,7 +302,7 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
     __syncthreads();
     const int n_need = L.need_off[nreg];
     const int n_act = L.act_off[nreg];
-    T *yrows = &L.xs[W * C];  // the band's own rows (region rows 1..rows_out)
+    T (*yrows)[MAXC + 8] = &L.xs[W];  // the band's own rows (region rows 1..rows_out)
 
     if (n_act > 0) {
         // region rows of this wave's need and active tiles: index into the
@@ -307,7 +310,7 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
         int nq[kNeedTiles], nx[kNeedTiles];
 #pragma unroll
         for (int j = 0; j < kNeedTiles; ++j) {
-            const int i = (wave + kWavesPerBlock * j) * 16 + r;
+            const int i = (wave + NW * j) * 16 + r;
             const int q = (i < n_need) ? static_cast<int>(L.need[i]) : -1;
             nq[j] = q;
             nx[j] = (q >= 0) ? (q / WP) * W + q % WP - 1 : W;  // past n_need: any row, never stored
@@ -315,7 +318,7 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
         int aq[kActTiles];
 #pragma unroll
         for (int j = 0; j < kActTiles; ++j) {
-            const int i = (wave + kWavesPerBlock * j) * 16 + r;
+            const int i = (wave + NW * j) * 16 + r;
             aq[j] = (i < n_act) ? static_cast<int>(L.act[i]) : -1;
         }
         floatx4 acc[kActTiles][MAXMT];
@@ -348,13 +351,13 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
             }
 #pragma unroll
             for (int j = 0; j < kNeedTiles; ++j) {
-                const int t = wave + kWavesPerBlock * j;
+                const int t = wave + NW * j;
                 if (t * 16 < n_need) {
                     typename M::frag bxs[MAXKS];
 #pragma unroll
                     for (int ks = 0; ks < MAXKS; ++ks) {
                         const int c0 = ks * 32 + g * 8;
-                        bxs[ks] = (c0 < C) ? M::load(&L.xs[nx[j] * C + c0]) : M::zero();
+                        bxs[ks] = (c0 < C) ? M::load(&L.xs[nx[j]][c0]) : M::zero();
                     }
 #pragma unroll
                     for (int m = 0; m < 2; ++m) {
@@ -391,7 +394,7 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
             const char *h1base = reinterpret_cast<const char *>(&L.h1r[0][8 * g]);
 #pragma unroll
             for (int j = 0; j < kActTiles; ++j) {
-                const int t = wave + kWavesPerBlock * j;
+                const int t = wave + NW * j;
                 if (t * 16 < n_act) {
                     float hv[8];
 #pragma unroll
@@ -430,10 +433,10 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
                     const int c0 = mt * 16 + 4 * g;
                     if (c0 < C) {
                         float xv[4], o[4];
-                        io<T>::load4(&yrows[q * C + c0], xv);
+                        io<T>::load4(&yrows[q][c0], xv);
 #pragma unroll
                         for (int v = 0; v < 4; ++v) o[v] = xv[v] + clamp_act(acc[j][mt][v], lo3, hi3);
-                        io<T>::store4(&yrows[q * C + c0], o);
+                        io<T>::store4(&yrows[q][c0], o);
                     }
                 }
             }
@@ -442,15 +445,16 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
     }
     // ---- 4b. store the band (inactive positions: x unchanged)
     {
-        const int nvec = rows_out * W * C / per16;
-        const uint4 *src = reinterpret_cast<const uint4 *>(yrows);
+        const int vpr = C / per16;
+        const int nvec = rows_out * W * vpr;
         uint4 *dst = reinterpret_cast<uint4 *>(yout + (img + h0) * W * C);
-        for (int i = tid; i < nvec; i += kBlock) dst[i] = src[i];
+        for (int i = tid; i < nvec; i += NT)
+            dst[i] = *reinterpret_cast<const uint4 *>(&yrows[i / vpr][(i % vpr) * per16]);
     }
     // ---- 4c. the next block's mask unit on the stored values
     if (mask_next) {
-        for (int q = tid; q < rows_out * W; q += kBlock) {
-            const T *row = &yrows[q * C];
+        for (int q = tid; q < rows_out * W; q += NT) {
+            const T *row = &yrows[q][0];
             float a = 0.0f;
             for (int c0 = 0; c0 < C; c0 += 8) {
                 float v[8];
@@ -461,6 +465,34 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
             const float m = a + bm_next;
             mask_next[(img + h0) * W + q] = (m > 0.0f) ? 1 : 0;
         }
+    }
+}
+
+// counts[2b], counts[2b+1] = sums of the per-band counts of block b
+// (one workgroup per block, fixed summation order).
+__global__ void __launch_bounds__(kBlock)
+k_band_counts(const int32_t *__restrict__ band_counts, int nbands, int32_t *__restrict__ counts) {
+    __shared__ int2 part[kBlock];
+    const int b = blockIdx.x;
+    const int2 *src = reinterpret_cast<const int2 *>(band_counts) + static_cast<int64_t>(b) * nbands;
+    int2 acc = make_int2(0, 0);
+    for (int i = threadIdx.x; i < nbands; i += kBlock) {
+        const int2 v = src[i];
+        acc.x += v.x;
+        acc.y += v.y;
+    }
+    part[threadIdx.x] = acc;
+    __syncthreads();
+    for (int off = kBlock / 2; off > 0; off >>= 1) {
+        if (threadIdx.x < off) {
+            part[threadIdx.x].x += part[threadIdx.x + off].x;
+            part[threadIdx.x].y += part[threadIdx.x + off].y;
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        counts[2 * b] = part[0].x;
+        counts[2 * b + 1] = part[0].y;
     }
 }
 

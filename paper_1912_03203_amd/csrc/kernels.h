@@ -201,12 +201,8 @@ __device__ __forceinline__ float activate(float v, int kind) {
 template <typename T>
 __global__ void __launch_bounds__(kBlock)
 k_mask(const T *__restrict__ x, int64_t npix, int C, const float *__restrict__ w_m, float b_m,
-       uint8_t *__restrict__ mask, float *__restrict__ logits, int32_t *__restrict__ zero,
-       int nzero) {
+       uint8_t *__restrict__ mask, float *__restrict__ logits) {
     int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
-    // optional: clear a small counter array for the kernels that follow
-    if (zero && blockIdx.x == 0)
-        for (int z = threadIdx.x; z < nzero; z += kBlock) zero[z] = 0;
     if (i >= npix) return;
     const T *row = x + i * C;
     float acc = 0.0f;

@@ -132,9 +132,10 @@ def test_stack_validation(lib):
     def up(v):
         return (v + 255) // 256 * 256
 
-    # one-launch blocks: ping-pong copy of x, two masks, counts
+    # one-launch blocks: ping-pong copy of x, two masks, counts, per-band counts
+    # (bands of up to 256 positions: 16 rows of 16, one band per image)
     fused = lib.dynconv_stack_workspace_bytes(s, blocks, 3, 1, 0)
-    assert fused == up(npos * 32 * 2) + 2 * up(npos) + up(8 * 3)
+    assert fused == up(npos * 32 * 2) + 2 * up(npos) + up(8 * 3) + up(8 * 3 * 4)
     # kernel chain: mask, lists, counts, row scratch, hidden tensor of the widest block
     need = lib.dynconv_stack_workspace_bytes(s, blocks, 3, 1, 2)
     assert need == (npos + 4 * npos + 4 * npos + 36 * npos + up(8 * 3) + up(8 * rows)
@@ -158,8 +159,8 @@ def test_stack_validation(lib):
     assert lib.dynconv_stack_workspace_bytes(s, blocks, 0, 1, 0) == 0
     pf = lib.dynconv_stack_forward_profiled
     ev = (ctypes.c_void_p * 8)(*([FAKE] * 8))
-    # 1 mask launch + 3 block launches need 8 events
-    assert pf(FAKE, FAKE, s, 1, blocks, 3, 0, None, None, FAKE, fused, None, ev, 7) == ERR_ARG
+    # 1 mask launch + 3 block launches + 1 count reduction need 10 events
+    assert pf(FAKE, FAKE, s, 1, blocks, 3, 0, None, None, FAKE, fused, None, ev, 8) == ERR_ARG
     assert pf(FAKE, FAKE, s, 1, blocks, 3, 0, None, None, FAKE, fused, None, None, 8) == ERR_NULL
 
 
@@ -173,9 +174,9 @@ def test_stack_launch_plans(lib):
         lib.dynconv_stack_launch_names(shape, arr, n, 1, flags, in_place, out, total)
         return [x.decode() for x in out]
 
-    assert names(0, 0) == ["k_mask"] + ["k_block_fused"] * 8
+    assert names(0, 0) == ["k_mask"] + ["k_block_fused"] * 8 + ["k_band_counts"]
     assert names(1, 1) == ["k_block_fused"] * 8
-    assert names(0, 1, n=3) == ["k_copy16", "k_mask"] + ["k_block_fused"] * 3
+    assert names(0, 1, n=3) == ["k_copy16", "k_mask"] + ["k_block_fused"] * 3 + ["k_band_counts"]
     assert names(2, 1) == ["k_mask", "k_rowcount", "k_rowscan", "k_compact", "k_expand",
                            "k_dw_project"] * 8
     assert names(3, 0) == ["k_copy16"] + ["k_expand", "k_dw_project"] * 8
