@@ -42,8 +42,44 @@ METRIC = "images/sec of sparse MobileNetV2 block stack at mask density 0.25; spe
 HBM_PEAK_GBS = 8000.0
 
 
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_block_fused_pose_stack8_traffic.md")
+KERNEL_SOURCES = ("paper_1912_03203_amd/csrc/fused.h", "paper_1912_03203_amd/csrc/kernels.h",
+                  "paper_1912_03203_amd/csrc/dynconv.hip")
+
+
 def log(msg):
     print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_source_sha1():
+    """Hash of the sources the kernels and their launch shapes are built from:
+    measured HBM traffic is only reported while it matches."""
+    import hashlib
+    h = hashlib.sha1()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload, density):
+    """HBM bytes per sparse one-launch block from the committed counter
+    summary, or None when it is absent, for another workload, or taken on
+    other kernel sources."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            text = f.read()
+    except OSError:
+        return None
+    tag = "<!-- traffic "
+    if tag not in text:
+        return None
+    rec = json.loads(text.split(tag, 1)[1].split(" -->", 1)[0])
+    if rec.get("source_sha1") != kernel_source_sha1():
+        return None
+    if rec.get("workload") != workload or abs(rec.get("density", -1) - density) > 1e-9:
+        return None
+    return rec
 
 
 # ------------------------------------------------------------------ HIP events
@@ -258,6 +294,105 @@ def density_sweep(dc, inputs, torch, steps, warmup, use_graph, flags):
     return {"workload": wl.name, "rows": rows}
 
 
+def traffic_pass(dc, torch, wl, x0, sparse_blocks, dense_blocks, reps=3):
+    """Launch sequence for one HBM-counter run (FETCH_SIZE or WRITE_SIZE):
+    (1) the kernel chain's plain copy (k_copy16, input -> output buffer, a
+    known number of bytes each way) as the counter's calibration, (2) the
+    sparse stack, (3) the dense stack; eager, synchronised after each."""
+    y = torch.empty_like(x0)
+    chain = dc.Stack(x0, y, sparse_blocks[:1], flags=dc.STACK_UNFUSED)
+    assert chain.launch_names()[0] == "k_copy16"
+    sp = Runner(dc, torch, x0, sparse_blocks, 0, False, wl.blocks)
+    dn = Runner(dc, torch, x0, dense_blocks, dc.STACK_DENSE, False, wl.blocks)
+    for run in (chain, sp.eager, dn.eager):
+        for _ in range(reps):
+            run()
+            torch.cuda.synchronize()
+    s = 2 if wl.dtype != "f32" else 4
+    print(json.dumps({"workload": wl.name, "copy_bytes": wl.nhw * wl.c * s, "reps": reps,
+                      "blocks": wl.blocks, "counts": sp.counts.cpu().numpy().tolist(),
+                      "source_sha1": kernel_source_sha1()}), flush=True)
+
+
+def _counter_rows(path):
+    import csv
+    with open(path) as f:
+        return list(csv.DictReader(f))
+
+
+def summarize_traffic(args):
+    """Per-dispatch FETCH_SIZE / WRITE_SIZE (KiB) of the copy, the sparse and
+    the dense one-launch block, each counter scaled by what it reads for the
+    copy of known size; written as the committed traffic summary."""
+    fetch_csv, write_csv = args.summarize_traffic
+    from paper_1912_03203_amd import inputs
+    wl = inputs.WORKLOADS[args.workload]
+    s = 2 if wl.dtype != "f32" else 4
+    copy_bytes = wl.nhw * wl.c * s
+    out = {}
+    for counter, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
+        groups = {"copy": [], "sparse": [], "dense": []}
+        for row in _counter_rows(path):
+            if row["Counter_Name"] != counter:
+                continue
+            name = row["Kernel_Name"]
+            v = float(row["Counter_Value"])
+            if "k_copy16" in name:
+                groups["copy"].append(v)
+            elif "k_block_fused" in name:
+                # template argument DENSE: mangled "...k_block_fusedI<type>Lb1E..."
+                # or demangled "k_block_fused<type, true, ...>"
+                if "<" in name:
+                    dense = name.split("<", 1)[1].split(",")[1].strip() == "true"
+                else:
+                    dense = "Lb1E" in name.split("k_block_fused", 1)[1][:12]
+                groups["dense" if dense else "sparse"].append(v)
+        if not all(groups.values()):
+            raise SystemExit("%s: missing dispatches in %s" % (counter, path))
+        out[counter] = {k: (float(np.mean(v)), len(v)) for k, v in groups.items()}
+    f_fetch = copy_bytes / (1024.0 * out["FETCH_SIZE"]["copy"][0])
+    f_write = copy_bytes / (1024.0 * out["WRITE_SIZE"]["copy"][0])
+    kib = {k: (out["FETCH_SIZE"][k][0], out["WRITE_SIZE"][k][0]) for k in ("copy", "sparse", "dense")}
+    by = {k: 1024.0 * (kib[k][0] * f_fetch + kib[k][1] * f_write) for k in ("sparse", "dense")}
+    rec = {"kernel": "k_block_fused", "workload": wl.name, "density": args.density,
+           "source_sha1": kernel_source_sha1(), "sparse_bytes": by["sparse"], "dense_bytes": by["dense"],
+           "fetch_scale": f_fetch, "write_scale": f_write}
+    lines = [
+        "# HBM traffic of k_block_fused: 8-block pose stack, 32 x 64x64x32, hidden 192, fp16, density %.2f"
+        % args.density,
+        "",
+        "Two counter runs of the same launch sequence (`bench.py --traffic-pass`: a plain copy of "
+        "%d bytes each way, the sparse stack, the dense stack, 3 times each). Each counter is scaled "
+        "by the ratio of the copy's known size to what the counter reads for it." % copy_bytes,
+        "",
+        "```",
+        "cd /tmp && export TMPDIR=/tmp && timeout -s KILL 120 rocprofv3 --pmc FETCH_SIZE --output-format csv "
+        "-d $REPO/gpurun_out/traffic_fetch -o run -- python3 $REPO/bench.py --traffic-pass",
+        "cd /tmp && export TMPDIR=/tmp && timeout -s KILL 120 rocprofv3 --pmc WRITE_SIZE --output-format csv "
+        "-d $REPO/gpurun_out/traffic_write -o run -- python3 $REPO/bench.py --traffic-pass",
+        "python3 bench.py --summarize-traffic gpurun_out/traffic_fetch/run_counter_collection.csv "
+        "gpurun_out/traffic_write/run_counter_collection.csv",
+        "```",
+        "",
+        "| dispatches | n | FETCH_SIZE KiB | WRITE_SIZE KiB | scaled bytes |",
+        "|---|---:|---:|---:|---:|",
+        "| k_copy16 (calibration) | %d | %.1f | %.1f | %d read + %d written |"
+        % (out["FETCH_SIZE"]["copy"][1], kib["copy"][0], kib["copy"][1], copy_bytes, copy_bytes),
+        "| k_block_fused sparse | %d | %.1f | %.1f | %.0f |"
+        % (out["FETCH_SIZE"]["sparse"][1], kib["sparse"][0], kib["sparse"][1], by["sparse"]),
+        "| k_block_fused dense | %d | %.1f | %.1f | %.0f |"
+        % (out["FETCH_SIZE"]["dense"][1], kib["dense"][0], kib["dense"][1], by["dense"]),
+        "",
+        "Scale factors: FETCH_SIZE x %.4f, WRITE_SIZE x %.4f." % (f_fetch, f_write),
+        "",
+        "<!-- traffic %s -->" % json.dumps(rec),
+        "",
+    ]
+    with open(TRAFFIC_FILE, "w") as f:
+        f.write("\n".join(lines))
+    print(json.dumps(rec))
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -271,7 +406,15 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--profile-steps", type=int, default=20)
+    ap.add_argument("--traffic-pass", action="store_true",
+                    help="untimed launches for an HBM-counter run: a plain copy of known size, "
+                         "then the sparse and the dense stack")
+    ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write the traffic summary from the counter CSVs of two --traffic-pass runs")
     args = ap.parse_args()
+    if args.summarize_traffic:
+        summarize_traffic(args)
+        return
 
     if args.gpus != 1:
         print("bench.py measures one GPU: the gated-block path runs on a single MI355X "
@@ -297,6 +440,9 @@ def main():
     x0 = torch.from_numpy(x_np).cuda().to(dt)
     sparse_blocks = calibrate(dc, inputs, torch, x0, blocks_np, dt, args.density)
     dense_blocks = [dc.BlockWeights.from_arrays(w, dt) for w in blocks_np]
+    if args.traffic_pass:
+        traffic_pass(dc, torch, wl, x0, sparse_blocks, dense_blocks)
+        return
 
     base_flags = dc.STACK_UNFUSED if args.unfused else 0
     sp = Runner(dc, torch, x0, sparse_blocks, base_flags, use_graph, wl.blocks)
@@ -327,8 +473,13 @@ def main():
     prof_dn, _ = profile_kernels(dc, torch, dn, args.profile_steps)
     s = 2 if wl.dtype != "f32" else 4
     rows = wl.n * wl.h
-    band_rows = max(1, min(256 // wl.w, 62, wl.h))  # rows per band of the one-launch block
-    bands = wl.n * -(-wl.h // band_rows)
+    # patches of the one-launch block: column strips of at most 32, R rows,
+    # at most `own` positions and `region` ring-included slots
+    own, region = (256, 340) if wl.c <= 32 else (128, 208)
+    strips = -(-wl.w // 32)
+    wu = -(-wl.w // strips)
+    pr = max(1, min(own // wu, region // (wu + 2) - 2, 50, wl.h))
+    bands = wl.n * -(-wl.h // pr) * -(-wl.w // wu)
 
     def avg_bytes(name, dense):
         if dense:
@@ -374,6 +525,10 @@ def main():
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
                      "algorithmic_bytes_per_launch": bytes_per_launch},
     }
+    rec = measured_traffic(wl.name, args.density) if dom == "k_block_fused" else None
+    if rec is not None:
+        result["roofline"]["traffic"] = rec["sparse_bytes"]
+        result["roofline"]["traffic_dense"] = rec["dense_bytes"]
     if not args.no_sweep:
         log("density sweep")
         result["sweep"] = density_sweep(dc, inputs, torch, min(args.steps, 100), min(args.warmup, 10),

@@ -202,14 +202,15 @@ size_t dynconv_stack_workspace_bytes(dynconv_shape s, const dynconv_block *blks,
  * With DYNCONV_STACK_DENSE the mask units are skipped and every block runs on
  * all positions (the baseline of Eq. 1).
  *
- * Execution: when s.w <= 64 and s.c <= 64 (s.c <= 32 for fp32) and
- * DYNCONV_STACK_UNFUSED is not set, each block is ONE kernel that builds the active and halo lists of a
- * band of image rows on chip (ballot ranks in raster order), gathers,
+ * Execution: when s.c <= 64 and DYNCONV_STACK_UNFUSED is not set, each
+ * block is ONE kernel over small patches of the image (at most 128
+ * positions, at most 32 columns wide), each of which builds the active and
+ * halo lists of its patch on chip (ballot ranks in raster order), gathers,
  * expands, runs the depthwise and the projection, adds the identity path and
  * computes the next block's mask; blocks alternate between y and a workspace
  * copy.  Otherwise the block runs the kernel chain of the per-block calls,
- * in place on y.  Both give identical masks and counts; outputs agree
- * within rounding of the same arithmetic.
+ * in place on y.  Both give identical masks, counts and outputs: the same
+ * arithmetic in the same order.
  *   x      (device) NHWC input, shape s, dtype dt; read only unless y == x
  *   y      (device) NHWC output; y == x runs in place, other overlap is
  *          DYNCONV_ERR_SHAPE

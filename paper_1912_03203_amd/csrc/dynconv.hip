@@ -229,29 +229,34 @@ void dispatch_mask(dynconv_dtype dt, const void *x, dynconv_shape s, const float
 }
 
 // ------------------------------------------------------------ fused block
-// Band size of the one-launch block kernel: at most kFusedBandPos positions
-// (R*W) per workgroup of kFusedWaves waves, register budget for
-// kFusedWavesPerSimd waves per SIMD.
-constexpr int kFusedBandPos = 256;
-constexpr int kFusedWaves = 4;
-constexpr int kFusedWavesPerSimd = 2;
+// Patches of the one-launch block kernel: the configuration PatchCfgOf picks
+// for the element type and channel bound.
+template <typename T, int MAXC>
+PatchGeom fused_geom_t(dynconv_shape s) {
+    typedef typename PatchCfgOf<T, MAXC>::type CFG;
+    return patch_geom(s.h, s.w, CFG::kOwn, CFG::kRegion);
+}
 
-int fused_band_count(dynconv_shape s) {
-    const int R = fused_rows(kFusedBandPos, s.w, s.h);
-    return s.n * ((s.h + R - 1) / R);
+PatchGeom fused_geom(dynconv_shape s, dynconv_dtype dt) {
+    if (dt == DYNCONV_F32) return s.c <= 32 ? fused_geom_t<float, 32>(s) : fused_geom_t<float, 64>(s);
+    return s.c <= 32 ? fused_geom_t<half_t, 32>(s) : fused_geom_t<half_t, 64>(s);
+}
+
+int fused_patch_count(dynconv_shape s, dynconv_dtype dt) {
+    const PatchGeom p = fused_geom(s, dt);
+    return s.n * p.nph * p.npw;
 }
 
 template <typename T, bool DENSE, int MAXKS, int MAXMT, int MAXC>
 void launch_fused_k(const void *src, void *dst, dynconv_shape s, const dynconv_block *b,
                     const uint8_t *mask_in, const dynconv_block *next, uint8_t *mask_next,
                     int32_t *counts, hipStream_t st, Marks &mk) {
-    constexpr int MAXPOS = kFusedBandPos;
-    const int R = fused_rows(MAXPOS, s.w, s.h);
-    const int nbands = fused_band_count(s);
-    const int grid = (nbands + 7) / 8 * 8;  // whole groups of 8 (one per XCD)
-    launch(mk, k_block_fused<T, DENSE, MAXKS, MAXMT, MAXC, MAXPOS, kFusedWaves, kFusedWavesPerSimd>,
-           dim3(grid), dim3(kFusedWaves * kWave), 0, st,
-           static_cast<const T *>(src), static_cast<T *>(dst), s.n, s.h, s.w, s.c, b->c_hidden, R,
+    typedef typename PatchCfgOf<T, MAXC>::type CFG;
+    const PatchGeom p = fused_geom_t<T, MAXC>(s);
+    const int npatch = s.n * p.nph * p.npw;
+    const int grid = (npatch + 7) / 8 * 8;  // whole groups of 8 (one per XCD)
+    launch(mk, k_block_fused<T, DENSE, MAXKS, MAXMT, MAXC, CFG>, dim3(grid), dim3(CFG::kThreads), 0, st,
+           static_cast<const T *>(src), static_cast<T *>(dst), s.n, s.h, s.w, s.c, b->c_hidden, p.R, p.Wu,
            mask_in, static_cast<const T *>(b->w_expand), b->b_expand, b->act_expand,
            static_cast<const T *>(b->w_dw), b->b_dw, b->act_dw,
            static_cast<const T *>(b->w_project), b->b_project, b->act_project,
@@ -263,14 +268,10 @@ template <typename T, bool DENSE>
 void launch_fused(const void *src, void *dst, dynconv_shape s, const dynconv_block *b,
                   const uint8_t *mask_in, const dynconv_block *next, uint8_t *mask_next,
                   int32_t *counts, hipStream_t st, Marks &mk) {
-    if constexpr (sizeof(T) == 4) {  // fp32: LDS holds at most 32 channels (use_fused)
+    if (s.c <= 32)
         launch_fused_k<T, DENSE, 1, 2, 32>(src, dst, s, b, mask_in, next, mask_next, counts, st, mk);
-    } else {
-        if (s.c <= 32)
-            launch_fused_k<T, DENSE, 1, 2, 32>(src, dst, s, b, mask_in, next, mask_next, counts, st, mk);
-        else
-            launch_fused_k<T, DENSE, 2, 4, 64>(src, dst, s, b, mask_in, next, mask_next, counts, st, mk);
-    }
+    else
+        launch_fused_k<T, DENSE, 2, 4, 64>(src, dst, s, b, mask_in, next, mask_next, counts, st, mk);
 }
 
 void dispatch_fused(dynconv_dtype dt, bool dense, const void *src, void *dst, dynconv_shape s,
@@ -296,12 +297,10 @@ void dispatch_block(dynconv_dtype dt, const void *x, void *y, dynconv_shape s, c
 constexpr int32_t kStackDense = 1;
 constexpr int32_t kStackUnfused = 2;
 
-// The one-launch block kernel covers widths up to one wave and at most 64
-// channels (32 in fp32, whose slices and band rows fill the LDS at 32);
-// other shapes run the unfused kernel chain.
-bool use_fused(dynconv_shape s, dynconv_dtype dt, int32_t flags) {
-    const int cmax = (dt == DYNCONV_F32) ? 32 : kMaxFusedC;
-    return !(flags & kStackUnfused) && s.w <= kWave && s.c <= cmax;
+// The one-launch block kernel covers up to 64 channels; wider blocks run the
+// unfused kernel chain.
+bool use_fused(dynconv_shape s, dynconv_dtype, int32_t flags) {
+    return !(flags & kStackUnfused) && s.c <= kMaxFusedC;
 }
 
 struct StackLayout {
@@ -320,7 +319,7 @@ StackLayout stack_layout(dynconv_shape s, const dynconv_block *blks, int32_t n_b
         L.masks = off;  off += align_up(npos);
         L.mask2 = off;  off += align_up(npos);
         L.counts = off; off += align_up(8 * static_cast<size_t>(n_blocks));
-        L.bands = off;  off += align_up(8 * static_cast<size_t>(n_blocks) * fused_band_count(s));
+        L.bands = off;  off += align_up(8 * static_cast<size_t>(n_blocks) * fused_patch_count(s, dt));
     } else {
         int emax = 0;
         for (int32_t b = 0; b < n_blocks; ++b)
@@ -385,7 +384,7 @@ void stack_walk(const void *x, void *y, dynconv_shape s, dynconv_dtype dt, const
             if (masks) return masks + static_cast<size_t>(b) * npos;
             return reinterpret_cast<uint8_t *>(base + ((b % 2) ? L.mask2 : L.masks));
         };
-        const int nbands = fused_band_count(s);
+        const int nbands = fused_patch_count(s, dt);
         int32_t *band_counts = reinterpret_cast<int32_t *>(base + L.bands);
         if (!dense && plan.note("k_mask"))
             dispatch_mask(dt, src, s, blks[0].w_mask, blks[0].b_mask, mask_of(0), nullptr, st, mk);

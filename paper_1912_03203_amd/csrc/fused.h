@@ -1,206 +1,260 @@
-// fused.h -- one-launch gated block for image widths up to 64 (gfx950).
+// fused.h -- one-launch gated block (gfx950).
 //
 // k_block_fused runs a whole spatially gated inverted-residual block
-// (Sec. 3.2) for one band of R image rows per workgroup, keeping every
-// intermediate on chip:
-//   1. the band's hard-mask rows (and one row above and below) become 64-bit
-//      ballot words; the active set A and its 3x3 dilation D (the positions
-//      the expansion must cover, rows h0-1 .. h0+R) are compacted in raster
-//      order into LDS lists with popcount ranks;
-//   2. x of the band's region rows (h0-1 .. h0+R) is copied into LDS at
-//      kernel start, one contiguous stretch of NHWC (the expansion's B
-//      operand; the band's own rows later become the output tile);
-//   3. for each 32-channel slice of the hidden layer (the slice's weights
-//      staged in LDS, the next slice's loads in flight meanwhile):
-//      expansion of the rows of D (MFMA, bias as the accumulator's start) +
-//      activation, stored at the row's position in a zero-bordered
-//      (R+2) x (W+2) region array, so that the depthwise 3x3 at an active
-//      position reads its 9 taps at fixed offsets from its own row (taps
-//      outside the image land on the zero border; taps inside it are in D);
-//      the depthwise output (fp32 sums, taps in registers, activation) is
-//      the B operand of the projection (MFMA), accumulated over the slices;
-//   4. epilogue: y = x + F at the active positions of the band's own rows in
-//      LDS (inactive positions keep x bit for bit), one coalesced store of
-//      the band, and the next block's mask unit on the stored values (the
-//      fp32 fused multiply-add chain of k_mask).
+// (Sec. 3.2) for one patch of R image rows x Wu columns per workgroup,
+// keeping every intermediate on chip:
+//   1. the hard-mask rows of the patch's region (the patch plus a one-pixel
+//      ring: rows h0-1 .. h0+R, columns w0-1 .. w0+Wu) become 64-bit ballot
+//      words; the patch's active set A and the part of its 3x3 dilation the
+//      expansion must cover (every in-image region position next to an
+//      active one) are compacted in raster order into LDS lists with
+//      popcount ranks;
+//   2. x at every in-image region position is copied into LDS; each wave
+//      keeps the expansion's B fragments of its needed positions in
+//      registers for all slices; the patch's own positions become the output;
+//   3. for each 32-channel slice of the hidden layer: expansion of the
+//      needed positions (MFMA, bias as the accumulator's start) +
+//      activation, stored at the position's slot of a (R+2) x (Wu+2) region
+//      array, so that the depthwise 3x3 at an active position reads its 9
+//      taps at fixed offsets (slots outside the image stay zero, slots inside
+//      it were expanded); the depthwise output (fp32 sums, activation) is the
+//      B operand of the projection (MFMA), accumulated over the slices.  The
+//      expansion weights and the depthwise/projection weights of a slice sit
+//      in one LDS buffer each: the next slice's expansion weights are written
+//      while the depthwise runs, its depthwise/projection weights while the
+//      next expansion runs, each loaded from memory one slice ahead;
+//   4. epilogue: y = x + F at the active positions (inactive positions keep
+//      x bit for bit), a coalesced store of the patch, and the next block's
+//      mask unit on the stored values (the fp32 multiply-add chain of k_mask).
+// Patches are small (at most 256 positions) and many, so the hardware
+// dispatcher spreads patches of very different active counts over the CUs.
 // The arithmetic of every output element is the one of the kernel chain
 // (k_expand, k_dw_project): same operand fragments, same summation order.
-// Input and output must be different buffers: neighbouring bands read the
-// rows next to this band as their halo.  Band i writes its active and
+// Input and output must be different buffers: neighbouring patches read the
+// positions next to this one as their ring.  Patch i writes its active and
 // dilated counts to band_counts[2i], [2i+1]; k_band_counts sums them.
 #pragma once
 
 #include "kernels.h"
 
+#include <type_traits>
+
 namespace dynconv {
 
-constexpr int kFusedMaxRegionRows = 64;     // R + 2
 constexpr int kChunk = 32;                  // hidden channels per slice
 constexpr int kChunkPad = kChunk + 8;       // padded LDS row of a slice
 constexpr int kMaxFusedC = 64;
+constexpr int kPatchMaxCols = 32;           // Wu
+constexpr int kPatchMaxRows = 50;           // R
 
-// Band geometry for at most MAXPOS active positions per band (R*W <= MAXPOS):
-// rows of the band, at most 62 (the region of rows h0-1 .. h0+R fits 64).
-__host__ __device__ constexpr int fused_rows(int maxpos, int W, int H) {
-    int r = maxpos / W;
-    if (r > kFusedMaxRegionRows - 2) r = kFusedMaxRegionRows - 2;
-    if (r > H) r = H;
-    return r < 1 ? 1 : r;
-}
-// largest zero-bordered region (R+2) x (W+2) over the widths 1..64
-__host__ __device__ constexpr int fused_max_region(int maxpos) {
-    int m = 0;
-    for (int w = 1; w <= kWave; ++w) {
-        const int r = fused_rows(maxpos, w, 1 << 20);
-        if ((r + 2) * (w + 2) > m) m = (r + 2) * (w + 2);
-    }
-    return m;
-}
-
-template <int MAXPOS, int NW>
-struct BandShape {
-    static constexpr int kThreads = NW * kWave;                // workgroup size
-    static constexpr int kMaxNeed = MAXPOS + 2 * kWave;       // region positions (R+2)*W
-    static constexpr int kMaxRegion = fused_max_region(MAXPOS);
-    static constexpr int kNeedTiles = (kMaxNeed / 16 + NW - 1) / NW;   // 16-row tiles per wave
-    static constexpr int kActTiles = (MAXPOS / 16 + NW - 1) / NW;
+// A patch configuration: at most OWN own positions and REGION region slots
+// per patch, NW waves per workgroup, register budget for WPE waves per SIMD.
+template <int OWN, int REGION, int NW, int WPE>
+struct PatchCfg {
+    static constexpr int kOwn = OWN, kRegion = REGION, kWaves = NW, kWpe = WPE;
+    static constexpr int kThreads = NW * kWave;
 };
+// Per element type and channel bound, the largest patches whose LDS lets the
+// most waves run per CU:
+//   16-bit, C <= 32: 8 x 32 patches, 8 waves, two workgroups per CU
+//   16-bit, C <= 64: 4 x 32 patches, 4 waves, two workgroups per CU
+//   fp32,   C <= 32: 8 x 32 patches, 8 waves, one workgroup per CU
+//   fp32,   C <= 64: 4 x 32 patches, 4 waves, one workgroup per CU
+template <typename T, int MAXC> struct PatchCfgOf;
+template <int MAXC> struct PatchCfgOf<float, MAXC> {
+    typedef typename std::conditional<MAXC <= 32, PatchCfg<256, 340, 8, 2>, PatchCfg<128, 208, 4, 1>>::type type;
+};
+template <int MAXC> struct PatchCfgOf<half_t, MAXC> {
+    typedef typename std::conditional<MAXC <= 32, PatchCfg<256, 340, 8, 4>, PatchCfg<128, 208, 4, 2>>::type type;
+};
+template <int MAXC> struct PatchCfgOf<bf16_t, MAXC> : PatchCfgOf<half_t, MAXC> {};
 
-// Weights of one 32-channel slice of the hidden layer.
+// Patch geometry: the image width is cut into equal column strips of at most
+// 32, the height into strips of R rows, with R * Wu <= own and the region
+// (R+2) x (Wu+2) <= region.
+struct PatchGeom {
+    int R, Wu, nph, npw;
+};
+__host__ __device__ inline PatchGeom patch_geom(int H, int W, int own, int region) {
+    PatchGeom p;
+    const int strips = (W + kPatchMaxCols - 1) / kPatchMaxCols;
+    p.Wu = (W + strips - 1) / strips;
+    int r = own / p.Wu;
+    const int rr = region / (p.Wu + 2) - 2;
+    if (r > rr) r = rr;
+    if (r > kPatchMaxRows) r = kPatchMaxRows;
+    if (r > H) r = H;
+    p.R = r < 1 ? 1 : r;
+    p.nph = (H + p.R - 1) / p.R;
+    p.npw = (W + p.Wu - 1) / p.Wu;
+    return p;
+}
+
+// Weights of one 32-channel slice of the hidden layer, in the two parts that
+// different phases of the slice read.
 template <typename T, int MAXC>
-struct SliceWeights {
+struct ExpandWeights {
     alignas(16) T w1[kChunk][MAXC + 8];    // expansion rows e (slice-local), c fastest, padded
+    alignas(16) float b1[kChunk];
+};
+template <typename T, int MAXC>
+struct DwProjWeights {
     alignas(16) T w3[MAXC][kChunkPad];     // projection rows c, slice channels fastest
     alignas(16) T w2[9][kChunk];           // depthwise taps, transposed
-    alignas(16) float b1[kChunk];
     alignas(16) float b2[kChunk];
 };
 
-template <typename T, int MAXC, int MAXPOS>
-struct FusedLds {
-    typedef BandShape<MAXPOS, 1> B;
-    uint64_t nw[kFusedMaxRegionRows];   // dilated positions (of the band's actives) per region row
-    uint64_t aw[kFusedMaxRegionRows];   // active positions (own rows only)
-    uint64_t gw[kFusedMaxRegionRows];   // mask words of region rows (image rows h0-1+rr)
-    int need_off[kFusedMaxRegionRows + 1];
-    int act_off[kFusedMaxRegionRows + 1];
-    int16_t need[B::kMaxNeed];          // zero-bordered region index rr*(W+2) + w+1, raster order
-    int16_t act[MAXPOS];
+template <typename T, int MAXC, class CFG>
+struct PatchLds {
+    static constexpr int kRows = kPatchMaxRows + 2;
+    uint64_t nw[kRows];                 // needed slots per region row (bit = region column)
+    uint64_t aw[kRows];                 // active own positions per region row
+    uint64_t gw[kRows];                 // mask words of the region rows
+    int need_off[kRows + 1];
+    int act_off[kRows + 1];
+    int16_t need[CFG::kRegion];         // region slot rr*(cols+2) + c, raster order
+    int16_t act[CFG::kOwn];
     alignas(16) float b3[MAXC];
-    SliceWeights<T, MAXC> wt[2];        // double-buffered slice weights
-    alignas(16) T xs[B::kMaxNeed][MAXC + 8];  // x of the region rows (rr*W + w), padded rows;
-                                              // the band's own rows become y
-    alignas(16) T h1r[B::kMaxRegion][kChunkPad];  // the slice, zero-bordered region layout
+    ExpandWeights<T, MAXC> we;
+    DwProjWeights<T, MAXC> wd;
+    alignas(16) T xs[CFG::kRegion][MAXC + 8];       // x at region slots; own slots become y
+    alignas(16) T h1r[CFG::kRegion + 1][kChunkPad]; // the slice in region layout + a spare row
 };
 
-// Cooperative global -> register -> LDS staging of one slice's weights: each
-// thread owns kStageSlots 16-byte pieces (zero beyond E).
+// Cooperative global -> register -> LDS staging of one part of a slice's
+// weights: each thread owns kSlots 16-byte pieces (zero beyond E).
 template <typename T, int MAXC, int NT>
-struct SliceStager {
+struct ExpandStager {
     static constexpr int kPer16 = 16 / static_cast<int>(sizeof(T));
-    static constexpr int kPieces = 2 * kChunk * MAXC / kPer16 + kChunk * 9 / kPer16 + 2 * kChunk / 4;
-    static constexpr int kStageSlots = (kPieces + NT - 1) / NT;
-    uint4 v[kStageSlots];
-    // piece index p enumerates, in order: w1 rows (32 x C), w3 rows (C x 32),
-    // w2 (32 channels x 9 taps, read as [e][9]), b1, b2
-    __device__ __forceinline__ void load(const T *w1, const T *w2, const T *w3, const float *b1,
-                                         const float *b2, int C, int E, int ec, int tid) {
-        constexpr int per16 = kPer16;
-        const int n1 = kChunk * C / per16, n3 = C * kChunk / per16;
+    static constexpr int kPieces = kChunk * MAXC / kPer16 + kChunk / 4;
+    static constexpr int kSlots = (kPieces + NT - 1) / NT;
+    uint4 v[kSlots];
+    // pieces: w1 rows (32 x C), then b1
+    __device__ __forceinline__ void load(const T *w1, const float *b1, int C, int E, int ec, int tid) {
+        const int n1 = kChunk * C / kPer16;
         const int e_base = ec * kChunk;
 #pragma unroll
-        for (int sl = 0; sl < kStageSlots; ++sl) {
+        for (int sl = 0; sl < kSlots; ++sl) {
             const int p = tid + sl * NT;
             uint4 val = make_uint4(0, 0, 0, 0);
             if (p < n1) {
-                const int e = p / (C / per16), c = (p % (C / per16)) * per16;
+                const int e = p / (C / kPer16), c = (p % (C / kPer16)) * kPer16;
                 if (e_base + e < E)
                     val = *reinterpret_cast<const uint4 *>(w1 + static_cast<int64_t>(e_base + e) * C + c);
-            } else if (p < n1 + n3) {
-                const int q = p - n1;
-                const int c = q / (kChunk / per16), e = (q % (kChunk / per16)) * per16;
-                if (e_base + e < E)
-                    val = *reinterpret_cast<const uint4 *>(w3 + static_cast<int64_t>(c) * E + e_base + e);
-            } else if (p < n1 + n3 + kChunk * 9 / per16) {
-                // w2 [E][9] for the slice's 32 channels is 288 contiguous elements;
-                // E - e_base is a multiple of 16, so no piece straddles E
-                const int q = p - n1 - n3;
-                const int first = q * per16;
-                if (first / 9 < E - e_base)
-                    val = *reinterpret_cast<const uint4 *>(w2 + static_cast<int64_t>(e_base) * 9 + first);
-            } else if (p < n1 + n3 + kChunk * 9 / per16 + 2 * kChunk / 4) {
-                const int q = p - n1 - n3 - kChunk * 9 / per16;
-                const float *b = (q < kChunk / 4) ? b1 : b2;
-                const int e = (q % (kChunk / 4)) * 4;
-                if (e_base + e < E) val = *reinterpret_cast<const uint4 *>(b + e_base + e);
+            } else if (p < n1 + kChunk / 4) {
+                const int e = (p - n1) * 4;
+                if (e_base + e < E) val = *reinterpret_cast<const uint4 *>(b1 + e_base + e);
             }
             v[sl] = val;
         }
     }
-    __device__ __forceinline__ void store(SliceWeights<T, MAXC> &dst, int C, int E, int ec,
-                                          int tid) const {
-        constexpr int per16 = kPer16;
-        const int n1 = kChunk * C / per16, n3 = C * kChunk / per16;
-        const int e_lim = E - ec * kChunk;
+    __device__ __forceinline__ void store(ExpandWeights<T, MAXC> &dst, int C, int tid) const {
+        const int n1 = kChunk * C / kPer16;
 #pragma unroll
-        for (int sl = 0; sl < kStageSlots; ++sl) {
+        for (int sl = 0; sl < kSlots; ++sl) {
             const int p = tid + sl * NT;
             if (p < n1) {
-                const int e = p / (C / per16), c = (p % (C / per16)) * per16;
+                const int e = p / (C / kPer16), c = (p % (C / kPer16)) * kPer16;
                 *reinterpret_cast<uint4 *>(&dst.w1[e][c]) = v[sl];
-            } else if (p < n1 + n3) {
-                const int q = p - n1;
-                const int c = q / (kChunk / per16), e = (q % (kChunk / per16)) * per16;
-                *reinterpret_cast<uint4 *>(&dst.w3[c][e]) = v[sl];
-            } else if (p < n1 + n3 + kChunk * 9 / per16) {
-                const int q = p - n1 - n3;
-                const T *vals = reinterpret_cast<const T *>(&v[sl]);
-#pragma unroll
-                for (int u = 0; u < per16; ++u) {
-                    const int idx = q * per16 + u;  // = e * 9 + k
-                    const int e = idx / 9, k = idx % 9;
-                    dst.w2[k][e] = (e < e_lim) ? vals[u] : static_cast<T>(0.0f);
-                }
-            } else if (p < n1 + n3 + kChunk * 9 / per16 + 2 * kChunk / 4) {
-                const int q = p - n1 - n3 - kChunk * 9 / per16;
-                float *b = (q < kChunk / 4) ? dst.b1 : dst.b2;
-                *reinterpret_cast<uint4 *>(&b[(q % (kChunk / 4)) * 4]) = v[sl];
+            } else if (p < n1 + kChunk / 4) {
+                *reinterpret_cast<uint4 *>(&dst.b1[(p - n1) * 4]) = v[sl];
             }
         }
     }
 };
 
-template <typename T, bool DENSE, int MAXKS, int MAXMT, int MAXC, int MAXPOS, int NW, int WPE>
-__global__ void __launch_bounds__(NW * kWave) __attribute__((amdgpu_waves_per_eu(WPE)))
+template <typename T, int MAXC, int NT>
+struct DwProjStager {
+    static constexpr int kPer16 = 16 / static_cast<int>(sizeof(T));
+    static constexpr int kPieces = MAXC * kChunk / kPer16 + kChunk * 9 / kPer16 + kChunk / 4;
+    static constexpr int kSlots = (kPieces + NT - 1) / NT;
+    uint4 v[kSlots];
+    // pieces: w3 rows (C x 32), then w2 (32 channels x 9 taps, read as [e][9]), then b2
+    __device__ __forceinline__ void load(const T *w2, const T *w3, const float *b2, int C, int E, int ec,
+                                         int tid) {
+        const int n3 = C * kChunk / kPer16, n2 = kChunk * 9 / kPer16;
+        const int e_base = ec * kChunk;
+#pragma unroll
+        for (int sl = 0; sl < kSlots; ++sl) {
+            const int p = tid + sl * NT;
+            uint4 val = make_uint4(0, 0, 0, 0);
+            if (p < n3) {
+                const int c = p / (kChunk / kPer16), e = (p % (kChunk / kPer16)) * kPer16;
+                if (e_base + e < E)
+                    val = *reinterpret_cast<const uint4 *>(w3 + static_cast<int64_t>(c) * E + e_base + e);
+            } else if (p < n3 + n2) {
+                // w2 [E][9] for the slice's 32 channels is 288 contiguous elements;
+                // E - e_base is a multiple of 16, so no piece straddles E
+                const int first = (p - n3) * kPer16;
+                if (first / 9 < E - e_base)
+                    val = *reinterpret_cast<const uint4 *>(w2 + static_cast<int64_t>(e_base) * 9 + first);
+            } else if (p < n3 + n2 + kChunk / 4) {
+                const int e = (p - n3 - n2) * 4;
+                if (e_base + e < E) val = *reinterpret_cast<const uint4 *>(b2 + e_base + e);
+            }
+            v[sl] = val;
+        }
+    }
+    __device__ __forceinline__ void store(DwProjWeights<T, MAXC> &dst, int C, int E, int ec, int tid) const {
+        const int n3 = C * kChunk / kPer16, n2 = kChunk * 9 / kPer16;
+        const int e_lim = E - ec * kChunk;
+#pragma unroll
+        for (int sl = 0; sl < kSlots; ++sl) {
+            const int p = tid + sl * NT;
+            if (p < n3) {
+                const int c = p / (kChunk / kPer16), e = (p % (kChunk / kPer16)) * kPer16;
+                *reinterpret_cast<uint4 *>(&dst.w3[c][e]) = v[sl];
+            } else if (p < n3 + n2) {
+                const T *vals = reinterpret_cast<const T *>(&v[sl]);
+#pragma unroll
+                for (int u = 0; u < kPer16; ++u) {
+                    const int idx = (p - n3) * kPer16 + u;  // = e * 9 + k
+                    const int e = idx / 9, k = idx % 9;
+                    dst.w2[k][e] = (e < e_lim) ? vals[u] : static_cast<T>(0.0f);
+                }
+            } else if (p < n3 + n2 + kChunk / 4) {
+                *reinterpret_cast<uint4 *>(&dst.b2[(p - n3 - n2) * 4]) = v[sl];
+            }
+        }
+    }
+};
+
+template <typename T, bool DENSE, int MAXKS, int MAXMT, int MAXC, class CFG>
+__global__ void __launch_bounds__(CFG::kThreads) __attribute__((amdgpu_waves_per_eu(CFG::kWpe)))
 k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int W, int C, int E,
-              int R, const uint8_t *__restrict__ mask_in,
+              int R, int Wu, const uint8_t *__restrict__ mask_in,
               const T *__restrict__ w1, const float *__restrict__ b1, int act1,
               const T *__restrict__ w2, const float *__restrict__ b2, int act2,
               const T *__restrict__ w3, const float *__restrict__ b3, int act3,
               const float *__restrict__ wm_next, float bm_next, uint8_t *__restrict__ mask_next,
               int32_t *__restrict__ band_counts) {
     typedef mma<T> M;
-    typedef BandShape<MAXPOS, NW> BS;
-    constexpr int kNeedTiles = BS::kNeedTiles, kActTiles = BS::kActTiles;
-    constexpr int NT = BS::kThreads;
-    __shared__ FusedLds<T, MAXC, MAXPOS> L;
+    constexpr int NW = CFG::kWaves, NT = CFG::kThreads, kRegion = CFG::kRegion;
+    constexpr int kNeedTiles = ((kRegion + 15) / 16 + NW - 1) / NW;  // 16-slot tiles per wave
+    constexpr int kActTiles = ((CFG::kOwn + 15) / 16 + NW - 1) / NW;
+    __shared__ PatchLds<T, MAXC, CFG> L;
     const int tid = threadIdx.x;
     const int wave = tid / kWave, lane = tid % kWave;
     const int r = lane % 16, g = lane / 16;
 
-    // Band index, XCD-aware: workgroup i runs on XCD i % 8, so consecutive
-    // bands (which share halo rows) go to the same XCD.
-    const int nbh = (H + R - 1) / R;
-    const int nbands = N * nbh;
-    const int per_xcd = (nbands + 7) / 8;
-    const int band = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-    if (band >= nbands) return;  // uniform per workgroup
-    const int n = band / nbh;
-    const int h0 = (band % nbh) * R;
+    // Patch index, XCD-aware: workgroup i runs on XCD i % 8, so consecutive
+    // patches (which share ring rows and columns) go to the same XCD.
+    const int nph = (H + R - 1) / R, npw = (W + Wu - 1) / Wu;
+    const int npatch = N * nph * npw;
+    const int per_xcd = (npatch + 7) / 8;
+    const int patch = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+    if (patch >= npatch) return;  // uniform per workgroup
+    const int n = patch / (nph * npw);
+    const int h0 = ((patch / npw) % nph) * R;
+    const int w0 = (patch % npw) * Wu;
     const int rows_out = min(R, H - h0);
+    const int cols_out = min(Wu, W - w0);
     const int nreg = rows_out + 2;
-    const int WP = W + 2;  // zero-bordered region row length
-    const uint64_t full = (W == 64) ? ~0ull : ((1ull << W) - 1ull);
+    const int WP = cols_out + 2;  // region row length; region column c is image column w0-1+c
+    const int c_lo = (w0 == 0) ? 1 : 0;                      // first in-image region column
+    const int c_hi = (w0 + cols_out < W) ? WP : WP - 1;      // one past the last
+    const uint64_t img_cols = ((1ull << c_hi) - 1ull) & ~((1ull << c_lo) - 1ull);
+    const uint64_t own_cols = ((1ull << (cols_out + 1)) - 1ull) & ~1ull;
     const int64_t img = static_cast<int64_t>(n) * H;
     const int nchunks = (E + kChunk - 1) / kChunk;
     const float lo1 = act_lo(act1), hi1 = act_hi(act1);
@@ -208,24 +262,30 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
     const float lo3 = act_lo(act3), hi3 = act_hi(act3);
     constexpr int per16 = 16 / static_cast<int>(sizeof(T));
 
-    // All of these only depend on the arguments, so their loads overlap:
-    // the first slice's weights, the projection bias, and x of every region
-    // row inside the image (rows h0-1 .. h0+R: one contiguous NHWC stretch).
-    SliceStager<T, MAXC, NT> stage;
-    stage.load(w1, w2, w3, b1, b2, C, E, 0, tid);
+    // These only depend on the arguments, so their loads overlap: the first
+    // slice's weights, the projection bias, x at the in-image region slots.
+    ExpandStager<T, MAXC, NT> stA;
+    DwProjStager<T, MAXC, NT> stB;
+    stA.load(w1, b1, C, E, 0, tid);
+    stB.load(w2, w3, b2, C, E, 0, tid);
     for (int c = tid; c < C; c += NT) L.b3[c] = b3[c];
     {
-        const int r_first = (h0 == 0) ? 1 : 0;          // region row of image row max(h0-1, 0)
+        const int r_first = (h0 == 0) ? 1 : 0;
         const int r_last = (h0 + rows_out < H) ? nreg - 1 : nreg - 2;
         const int vpr = C / per16;                      // 16-byte pieces per position
-        const int nvec = (r_last - r_first + 1) * W * vpr;
-        const uint4 *src = reinterpret_cast<const uint4 *>(xin + (img + h0 - 1 + r_first) * W * C);
-        for (int i = tid; i < nvec; i += NT)
-            *reinterpret_cast<uint4 *>(&L.xs[r_first * W + i / vpr][(i % vpr) * per16]) = src[i];
+        const int per_row = (c_hi - c_lo) * vpr;
+        const int nvec = (r_last - r_first + 1) * per_row;
+        for (int i = tid; i < nvec; i += NT) {
+            const int rr = r_first + i / per_row, k = i % per_row;
+            const int c = c_lo + k / vpr, piece = k % vpr;
+            const uint4 *src = reinterpret_cast<const uint4 *>(
+                xin + ((img + h0 - 1 + rr) * W + (w0 - 1 + c)) * C);
+            *reinterpret_cast<uint4 *>(&L.xs[rr * WP + c][piece * per16]) = src[piece];
+        }
     }
-    {   // zero region: its border and out-of-image rows are never written again
+    {   // zero region: slots outside the image are never written again
         uint4 *z = reinterpret_cast<uint4 *>(&L.h1r[0][0]);
-        constexpr int nz = BS::kMaxRegion * kChunkPad * static_cast<int>(sizeof(T)) / 16;
+        constexpr int nz = kRegion * kChunkPad * static_cast<int>(sizeof(T)) / 16;
         for (int i = tid; i < nz; i += NT) z[i] = make_uint4(0, 0, 0, 0);
     }
 
@@ -233,8 +293,8 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
     for (int rr = wave; rr < nreg; rr += NW) {
         const int hh = h0 - 1 + rr;
         bool bit = false;
-        if (hh >= 0 && hh < H && lane < W)
-            bit = DENSE ? true : mask_in[(img + hh) * W + lane] != 0;
+        if (hh >= 0 && hh < H && lane < WP && ((img_cols >> lane) & 1ull))
+            bit = DENSE ? true : mask_in[(img + hh) * W + (w0 - 1 + lane)] != 0;
         const uint64_t b = __ballot(bit);
         if (lane == 0) L.gw[rr] = b;
     }
@@ -247,14 +307,14 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
             const bool own = rr >= 1 && rr <= rows_out;
             const int hh = h0 - 1 + rr;
             const bool inimg = hh >= 0 && hh < H;
-            const uint64_t above = (rr - 1 >= 1 && rr - 1 <= rows_out) ? L.gw[rr - 1] : 0ull;
-            const uint64_t below = (rr + 1 >= 1 && rr + 1 <= rows_out) ? L.gw[rr + 1] : 0ull;
-            a = own ? L.gw[rr] : 0ull;
+            const uint64_t above = (rr - 1 >= 1 && rr - 1 <= rows_out) ? (L.gw[rr - 1] & own_cols) : 0ull;
+            const uint64_t below = (rr + 1 >= 1 && rr + 1 <= rows_out) ? (L.gw[rr + 1] & own_cols) : 0ull;
+            a = own ? (L.gw[rr] & own_cols) : 0ull;
             const uint64_t v = above | a | below;
-            nwd = inimg ? ((v | (v << 1) | (v >> 1)) & full) : 0ull;
+            nwd = inimg ? ((v | (v << 1) | (v >> 1)) & img_cols) : 0ull;
             if (own) {
                 const uint64_t gv = L.gw[rr - 1] | L.gw[rr] | L.gw[rr + 1];
-                dil_own = (gv | (gv << 1) | (gv >> 1)) & full;
+                dil_own = (gv | (gv << 1) | (gv >> 1)) & own_cols;
             }
             L.aw[rr] = a;
             L.nw[rr] = nwd;
@@ -278,42 +338,47 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
             L.act_off[nreg] = sa;
         }
         if (!DENSE && band_counts) {
-            // this band's active and dilated counts (a plain store per band:
+            // this patch's active and dilated counts (a plain store per patch:
             // atomics on one address from every XCD serialise)
             int pa = ca, pd = __popcll(dil_own);
             for (int off = 32; off > 0; off >>= 1) {
                 pa += __shfl_down(pa, off);
                 pd += __shfl_down(pd, off);
             }
-            if (lane == 0) *reinterpret_cast<int2 *>(band_counts + 2 * band) = make_int2(pa, pd);
+            if (lane == 0) *reinterpret_cast<int2 *>(band_counts + 2 * patch) = make_int2(pa, pd);
         }
     }
     __syncthreads();
     const uint64_t lt = lanemask_lt(lane);
     for (int rr = wave; rr < nreg; rr += NW) {
-        if (lane < W) {
+        if (lane < WP) {
             const uint64_t nwd = L.nw[rr], awd = L.aw[rr];
-            const int16_t q = static_cast<int16_t>(rr * WP + lane + 1);
+            const int16_t q = static_cast<int16_t>(rr * WP + lane);
             if ((nwd >> lane) & 1ull) L.need[L.need_off[rr] + __popcll(nwd & lt)] = q;
             if ((awd >> lane) & 1ull) L.act[L.act_off[rr] + __popcll(awd & lt)] = q;
         }
     }
-    stage.store(L.wt[0], C, E, 0, tid);
+    stA.store(L.we, C, tid);
     __syncthreads();
     const int n_need = L.need_off[nreg];
     const int n_act = L.act_off[nreg];
-    T (*yrows)[MAXC + 8] = &L.xs[W];  // the band's own rows (region rows 1..rows_out)
 
     if (n_act > 0) {
-        // region rows of this wave's need and active tiles: index into the
-        // zero-bordered region (h1r) and into the unbordered x rows (xs)
-        int nq[kNeedTiles], nx[kNeedTiles];
+        // this wave's needed slots (the expansion's output rows; past n_need:
+        // the spare row) and their B fragments, kept for every slice
+        int nq[kNeedTiles];
+        typename M::frag bx[kNeedTiles][MAXKS];
 #pragma unroll
         for (int j = 0; j < kNeedTiles; ++j) {
             const int i = (wave + NW * j) * 16 + r;
             const int q = (i < n_need) ? static_cast<int>(L.need[i]) : -1;
-            nq[j] = q;
-            nx[j] = (q >= 0) ? (q / WP) * W + q % WP - 1 : W;  // past n_need: any row, never stored
+            nq[j] = (q >= 0) ? q : kRegion;
+            const int qx = (q >= 0) ? q : WP + 1;  // an own slot; its column is never stored
+#pragma unroll
+            for (int ks = 0; ks < MAXKS; ++ks) {
+                const int c0 = ks * 32 + g * 8;
+                bx[j][ks] = (c0 < C) ? M::load(&L.xs[qx][c0]) : M::zero();
+            }
         }
         int aq[kActTiles];
 #pragma unroll
@@ -332,11 +397,14 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
             }
         const int row_bytes = WP * kChunkPad * static_cast<int>(sizeof(T));
         constexpr int col_bytes = kChunkPad * static_cast<int>(sizeof(T));
+        if (nchunks > 1) stA.load(w1, b1, C, E, 1, tid);
 
         for (int ec = 0; ec < nchunks; ++ec) {
-            const SliceWeights<T, MAXC> &sw = L.wt[ec & 1];
-            if (ec + 1 < nchunks) stage.load(w1, w2, w3, b1, b2, C, E, ec + 1, tid);
-            // ---- 3a. expansion of this slice into the region array
+            // ---- 3a. expansion of this slice into the region array; meanwhile
+            // this slice's depthwise/projection weights go to LDS and the next
+            // slice's are requested
+            stB.store(L.wd, C, E, ec, tid);
+            if (ec + 1 < nchunks) stB.load(w2, w3, b2, C, E, ec + 1, tid);
             typename M::frag a1[2][MAXKS];
             floatx4 binit[2];
 #pragma unroll
@@ -344,52 +412,45 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
 #pragma unroll
                 for (int ks = 0; ks < MAXKS; ++ks) {
                     const int c0 = ks * 32 + g * 8;
-                    a1[m][ks] = (c0 < C) ? M::load(&sw.w1[m * 16 + r][c0]) : M::zero();
+                    a1[m][ks] = (c0 < C) ? M::load(&L.we.w1[m * 16 + r][c0]) : M::zero();
                 }
 #pragma unroll
-                for (int v = 0; v < 4; ++v) binit[m][v] = sw.b1[m * 16 + 4 * g + v];
+                for (int v = 0; v < 4; ++v) binit[m][v] = L.we.b1[m * 16 + 4 * g + v];
             }
 #pragma unroll
             for (int j = 0; j < kNeedTiles; ++j) {
                 const int t = wave + NW * j;
                 if (t * 16 < n_need) {
-                    typename M::frag bxs[MAXKS];
-#pragma unroll
-                    for (int ks = 0; ks < MAXKS; ++ks) {
-                        const int c0 = ks * 32 + g * 8;
-                        bxs[ks] = (c0 < C) ? M::load(&L.xs[nx[j]][c0]) : M::zero();
-                    }
 #pragma unroll
                     for (int m = 0; m < 2; ++m) {
                         floatx4 d = binit[m];
 #pragma unroll
-                        for (int ks = 0; ks < MAXKS; ++ks) d = M::run(a1[m][ks], bxs[ks], d);
+                        for (int ks = 0; ks < MAXKS; ++ks) d = M::run(a1[m][ks], bx[j][ks], d);
                         const int e0 = ec * kChunk + m * 16 + 4 * g;
-                        if (nq[j] >= 0 && e0 < E) {
-                            float o[4];
+                        float o[4];
 #pragma unroll
-                            for (int v = 0; v < 4; ++v) o[v] = clamp_act(d[v], lo1, hi1);
-                            io<T>::store4(&L.h1r[nq[j]][m * 16 + 4 * g], o);
-                        }
+                        for (int v = 0; v < 4; ++v) o[v] = clamp_act(d[v], lo1, hi1);
+                        // channels past E go to the spare row
+                        const int q = (e0 < E) ? nq[j] : kRegion;
+                        io<T>::store4(&L.h1r[q][m * 16 + 4 * g], o);
                     }
                 }
             }
-            if (ec + 1 < nchunks) stage.store(L.wt[(ec + 1) & 1], C, E, ec + 1, tid);
             __syncthreads();
-            // ---- 3b. depthwise at the active positions + projection slice
+            // ---- 3b. depthwise at the active positions + projection slice;
+            // meanwhile the next slice's expansion weights go to LDS
+            if (ec + 1 < nchunks) stA.store(L.we, C, tid);
+            if (ec + 2 < nchunks) stA.load(w1, b1, C, E, ec + 2, tid);
             const int e8 = ec * kChunk + 8 * g;
             const bool ein = e8 < E;
-            typename io<T>::vec8 wk[9];  // the lane's 8 channels of each tap, packed
-#pragma unroll
-            for (int k = 0; k < 9; ++k) wk[k] = io<T>::raw8(&sw.w2[k][8 * g]);
             float bk[8];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) bk[u] = sw.b2[8 * g + u];
+            for (int u = 0; u < 8; ++u) bk[u] = L.wd.b2[8 * g + u];
             typename M::frag a3[MAXMT];
 #pragma unroll
             for (int mt = 0; mt < MAXMT; ++mt) {
                 const int c = mt * 16 + r;
-                a3[mt] = (ein && c < C) ? M::load(&sw.w3[c][8 * g]) : M::zero();
+                a3[mt] = (ein && c < C) ? M::load(&L.wd.w3[c][8 * g]) : M::zero();
             }
             const char *h1base = reinterpret_cast<const char *>(&L.h1r[0][8 * g]);
 #pragma unroll
@@ -401,17 +462,24 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
                     for (int u = 0; u < 8; ++u) hv[u] = 0.0f;
                     if (aq[j] >= 0 && ein) {
                         const char *own = h1base + aq[j] * col_bytes;
+                        // all nine taps in flight before the first FMA
+                        typename io<T>::vec8 tv[9];
+#pragma unroll
+                        for (int k = 0; k < 9; ++k) {
+                            const int off = (k / 3 - 1) * row_bytes + (k % 3 - 1) * col_bytes;
+                            tv[k] = io<T>::raw8(reinterpret_cast<const T *>(own + off));
+                        }
                         float s[8];
 #pragma unroll
                         for (int u = 0; u < 8; ++u) s[u] = bk[u];
 #pragma unroll
                         for (int k = 0; k < 9; ++k) {
-                            const int off = (k / 3 - 1) * row_bytes + (k % 3 - 1) * col_bytes;
-                            float v[8];
-                            io<T>::load8(reinterpret_cast<const T *>(own + off), v);
+                            // the lane's 8 channels of tap k (4 addresses per wave)
+                            const typename io<T>::vec8 wk = io<T>::raw8(&L.wd.w2[k][8 * g]);
 #pragma unroll
                             for (int u = 0; u < 8; ++u)
-                                s[u] = __builtin_fmaf(static_cast<float>(wk[k][u]), v[u], s[u]);
+                                s[u] = __builtin_fmaf(static_cast<float>(wk[u]),
+                                                      static_cast<float>(tv[k][u]), s[u]);
                         }
 #pragma unroll
                         for (int u = 0; u < 8; ++u) hv[u] = clamp_act(s[u], lo2, hi2);
@@ -423,38 +491,42 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
             }
             __syncthreads();
         }
-        // ---- 4a. residual sum at the active positions, in the band's own x rows
+        // ---- 4a. residual sum at the active positions, in place in xs
 #pragma unroll
         for (int j = 0; j < kActTiles; ++j) {
             if (aq[j] >= 0) {
-                const int q = (aq[j] / WP - 1) * W + aq[j] % WP - 1;  // own-row index
 #pragma unroll
                 for (int mt = 0; mt < MAXMT; ++mt) {
                     const int c0 = mt * 16 + 4 * g;
                     if (c0 < C) {
                         float xv[4], o[4];
-                        io<T>::load4(&yrows[q][c0], xv);
+                        io<T>::load4(&L.xs[aq[j]][c0], xv);
 #pragma unroll
                         for (int v = 0; v < 4; ++v) o[v] = xv[v] + clamp_act(acc[j][mt][v], lo3, hi3);
-                        io<T>::store4(&yrows[q][c0], o);
+                        io<T>::store4(&L.xs[aq[j]][c0], o);
                     }
                 }
             }
         }
         __syncthreads();
     }
-    // ---- 4b. store the band (inactive positions: x unchanged)
+    // ---- 4b. store the patch (inactive positions: x unchanged)
     {
         const int vpr = C / per16;
-        const int nvec = rows_out * W * vpr;
-        uint4 *dst = reinterpret_cast<uint4 *>(yout + (img + h0) * W * C);
-        for (int i = tid; i < nvec; i += NT)
-            dst[i] = *reinterpret_cast<const uint4 *>(&yrows[i / vpr][(i % vpr) * per16]);
+        const int per_row = cols_out * vpr;
+        const int nvec = rows_out * per_row;
+        for (int i = tid; i < nvec; i += NT) {
+            const int rr = 1 + i / per_row, k = i % per_row;
+            const int c = 1 + k / vpr, piece = k % vpr;
+            uint4 *dst = reinterpret_cast<uint4 *>(yout + ((img + h0 - 1 + rr) * W + (w0 - 1 + c)) * C);
+            dst[piece] = *reinterpret_cast<const uint4 *>(&L.xs[rr * WP + c][piece * per16]);
+        }
     }
     // ---- 4c. the next block's mask unit on the stored values
     if (mask_next) {
-        for (int q = tid; q < rows_out * W; q += NT) {
-            const T *row = &yrows[q][0];
+        for (int i = tid; i < rows_out * cols_out; i += NT) {
+            const int rr = 1 + i / cols_out, c = 1 + i % cols_out;
+            const T *row = &L.xs[rr * WP + c][0];
             float a = 0.0f;
             for (int c0 = 0; c0 < C; c0 += 8) {
                 float v[8];
@@ -463,12 +535,12 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
                 for (int u = 0; u < 8; ++u) a = __builtin_fmaf(wm_next[c0 + u], v[u], a);
             }
             const float m = a + bm_next;
-            mask_next[(img + h0) * W + q] = (m > 0.0f) ? 1 : 0;
+            mask_next[(img + h0 - 1 + rr) * W + (w0 - 1 + c)] = (m > 0.0f) ? 1 : 0;
         }
     }
 }
 
-// counts[2b], counts[2b+1] = sums of the per-band counts of block b
+// counts[2b], counts[2b+1] = sums of the per-patch counts of block b
 // (one workgroup per block, fixed summation order).
 __global__ void __launch_bounds__(kBlock)
 k_band_counts(const int32_t *__restrict__ band_counts, int nbands, int32_t *__restrict__ counts) {

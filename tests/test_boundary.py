@@ -132,18 +132,23 @@ def test_stack_validation(lib):
     def up(v):
         return (v + 255) // 256 * 256
 
-    # one-launch blocks: ping-pong copy of x, two masks, counts, per-band counts
-    # (bands of up to 256 positions: 16 rows of 16, one band per image)
+    # one-launch blocks: ping-pong copy of x, two masks, counts, per-patch
+    # counts (fp16 at 32 channels: patches of 16 x 16, one per image)
     fused = lib.dynconv_stack_workspace_bytes(s, blocks, 3, 1, 0)
     assert fused == up(npos * 32 * 2) + 2 * up(npos) + up(8 * 3) + up(8 * 3 * 4)
     # kernel chain: mask, lists, counts, row scratch, hidden tensor of the widest block
     need = lib.dynconv_stack_workspace_bytes(s, blocks, 3, 1, 2)
     assert need == (npos + 4 * npos + 4 * npos + 36 * npos + up(8 * 3) + up(8 * rows)
                     + up(8 * (rows + 1)) + up((npos + 1) * 192 * 2))
-    # widths beyond one wave always take the kernel chain
+    # more than 64 channels always take the kernel chain
+    wide_c = dc.Shape(1, 4, 100, 72)
+    blocks72 = (dc.Block * 1)(fake_block(C=72))
+    assert lib.dynconv_stack_workspace_bytes(wide_c, blocks72, 1, 1, 0) == \
+        lib.dynconv_stack_workspace_bytes(wide_c, blocks72, 1, 1, 2)
+    # wide images stay on the one-launch path: patches of 4 rows x 25 columns
     wide = dc.Shape(1, 4, 100, 32)
     assert lib.dynconv_stack_workspace_bytes(wide, blocks, 3, 1, 0) == \
-        lib.dynconv_stack_workspace_bytes(wide, blocks, 3, 1, 2)
+        up(400 * 32 * 2) + 2 * up(400) + up(8 * 3) + up(8 * 3 * 4)
     f = lib.dynconv_stack_forward
     assert f(None, FAKE, s, 1, blocks, 3, 0, None, None, FAKE, need, None) == ERR_NULL
     assert f(FAKE, None, s, 1, blocks, 3, 0, None, None, FAKE, need, None) == ERR_NULL
@@ -180,6 +185,12 @@ def test_stack_launch_plans(lib):
     assert names(2, 1) == ["k_mask", "k_rowcount", "k_rowscan", "k_compact", "k_expand",
                            "k_dw_project"] * 8
     assert names(3, 0) == ["k_copy16"] + ["k_expand", "k_dw_project"] * 8
-    assert names(0, 1, shape=dc.Shape(2, 8, 65, 32))[:7] == [
+    assert names(0, 1, shape=dc.Shape(2, 8, 300, 32), n=2) == ["k_mask"] + ["k_block_fused"] * 2 + \
+        ["k_band_counts"]
+    arr72 = (dc.Block * 2)(*([fake_block(C=72)] * 2))
+    total = lib.dynconv_stack_launch_names(dc.Shape(2, 8, 8, 72), arr72, 2, 1, 0, 1, None, 0)
+    out = (ctypes.c_char_p * total)()
+    lib.dynconv_stack_launch_names(dc.Shape(2, 8, 8, 72), arr72, 2, 1, 0, 1, out, total)
+    assert [x.decode() for x in out][:7] == [
         "k_mask", "k_rowcount", "k_rowscan", "k_compact", "k_expand", "k_dw_project", "k_mask"]
     assert lib.dynconv_stack_launch_names(s, arr, 0, 1, 0, 0, None, 0) == -1

@@ -1,5 +1,5 @@
-"""Parity of the one-launch block kernel (the stack's execution for widths up
-to 64 and at most 64 channels) with the CPU oracle, and its agreement with the
+"""Parity of the one-launch block kernel (the stack's execution for at most
+64 channels) with the CPU oracle, and its agreement with the
 multi-kernel chain.  Same tolerances as the per-block calls: masks and counts
 bit-exact, outputs within 1e-5 (fp32) / 2e-2 (fp16, bf16) normwise, inactive
 positions untouched."""
@@ -52,6 +52,10 @@ FUSED_CASES = [
     ("width1_f16", "f16", (2, 300, 1, 16, 48), 0.3, 6),
     ("width7_f32", "f32", (3, 20, 7, 8, 16), 0.6, 7),
     ("height1_bf16", "bf16", (5, 1, 50, 24, 96), 0.5, 8),
+    ("wide_w100_f16", "f16", (2, 9, 100, 32, 96), 0.3, 9),
+    ("wide_w130_bf16", "bf16", (1, 7, 130, 24, 48), 0.5, 10),
+    ("fp32_c48", "f32", (2, 10, 20, 48, 96), 0.4, 11),
+    ("fp32_c64_w33", "f32", (1, 6, 33, 64, 64), 0.6, 12),
 ]
 
 
@@ -89,7 +93,9 @@ def test_fused_empty_and_full_masks(bias):
 
 @pytest.mark.parametrize("dtype,shape,nb", [("f16", (32, 64, 64, 32, 192), 8),
                                             ("bf16", (4, 20, 28, 48, 96), 3),
-                                            ("f32", (2, 16, 16, 16, 96), 2)])
+                                            ("f32", (2, 16, 16, 16, 96), 2),
+                                            ("f16", (2, 12, 90, 64, 128), 2),
+                                            ("f32", (1, 9, 40, 40, 80), 3)])
 def test_fused_stack_matches_kernel_chain(dtype, shape, nb):
     """One-launch blocks (out of place and in place, which takes the extra copy
     for an odd block count) and the multi-kernel chain give the same masks,
