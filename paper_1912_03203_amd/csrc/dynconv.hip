@@ -22,6 +22,7 @@ constexpr int kMaxDilate = 3;
 constexpr int kMaxBlocks = 1024;
 constexpr int64_t kMaxPositions = (int64_t{1} << 31) / 9 - 1;
 constexpr int kMaxGrid = 2048;  // workgroups of the row-tile kernels (grid-stride beyond)
+constexpr int kMaxDwGrid = 8192;  // workgroups of the depthwise-projection kernel
 constexpr size_t kAlign = 256;
 
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
@@ -76,11 +77,13 @@ dynconv_status launch_status() {
     return hipGetLastError() == hipSuccess ? DYNCONV_OK : DYNCONV_ERR_HIP;
 }
 
+// whole groups of 8 workgroups (one per XCD)
 int grid_for_rows(int64_t rows) {
     int64_t tiles = (rows + 15) / 16;
     int64_t blocks = (tiles + kWavesPerBlock - 1) / kWavesPerBlock;
     if (blocks < 1) blocks = 1;
-    return static_cast<int>(blocks < kMaxGrid ? blocks : kMaxGrid);
+    if (blocks > kMaxGrid) blocks = kMaxGrid;
+    return static_cast<int>((blocks + 7) / 8 * 8);
 }
 
 // Optional per-launch timing: launch i gets the event pair (ev[2i], ev[2i+1]),
@@ -111,11 +114,14 @@ void launch(Marks &mk, void (*kernel)(KArgs...), dim3 grid, dim3 block, size_t l
 struct IndexScratch {
     int2 *rowcnt;
     int2 *rowoff;
+    uint64_t *words;  // mask words, [N*H][ceil(W/64)]
 };
 
 size_t index_scratch_bytes(dynconv_shape s) {
     int64_t rows = static_cast<int64_t>(s.n) * s.h;
-    return align_up(sizeof(int2) * rows) + align_up(sizeof(int2) * (rows + 1));
+    int64_t nseg = (s.w + kWave - 1) / kWave;
+    return align_up(sizeof(int2) * rows) + align_up(sizeof(int2) * (rows + 1)) +
+           align_up(sizeof(uint64_t) * rows * nseg);
 }
 
 IndexScratch carve_index_scratch(void *ws, dynconv_shape s) {
@@ -125,6 +131,8 @@ IndexScratch carve_index_scratch(void *ws, dynconv_shape s) {
     sc.rowcnt = reinterpret_cast<int2 *>(p);
     p += align_up(sizeof(int2) * rows);
     sc.rowoff = reinterpret_cast<int2 *>(p);
+    p += align_up(sizeof(int2) * (rows + 1));
+    sc.words = reinterpret_cast<uint64_t *>(p);
     return sc;
 }
 
@@ -149,21 +157,33 @@ void launch_indices(const uint8_t *mask, dynconv_shape s, int dilate, const dync
     int64_t rows = static_cast<int64_t>(s.n) * s.h;
     int grid = static_cast<int>((rows + kWavesPerBlock - 1) / kWavesPerBlock);
     launch(mk, k_rowcount, dim3(grid), dim3(kBlock), 0, st, mask, s.n, s.h, s.w, dilate,
-                       sc.rowcnt);
+                       sc.rowcnt, sc.words);
     launch(mk, k_rowscan, dim3(1), dim3(kScanThreads), 0, st, sc.rowcnt, rows, sc.rowoff,
                        idx->counts);
-    launch(mk, k_compact, dim3(grid), dim3(kBlock), 0, st, mask, s.n, s.h, s.w, dilate,
-                       sc.rowoff, idx->active, idx->dilated, idx->nbr);
+    launch(mk, k_compact, dim3(grid), dim3(kBlock), 0, st, static_cast<const uint64_t *>(sc.words),
+                       s.n, s.h, s.w, dilate, sc.rowoff, idx->active, idx->dilated, idx->nbr);
+}
+
+// expansion weights (rows of C+8) and bias staged in LDS when they fit in 64 KiB
+constexpr size_t kMaxDynLds = 64 * 1024;
+template <typename T>
+size_t expand_lds_bytes(int C, int E) {
+    return ((static_cast<size_t>(E) * (C + 8) * sizeof(T) + 15) & ~size_t(15)) + 4 * static_cast<size_t>(E);
 }
 
 template <typename T, bool DENSE, int MAXKS>
 void launch_expand_k(const void *x, dynconv_shape s, const dynconv_block *b, const int32_t *dil,
                      const int32_t *counts, void *h1, hipStream_t st, Marks &mk) {
     int64_t rows = positions(s);
-    launch(mk, k_expand<T, DENSE, MAXKS>, dim3(grid_for_rows(rows)), dim3(kBlock), 0, st,
-                       static_cast<const T *>(x), b->c_in, b->c_hidden,
-                       static_cast<const T *>(b->w_expand), b->b_expand, b->act_expand, dil, counts,
-                       rows, static_cast<T *>(h1));
+    const size_t lds = expand_lds_bytes<T>(b->c_in, b->c_hidden);
+    if (lds <= kMaxDynLds)
+        launch(mk, k_expand<T, DENSE, MAXKS, true>, dim3(grid_for_rows(rows)), dim3(kBlock), lds, st,
+               static_cast<const T *>(x), b->c_in, b->c_hidden, static_cast<const T *>(b->w_expand),
+               b->b_expand, b->act_expand, dil, counts, rows, static_cast<T *>(h1));
+    else
+        launch(mk, k_expand<T, DENSE, MAXKS, false>, dim3(grid_for_rows(rows)), dim3(kBlock), 0, st,
+               static_cast<const T *>(x), b->c_in, b->c_hidden, static_cast<const T *>(b->w_expand),
+               b->b_expand, b->act_expand, dil, counts, rows, static_cast<T *>(h1));
 }
 
 template <typename T, bool DENSE>
@@ -181,8 +201,10 @@ void launch_dw_project_k(const void *h1, const void *x, void *y, dynconv_shape s
                          const dynconv_block *b, const int32_t *act, const int32_t *nbr,
                          const int32_t *counts, hipStream_t st, Marks &mk) {
     int64_t rows = positions(s);
-    size_t lds = sizeof(float) * 10 * static_cast<size_t>(b->c_hidden);
-    launch(mk, k_dw_project<T, DENSE, MAXMT>, dim3(grid_for_rows(rows)), dim3(kBlock), lds,
+    const int64_t groups = (rows + 16 * kDwGroup - 1) / (16 * kDwGroup);
+    const int64_t g = groups < kMaxDwGrid ? (groups < 1 ? 1 : groups) : kMaxDwGrid;
+    const int grid = static_cast<int>((g + 7) / 8 * 8);  // whole groups of 8 (one per XCD)
+    launch(mk, k_dw_project<T, DENSE, MAXMT>, dim3(grid), dim3(kBlock), dw_lds_bytes<T>(),
                        st, static_cast<const T *>(h1), static_cast<const T *>(x), static_cast<T *>(y),
                        s.n, s.h, s.w, s.c, b->c_hidden, static_cast<const T *>(b->w_dw), b->b_dw,
                        b->act_dw, static_cast<const T *>(b->w_project), b->b_project, b->act_project,
@@ -212,11 +234,10 @@ void launch_block(const void *x, void *y, dynconv_shape s, const dynconv_block *
     }
 }
 
-void launch_copy(const void *src, void *dst, size_t bytes, hipStream_t st) {
+void launch_copy(const void *src, void *dst, size_t bytes, hipStream_t st, Marks &mk) {
     int64_t n16 = static_cast<int64_t>(bytes / 16);
     int64_t blocks = (n16 + kBlock - 1) / kBlock;
     int grid = static_cast<int>(blocks < 4096 ? (blocks < 1 ? 1 : blocks) : 4096);
-    Marks mk;
     launch(mk, k_copy16, dim3(grid), dim3(kBlock), 0, st, static_cast<const uint4 *>(src),
            static_cast<uint4 *>(dst), n16);
 }
@@ -377,7 +398,7 @@ void stack_walk(const void *x, void *y, dynconv_shape s, dynconv_dtype dt, const
         void *tb = base + L.tbuf;
         const void *src = x;
         if (in_place && (n_blocks % 2 == 1)) {
-            if (plan.note("k_copy16")) launch_copy(x, tb, bytes, st);  // keeps y free for block 0
+            if (plan.note("k_copy16")) launch_copy(x, tb, bytes, st, mk);  // keeps y free for block 0
             src = tb;
         }
         auto mask_of = [&](int32_t b) -> uint8_t * {
@@ -403,7 +424,7 @@ void stack_walk(const void *x, void *y, dynconv_shape s, dynconv_dtype dt, const
         return;
     }
     // Unfused chain, in place on y.
-    if (!in_place && plan.note("k_copy16")) launch_copy(x, y, bytes, st);
+    if (!in_place && plan.note("k_copy16")) launch_copy(x, y, bytes, st, mk);
     void *h1 = base + L.hidden;
     if (dense) {
         for (int32_t b = 0; b < n_blocks; ++b) {
@@ -517,8 +538,8 @@ dynconv_status dynconv_block_forward(const void *x, void *y, dynconv_shape s, dy
     if (!aligned16(ws)) return DYNCONV_ERR_ALIGN;
     hipStream_t st = static_cast<hipStream_t>(stream);
     (void)hipGetLastError();
-    if (x != y) launch_copy(x, y, bytes, st);
     Marks mk;
+    if (x != y) launch_copy(x, y, bytes, st, mk);
     dispatch_block(dt, x, y, s, blk, idx, ws, st, mk);
     return launch_status();
 }

@@ -218,43 +218,64 @@ k_mask(const T *__restrict__ x, int64_t npix, int C, const float *__restrict__ w
 }
 
 // ------------------------------------------------------ K2 bookkeeping helpers
-__device__ __forceinline__ bool dilated_at(const uint8_t *__restrict__ mask, int n, int h, int w,
-                                           int H, int W, int r) {
-    bool d = false;
-    for (int dh = -r; dh <= r; ++dh) {
-        int hh = h + dh;
-        if (hh < 0 || hh >= H) continue;
-        const uint8_t *mrow = mask + (static_cast<int64_t>(n) * H + hh) * W;
-        for (int dw = -r; dw <= r; ++dw) {
-            int ww = w + dw;
-            if (ww >= 0 && ww < W && mrow[ww]) d = true;
-        }
-    }
-    return d;
-}
-
 __device__ __forceinline__ uint64_t lanemask_lt(int lane) {
     return (lane == 0) ? 0ull : (~0ull >> (64 - lane));
 }
 
-// K2a: one wave per image row (row = n*H + h): counts of active and dilated
-// positions, from 64-lane ballots.
+// Bits of image columns seg*64 .. seg*64+63 that lie inside a row of width W.
+__device__ __forceinline__ uint64_t seg_valid(int seg, int W) {
+    const int n = W - seg * kWave;
+    return (n >= kWave) ? ~0ull : ((1ull << n) - 1ull);
+}
+
+// Horizontal dilation by radius r of segment `seg` of one row, given the
+// row's mask words (bit b of word s = column 64*s + b); columns past the
+// neighbouring segments' edges come from those segments.
+__device__ __forceinline__ uint64_t hdilate(const uint64_t *row, int seg, int nseg, int r, int W) {
+    const uint64_t m = row[seg];
+    const uint64_t lo = (seg > 0) ? row[seg - 1] : 0ull;
+    const uint64_t hi = (seg + 1 < nseg) ? row[seg + 1] : 0ull;
+    uint64_t d = m;
+    for (int k = 1; k <= r; ++k) d |= (m << k) | (lo >> (kWave - k)) | (m >> k) | (hi << (kWave - k));
+    return d & seg_valid(seg, W);
+}
+
+// K2a: one wave per image row (row = n*H + h): the row's mask words (ballots
+// of 64 columns) and its counts of active and dilated positions (the 3x3
+// (radius r) dilation: OR over rows h-r .. h+r of the horizontally dilated
+// words).
 __global__ void __launch_bounds__(kBlock)
-k_rowcount(const uint8_t *__restrict__ mask, int N, int H, int W, int r, int2 *__restrict__ rowcnt) {
+k_rowcount(const uint8_t *__restrict__ mask, int N, int H, int W, int r, int2 *__restrict__ rowcnt,
+           uint64_t *__restrict__ words) {
+    __shared__ uint64_t rows[kWavesPerBlock][7][kMaxSeg];  // rows h-r .. h+r, r <= 3
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int64_t row = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + wave;
-    if (row >= static_cast<int64_t>(N) * H) return;  // uniform per wave
+    if (row >= static_cast<int64_t>(N) * H) return;  // uniform per wave; no block barrier below
     const int n = static_cast<int>(row / H), h = static_cast<int>(row % H);
-    int ca = 0, cd = 0;
-    for (int w0 = 0; w0 < W; w0 += kWave) {
-        const int w = w0 + lane;
-        bool a = false, d = false;
-        if (w < W) {
-            a = mask[row * W + w] != 0;
-            d = dilated_at(mask, n, h, w, H, W, r);
+    const int nseg = (W + kWave - 1) / kWave;
+    for (int q = 0; q <= 2 * r; ++q) {
+        const int hh = h + q - r;
+        for (int seg = 0; seg < nseg; ++seg) {
+            const int w = seg * kWave + lane;
+            const bool a = hh >= 0 && hh < H && w < W && mask[(static_cast<int64_t>(n) * H + hh) * W + w] != 0;
+            const uint64_t b = __ballot(a);
+            if (lane == 0) rows[wave][q][seg] = b;
         }
-        ca += __popcll(__ballot(a));
-        cd += __popcll(__ballot(d));
+    }
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    int ca = 0, cd = 0;
+    for (int seg = lane; seg < nseg; seg += kWave) {
+        uint64_t d = 0;
+        for (int q = 0; q <= 2 * r; ++q) d |= hdilate(rows[wave][q], seg, nseg, r, W);
+        const uint64_t m = rows[wave][r][seg];
+        words[row * nseg + seg] = m;
+        ca += __popcll(m);
+        cd += __popcll(d);
+    }
+    for (int off = 32; off > 0; off >>= 1) {
+        ca += __shfl_down(ca, off);
+        cd += __shfl_down(cd, off);
     }
     if (lane == 0) rowcnt[row] = make_int2(ca, cd);
 }
@@ -301,70 +322,82 @@ k_rowscan(const int2 *__restrict__ rowcnt, int64_t nrows, int2 *__restrict__ row
     }
 }
 
-// K2c: one wave per image row.  The wave first records, for rows h-1, h and
-// h+1, the dilated-mask ballot words of every 64-column segment and their
-// running counts (LDS); then the active and dilated positions of row h get
-// their ranks from ballots, and every active position looks up its 9
+// K2c: one wave per image row.  From the mask words of rows h-1-r .. h+1+r
+// the wave forms the dilated words of rows h-1, h and h+1 and their running
+// per-segment counts (LDS); then the active and dilated positions of row h
+// get their ranks from the words, and every active position finds its 9
 // neighbours' ranks among the dilated positions of the three rows.
 __global__ void __launch_bounds__(kBlock)
-k_compact(const uint8_t *__restrict__ mask, int N, int H, int W, int r,
+k_compact(const uint64_t *__restrict__ words, int N, int H, int W, int r,
           const int2 *__restrict__ rowoff, int32_t *__restrict__ active,
           int32_t *__restrict__ dilated, int32_t *__restrict__ nbr) {
-    __shared__ uint64_t words[kWavesPerBlock][3][kMaxSeg];
+    __shared__ uint64_t dw[kWavesPerBlock][3][kMaxSeg];
     __shared__ int segpre[kWavesPerBlock][3][kMaxSeg];
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int64_t row = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + wave;
-    const bool live = row < static_cast<int64_t>(N) * H;  // uniform per wave
-    const int n = live ? static_cast<int>(row / H) : 0;
-    const int h = live ? static_cast<int>(row % H) : 0;
+    if (row >= static_cast<int64_t>(N) * H) return;  // uniform per wave; no block barrier below
+    const int h = static_cast<int>(row % H);
     const int nseg = (W + kWave - 1) / kWave;
 
-    if (live) {
+    // dilated words of rows h-1, h, h+1 (zero outside the image)
+    for (int seg = lane; seg < nseg; seg += kWave) {
         for (int q = 0; q < 3; ++q) {
-            const int hh = h + q - 1;
-            int pre = 0;
-            for (int seg = 0; seg < nseg; ++seg) {
-                const int w = seg * kWave + lane;
-                bool d = false;
-                if (hh >= 0 && hh < H && w < W) d = dilated_at(mask, n, hh, w, H, W, r);
-                const uint64_t b = __ballot(d);
-                if (lane == 0) {
-                    words[wave][q][seg] = b;
-                    segpre[wave][q][seg] = pre;
+            const int hc = h + q - 1;
+            uint64_t d = 0;
+            if (hc >= 0 && hc < H) {
+                for (int dh = -r; dh <= r; ++dh) {
+                    const int hh = hc + dh;
+                    if (hh < 0 || hh >= H) continue;
+                    const uint64_t *wr = words + (row + (hh - h)) * nseg;
+                    uint64_t m = wr[seg];
+                    const uint64_t lo = (seg > 0) ? wr[seg - 1] : 0ull;
+                    const uint64_t hi = (seg + 1 < nseg) ? wr[seg + 1] : 0ull;
+                    uint64_t x = m;
+                    for (int k = 1; k <= r; ++k)
+                        x |= (m << k) | (lo >> (kWave - k)) | (m >> k) | (hi << (kWave - k));
+                    d |= x;
                 }
-                pre += __popcll(b);
+                d &= seg_valid(seg, W);
             }
+            dw[wave][q][seg] = d;
         }
     }
-    __syncthreads();
-    if (!live) return;
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    if (lane < 3) {  // running counts per segment of rows h-1, h, h+1
+        int pre = 0;
+        for (int seg = 0; seg < nseg; ++seg) {
+            segpre[wave][lane][seg] = pre;
+            pre += __popcll(dw[wave][lane][seg]);
+        }
+    }
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
 
     const int2 base = rowoff[row];
     const uint64_t lt = lanemask_lt(lane);
     int pre_a = 0;
     for (int seg = 0; seg < nseg; ++seg) {
         const int w = seg * kWave + lane;
-        const bool a = (w < W) && mask[row * W + w] != 0;
-        const uint64_t ba = __ballot(a);
-        const uint64_t bd = words[wave][1][seg];
+        const uint64_t ba = words[row * nseg + seg];
+        const uint64_t bd = dw[wave][1][seg];
         const int64_t pix = row * W + w;
-        if ((bd >> lane) & 1ull) {
+        if ((bd >> lane) & 1ull)
             dilated[base.y + segpre[wave][1][seg] + __popcll(bd & lt)] = static_cast<int32_t>(pix);
-        }
-        if (a) {
+        if ((ba >> lane) & 1ull) {
             const int64_t p = base.x + pre_a + __popcll(ba & lt);
             active[p] = static_cast<int32_t>(pix);
             int32_t *out = nbr + p * 9;
 #pragma unroll
             for (int k = 0; k < 9; ++k) {
-                const int dh = k / 3 - 1, dw = k % 3 - 1;
-                const int hh = h + dh, ww = w + dw;
+                const int dh = k / 3 - 1, dwc = k % 3 - 1;
+                const int hh = h + dh, ww = w + dwc;
                 int32_t j = -1;
                 if (hh >= 0 && hh < H && ww >= 0 && ww < W) {
                     const int q = dh + 1, sg = ww / kWave, bit = ww % kWave;
-                    const uint64_t wd = words[wave][q][sg];
+                    const uint64_t wd = dw[wave][q][sg];
                     if ((wd >> bit) & 1ull) {
-                        const uint64_t below = (bit == 0) ? 0ull : (wd & (~0ull >> (64 - bit)));
+                        const uint64_t below = (bit == 0) ? 0ull : (wd & (~0ull >> (kWave - bit)));
                         j = rowoff[row + dh].y + segpre[wave][q][sg] + __popcll(below);
                     }
                 }
@@ -378,17 +411,21 @@ k_compact(const uint8_t *__restrict__ mask, int N, int H, int W, int r,
 // ----------------------------------------------- K3+K4 gather + 1x1 expansion
 // Each wave owns tiles of 16 rows of the intermediate tensor.  The rows' input
 // pixels (dilated[j], or j itself when dense) are loaded straight into the
-// B operand (16 bytes per lane), so the gather costs no extra pass.  For each
+// B operand (16 bytes per lane), so the gather costs no extra pass; the next
+// tile's rows are requested before the current one is computed.  For each
 // 16-channel slice of the hidden layer the wave runs the C-long contraction
 // on the matrix cores (D^T = W1 T^T: hidden channels along M, rows along N),
-// adds the bias, applies the activation and stores 4 consecutive channels per
-// lane.  MAXKS = ceil(C / 32) slices of the contraction stay in registers.
-template <typename T, bool DENSE, int MAXKS>
+// starting from the bias, applies the activation and stores 4 consecutive
+// channels per lane.  With LDSW the expansion weights and bias are staged in
+// LDS once per workgroup (row stride C+8); otherwise the A fragments come
+// from memory.  MAXKS = ceil(C / 32) slices of the contraction.
+template <typename T, bool DENSE, int MAXKS, bool LDSW>
 __global__ void __launch_bounds__(kBlock)
 k_expand(const T *__restrict__ x, int C, int E, const T *__restrict__ w1,
          const float *__restrict__ b1, int act1, const int32_t *__restrict__ dil,
          const int32_t *__restrict__ counts, int64_t dense_rows, T *__restrict__ h1) {
     typedef mma<T> M;
+    extern __shared__ __align__(16) unsigned char ex_lds[];
     // sparse: P_d from the device, clamped to the capacity N*H*W (= dense_rows)
     const int64_t nrows = DENSE ? dense_rows : min(max(static_cast<int64_t>(counts[1]), int64_t{0}), dense_rows);
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
@@ -396,55 +433,111 @@ k_expand(const T *__restrict__ x, int C, int E, const T *__restrict__ w1,
     const int64_t ntiles = (nrows + 15) / 16;
     const int nks = (C + 31) / 32;
     const int nmt = E / 16;
+    const float lo1 = act_lo(act1), hi1 = act_hi(act1);
     // row dense_rows (one past the capacity) stays zero: the depthwise reads it
     // for neighbours outside the image or the dilated list
     if (blockIdx.x == 0)
         for (int e = threadIdx.x; e < E; e += kBlock) h1[dense_rows * E + e] = static_cast<T>(0.0f);
-    for (int64_t t = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + wave; t < ntiles;
-         t += static_cast<int64_t>(gridDim.x) * kWavesPerBlock) {
+    // XCD-aware order: workgroup i runs on XCD i % 8; each XCD walks its own
+    // contiguous range of tiles (gridDim.x is a multiple of 8)
+    const int64_t per_xcd = (ntiles + 7) / 8;
+    const int64_t xcd = blockIdx.x % 8, slot = blockIdx.x / 8, nslot = gridDim.x / 8;
+    if (slot * kWavesPerBlock >= per_xcd) return;  // uniform per workgroup
+    const int cs = C + 8;  // LDS row stride of the weights
+    T *w1s = reinterpret_cast<T *>(ex_lds);
+    float *b1s = reinterpret_cast<float *>(ex_lds + ((static_cast<size_t>(E) * cs * sizeof(T) + 15) & ~size_t(15)));
+    if (LDSW) {
+        constexpr int per16 = 16 / static_cast<int>(sizeof(T));
+        const int vpr = C / per16;
+        for (int i = threadIdx.x; i < E * vpr; i += kBlock) {
+            const int e = i / vpr, k = i % vpr;
+            *reinterpret_cast<uint4 *>(w1s + e * cs + k * per16) =
+                *reinterpret_cast<const uint4 *>(w1 + static_cast<int64_t>(e) * C + k * per16);
+        }
+        for (int e = threadIdx.x; e < E; e += kBlock) b1s[e] = b1[e];
+        __syncthreads();
+    }
+    const int64_t stride = nslot * kWavesPerBlock;  // in tiles of this XCD's range
+    const int64_t t_end = min((xcd + 1) * per_xcd, ntiles);
+    auto load_rows = [&](int64_t t, typename M::frag (&b)[MAXKS]) {
         const int64_t j = t * 16 + r;
-        const bool valid = j < nrows;
+        const bool valid = t < t_end && j < nrows;
         const int64_t pix = valid ? (DENSE ? j : static_cast<int64_t>(dil[j])) : 0;
-        typename M::frag b[MAXKS];
 #pragma unroll
         for (int ks = 0; ks < MAXKS; ++ks) {
             const int c0 = ks * 32 + g * 8;
             b[ks] = (ks < nks && valid && c0 < C) ? M::load(x + pix * C + c0) : M::zero();
         }
+    };
+    int64_t t = xcd * per_xcd + slot * kWavesPerBlock + wave;
+    typename M::frag b[MAXKS];
+    load_rows(t, b);
+    for (; t < t_end; t += stride) {
+        typename M::frag bn[MAXKS];
+        load_rows(t + stride, bn);  // next tile's rows in flight meanwhile
+        const int64_t j = t * 16 + r;
+        const bool valid = j < nrows;
         for (int mt = 0; mt < nmt; ++mt) {
             const int e = mt * 16 + r;
             const int e0 = mt * 16 + 4 * g;
-            floatx4 acc = {b1[e0], b1[e0 + 1], b1[e0 + 2], b1[e0 + 3]};  // bias first
+            floatx4 acc;  // bias first
+            if (LDSW) {
+                acc = *reinterpret_cast<const floatx4 *>(b1s + e0);
+            } else {
+                acc = floatx4{b1[e0], b1[e0 + 1], b1[e0 + 2], b1[e0 + 3]};
+            }
             // Every MFMA is issued unconditionally (slices past C get zero
             // fragments): a branch around an MFMA whose result is read at the
             // join has been compiled without the wait states the read needs.
 #pragma unroll
             for (int ks = 0; ks < MAXKS; ++ks) {
                 const int c0 = ks * 32 + g * 8;
-                typename M::frag a = (ks < nks && c0 < C)
-                    ? M::load(w1 + static_cast<int64_t>(e) * C + c0) : M::zero();
+                typename M::frag a;
+                if (LDSW)
+                    a = (ks < nks && c0 < C) ? M::load(w1s + e * cs + c0) : M::zero();
+                else
+                    a = (ks < nks && c0 < C) ? M::load(w1 + static_cast<int64_t>(e) * C + c0) : M::zero();
                 acc = M::run(a, b[ks], acc);
             }
             if (valid) {
                 float o[4];
 #pragma unroll
-                for (int v = 0; v < 4; ++v) o[v] = activate(acc[v], act1);
+                for (int v = 0; v < 4; ++v) o[v] = clamp_act(acc[v], lo1, hi1);
                 io<T>::store4(h1 + j * E + e0, o);
             }
         }
+#pragma unroll
+        for (int ks = 0; ks < MAXKS; ++ks) b[ks] = bn[ks];
     }
 }
 
 // ------------------------- K5+K6 depthwise + 1x1 projection + scatter-add
-// Each wave owns tiles of 16 active rows.  Lane (r, g) computes the depthwise
-// output of row r for the 8 hidden channels it supplies to the projection's B
-// operand: 9 taps, each a 16-byte load of an expanded row found through the
-// neighbour table (missing neighbours read the all-zero row N*H*W of the
-// expanded tensor, so the loads carry no branch), fp32 accumulation with the
-// folded depthwise weights staged transposed in LDS, bias, activation, rounding
-// to the storage type.  The projection (F^T = W3 H2^T) accumulates over the
-// hidden channels on the matrix cores; the epilogue adds bias and the identity
-// path and writes y at the active position (in place when y == x).
+// A workgroup takes groups of kDwGroup tiles of 16 active rows.  The
+// depthwise of one tile for one 32-channel slice of the hidden layer is a
+// work item; the items of a group are spread over the four waves: lane (r, g)
+// computes the depthwise output of row r for the 8 hidden channels it would
+// supply to the projection's B operand (9 taps, each a 16-byte load of an
+// expanded row found through the neighbour table -- missing neighbours read
+// the all-zero row N*H*W -- fp32 accumulation from the bias with the folded
+// weights staged transposed in LDS, activation, rounding to the storage
+// type) and parks that fragment in LDS.  Then one wave per tile runs the
+// projection (F^T = W3 H2^T) over the slices in order on the matrix cores,
+// starting from the projection bias, and the epilogue adds the identity path
+// and writes y at the active position (in place when y == x).  Hidden slices
+// pass through LDS in chunks of kDwChunk.
+constexpr int kDwGroup = 2;
+constexpr int kDwChunk = 8;
+
+constexpr int kDwChunkCh = kDwChunk * 32;  // hidden channels per chunk
+
+template <typename T>
+__host__ __device__ constexpr size_t dw_lds_bytes() {
+    return 9 * kDwChunkCh * sizeof(T)                                      // w2 of a chunk, [9][256]
+           + 4 * kDwChunkCh                                                // b2 of a chunk
+           + static_cast<size_t>(kDwGroup) * kDwChunk * kWave * sizeof(typename mma<T>::frag)  // fragments
+           + static_cast<size_t>(kDwGroup) * 16 * 10 * 4;                 // positions + neighbour rows
+}
+
 template <typename T, bool DENSE, int MAXMT>
 __global__ void __launch_bounds__(kBlock)
 k_dw_project(const T *__restrict__ h1, const T *x, T *y, int N, int H, int W, int C, int E,
@@ -453,46 +546,80 @@ k_dw_project(const T *__restrict__ h1, const T *x, T *y, int N, int H, int W, in
              const int32_t *__restrict__ act_list, const int32_t *__restrict__ nbr,
              const int32_t *__restrict__ counts) {
     typedef mma<T> M;
-    extern __shared__ float lds[];  // [9][E] depthwise weights, then [E] bias
-    for (int i = threadIdx.x; i < 9 * E; i += kBlock) {
-        const int e = i / 9, k = i % 9;
-        lds[k * E + e] = static_cast<float>(w2[i]);
-    }
-    for (int e = threadIdx.x; e < E; e += kBlock) lds[9 * E + e] = b2[e];
-    __syncthreads();
-
+    typedef typename M::frag Frag;
+    extern __shared__ __align__(16) unsigned char dw_lds[];
     const int64_t HW = static_cast<int64_t>(H) * W;
     const int64_t npos = static_cast<int64_t>(N) * HW;
     // sparse: P from the device, clamped to the capacity N*H*W
     const int64_t nrows = DENSE ? npos : min(max(static_cast<int64_t>(counts[0]), int64_t{0}), npos);
+    constexpr int GR = kDwGroup * 16;  // rows per group
+    const int64_t ngroups = (nrows + GR - 1) / GR;
+    if ((blockIdx.x / 8) >= (ngroups + 7) / 8) return;  // no group on this slot (uniform)
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int r = lane % 16, g = lane / 16;
-    const int64_t ntiles = (nrows + 15) / 16;
-    const int nks = (E + 31) / 32;
+    const int nsl = (E + 31) / 32;
     const int nmt = (C + 15) / 16;
-    for (int64_t t = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + wave; t < ntiles;
-         t += static_cast<int64_t>(gridDim.x) * kWavesPerBlock) {
-        const int64_t p = t * 16 + r;
-        const bool valid = p < nrows;
-        int64_t pix = 0;
-        int32_t nb[9];
-        if (DENSE) {
-            pix = valid ? p : 0;
-            const int hh0 = static_cast<int>((pix / W) % H), ww0 = static_cast<int>(pix % W);
+    const float lo2 = act_lo(act2), hi2 = act_hi(act2);
+    const float lo3 = act_lo(act3), hi3 = act_hi(act3);
+
+    T *w2t = reinterpret_cast<T *>(dw_lds);  // [9][kDwChunkCh]: the chunk's taps, transposed
+    size_t off = 9 * kDwChunkCh * sizeof(T);
+    float *b2s = reinterpret_cast<float *>(dw_lds + off);
+    off += 4 * kDwChunkCh;
+    Frag *fr = reinterpret_cast<Frag *>(dw_lds + off);  // [kDwGroup][kDwChunk][64]
+    off += static_cast<size_t>(kDwGroup) * kDwChunk * kWave * sizeof(Frag);
+    int32_t *gpix = reinterpret_cast<int32_t *>(dw_lds + off);  // [GR]
+    int32_t *gnb = gpix + GR;                                   // [GR][9]
+    // depthwise weights and bias of hidden channels e_base .. e_base+255
+    auto stage_chunk = [&](int e_base) {
+        const int ne = min(kDwChunkCh, E - e_base);
+        for (int i = threadIdx.x; i < 9 * ne; i += kBlock) {
+            const int e = i / 9, k = i % 9;
+            w2t[k * kDwChunkCh + e] = w2[static_cast<int64_t>(e_base) * 9 + i];
+        }
+        for (int e = threadIdx.x; e < ne; e += kBlock) b2s[e] = b2[e_base + e];
+    };
+    const bool one_chunk = nsl <= kDwChunk;
+    if (one_chunk) stage_chunk(0);  // visible after the group's first barrier
+
+    // XCD-aware order: workgroup i runs on XCD i % 8; each XCD walks its own
+    // contiguous range of groups, so the rows a group's taps read (the
+    // previous and next image rows) were just expanded or read on that XCD
+    // and sit in its L2.  gridDim.x is a multiple of 8.
+    const int64_t per_xcd = (ngroups + 7) / 8;
+    const int64_t xcd = blockIdx.x % 8, slot = blockIdx.x / 8, nslot = gridDim.x / 8;
+    for (int64_t k = slot; k < per_xcd; k += nslot) {
+        const int64_t grp = xcd * per_xcd + k;
+        if (grp >= ngroups) break;  // uniform per workgroup
+        const int64_t p0 = grp * GR;
+        const int gt = static_cast<int>(min(static_cast<int64_t>(kDwGroup), (nrows - p0 + 15) / 16));
+        // positions and neighbour rows of the group (missing: the zero row)
+        for (int i = threadIdx.x; i < GR; i += kBlock) {
+            const int64_t p = p0 + i;
+            const bool valid = p < nrows;
+            const int64_t pix = valid ? (DENSE ? p : static_cast<int64_t>(act_list[p])) : -1;
+            gpix[i] = static_cast<int32_t>(pix);
+            if (DENSE) {
+                const int hh0 = valid ? static_cast<int>((pix / W) % H) : 0;
+                const int ww0 = valid ? static_cast<int>(pix % W) : 0;
 #pragma unroll
-            for (int k = 0; k < 9; ++k) {
-                const int dh = k / 3 - 1, dw = k % 3 - 1;
-                const bool in = valid && hh0 + dh >= 0 && hh0 + dh < H && ww0 + dw >= 0 && ww0 + dw < W;
-                nb[k] = in ? static_cast<int32_t>(pix + dh * W + dw) : static_cast<int32_t>(npos);
-            }
-        } else {
-            pix = valid ? static_cast<int64_t>(act_list[p]) : 0;
+                for (int k = 0; k < 9; ++k) {
+                    const int dh = k / 3 - 1, dwc = k % 3 - 1;
+                    const bool in = valid && hh0 + dh >= 0 && hh0 + dh < H && ww0 + dwc >= 0 && ww0 + dwc < W;
+                    gnb[i * 9 + k] = in ? static_cast<int32_t>(pix + dh * W + dwc) : static_cast<int32_t>(npos);
+                }
+            } else {
 #pragma unroll
-            for (int k = 0; k < 9; ++k) {
-                const int32_t q = valid ? nbr[p * 9 + k] : -1;
-                nb[k] = (q >= 0) ? q : static_cast<int32_t>(npos);  // missing: the zero row
+                for (int k = 0; k < 9; ++k) {
+                    const int32_t q = valid ? nbr[p * 9 + k] : -1;
+                    gnb[i * 9 + k] = (q >= 0) ? q : static_cast<int32_t>(npos);
+                }
             }
         }
+        __syncthreads();
+        // the projection wave's tile (waves past the group's tiles repeat the
+        // last one, so every wave issues the same MFMAs; only real tiles store)
+        const int pt = min(wave, gt - 1);
         floatx4 acc[MAXMT];  // projection bias first
 #pragma unroll
         for (int mt = 0; mt < MAXMT; ++mt) {
@@ -500,38 +627,57 @@ k_dw_project(const T *__restrict__ h1, const T *x, T *y, int N, int H, int W, in
 #pragma unroll
             for (int v = 0; v < 4; ++v) acc[mt][v] = (mt < nmt && c0 < C) ? b3[c0 + v] : 0.0f;
         }
-
-        for (int ks = 0; ks < nks; ++ks) {
-            const int e0 = ks * 32 + g * 8;
-            const bool ein = e0 < E;
-            float hv[8];
+        for (int s0 = 0; s0 < nsl; s0 += kDwChunk) {
+            const int ns = min(kDwChunk, nsl - s0);
+            if (!one_chunk) {
+                stage_chunk(s0 * 32);
+                __syncthreads();
+            }
+            // depthwise items (tile, slice) of this chunk
+            for (int it = wave; it < gt * ns; it += kWavesPerBlock) {
+                const int t = it % gt, sl = it / gt;
+                const int q = t * 16 + r;
+                const int e0 = (s0 + sl) * 32 + g * 8;
+                float hv[8];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) hv[u] = 0.0f;
-            if (ein && valid) {
-                float s[8];  // depthwise bias first, then the taps in order
+                for (int u = 0; u < 8; ++u) hv[u] = 0.0f;
+                if (e0 < E && gpix[q] >= 0) {
+                    const int el = e0 - s0 * 32;  // channel within the chunk
+                    typename io<T>::vec8 tv[9];
 #pragma unroll
-                for (int u = 0; u < 8; ++u) s[u] = lds[9 * E + e0 + u];
+                    for (int k = 0; k < 9; ++k)  // branch free: missing taps read zeros
+                        tv[k] = io<T>::raw8(h1 + static_cast<int64_t>(gnb[q * 9 + k]) * E + e0);
+                    float sacc[8];  // depthwise bias first, then the taps in order
 #pragma unroll
-                for (int k = 0; k < 9; ++k) {  // branch free: missing taps read zeros
-                    float v[8];
-                    io<T>::load8(h1 + static_cast<int64_t>(nb[k]) * E + e0, v);
-                    const float *wk = lds + k * E + e0;
+                    for (int u = 0; u < 8; ++u) sacc[u] = b2s[el + u];
 #pragma unroll
-                    for (int u = 0; u < 8; ++u) s[u] = __builtin_fmaf(wk[u], v[u], s[u]);
+                    for (int k = 0; k < 9; ++k) {
+                        const typename io<T>::vec8 wk = io<T>::raw8(w2t + k * kDwChunkCh + el);
+#pragma unroll
+                        for (int u = 0; u < 8; ++u)
+                            sacc[u] = __builtin_fmaf(static_cast<float>(wk[u]), static_cast<float>(tv[k][u]), sacc[u]);
+                    }
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) hv[u] = clamp_act(sacc[u], lo2, hi2);
                 }
-#pragma unroll
-                for (int u = 0; u < 8; ++u) hv[u] = activate(s[u], act2);
+                fr[(t * kDwChunk + sl) * kWave + lane] = M::pack(hv);
             }
-            const typename M::frag bf = M::pack(hv);
+            __syncthreads();
+            for (int sl = 0; sl < ns; ++sl) {
+                const Frag bf = fr[(pt * kDwChunk + sl) * kWave + lane];
+                const int e0 = (s0 + sl) * 32 + g * 8;
 #pragma unroll
-            for (int mt = 0; mt < MAXMT; ++mt) {  // unconditional MFMAs, as in k_expand
-                const int c = mt * 16 + r;
-                typename M::frag a = (mt < nmt && ein && c < C)
-                    ? M::load(w3 + static_cast<int64_t>(c) * E + e0) : M::zero();
-                acc[mt] = M::run(a, bf, acc[mt]);
+                for (int mt = 0; mt < MAXMT; ++mt) {  // unconditional MFMAs, as in k_expand
+                    const int c = mt * 16 + r;
+                    const Frag a = (mt < nmt && e0 < E && c < C) ? M::load(w3 + static_cast<int64_t>(c) * E + e0)
+                                                                  : M::zero();
+                    acc[mt] = M::run(a, bf, acc[mt]);
+                }
             }
+            __syncthreads();
         }
-        if (valid) {
+        const int64_t pix = gpix[pt * 16 + r];
+        if (wave < gt && pix >= 0) {
 #pragma unroll
             for (int mt = 0; mt < MAXMT; ++mt) {
                 const int c0 = mt * 16 + 4 * g;
@@ -539,11 +685,12 @@ k_dw_project(const T *__restrict__ h1, const T *x, T *y, int N, int H, int W, in
                     float xv[4], o[4];
                     io<T>::load4(x + pix * C + c0, xv);
 #pragma unroll
-                    for (int v = 0; v < 4; ++v) o[v] = xv[v] + activate(acc[mt][v], act3);
+                    for (int v = 0; v < 4; ++v) o[v] = xv[v] + clamp_act(acc[mt][v], lo3, hi3);
                     io<T>::store4(y + pix * C + c0, o);
                 }
             }
         }
+        __syncthreads();  // gpix / gnb are rewritten for the next group
     }
 }
 

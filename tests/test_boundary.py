@@ -78,7 +78,7 @@ def test_mask_validation(lib):
 def test_build_indices_validation(lib):
     s = dc.Shape(2, 8, 8, 0)
     need = lib.dynconv_indices_workspace_bytes(s)
-    assert need == 256 + 256  # 16 rows of int2 counts, 17 of offsets, each 256-aligned
+    assert need == 256 + 256 + 256  # 16 rows of int2 counts, 17 of offsets, 16 mask words; 256-aligned
     idx = dc.Indices(FAKE, FAKE, FAKE, FAKE, 128)
     f = lib.dynconv_build_indices
     assert f(None, s, 1, ctypes.byref(idx), FAKE, need, None) == ERR_NULL
@@ -139,7 +139,7 @@ def test_stack_validation(lib):
     # kernel chain: mask, lists, counts, row scratch, hidden tensor of the widest block
     need = lib.dynconv_stack_workspace_bytes(s, blocks, 3, 1, 2)
     assert need == (npos + 4 * npos + 4 * npos + 36 * npos + up(8 * 3) + up(8 * rows)
-                    + up(8 * (rows + 1)) + up((npos + 1) * 192 * 2))
+                    + up(8 * (rows + 1)) + up(8 * rows) + up((npos + 1) * 192 * 2))
     # more than 64 channels always take the kernel chain
     wide_c = dc.Shape(1, 4, 100, 72)
     blocks72 = (dc.Block * 1)(fake_block(C=72))
