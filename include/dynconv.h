@@ -203,12 +203,14 @@ size_t dynconv_stack_workspace_bytes(dynconv_shape s, const dynconv_block *blks,
  * all positions (the baseline of Eq. 1).
  *
  * Execution: when s.c <= 64 and DYNCONV_STACK_UNFUSED is not set, each
- * block is ONE kernel over small patches of the image (at most 128
+ * block is ONE kernel over small patches of the image (at most 256
  * positions, at most 32 columns wide), each of which builds the active and
  * halo lists of its patch on chip (ballot ranks in raster order), gathers,
  * expands, runs the depthwise and the projection, adds the identity path and
- * computes the next block's mask; blocks alternate between y and a workspace
- * copy.  Otherwise the block runs the kernel chain of the per-block calls,
+ * computes the next block's mask (the first block also runs its own mask
+ * unit); blocks alternate between y and a workspace copy.  The per-block
+ * counts P, P_d take one more small kernel, launched only when counts is not
+ * NULL.  Otherwise the block runs the kernel chain of the per-block calls,
  * in place on y.  Both give identical masks, counts and outputs: the same
  * arithmetic in the same order.
  *   x      (device) NHWC input, shape s, dtype dt; read only unless y == x
@@ -229,7 +231,9 @@ dynconv_status dynconv_stack_forward(const void *x, void *y, dynconv_shape s, dy
  * Launch sequence of dynconv_stack_forward, for profiling: stores up to `cap`
  * kernel names (static strings) in launch order into `names` (may be NULL
  * when cap is 0) and returns the number of launches, or -1 for invalid
- * arguments.  in_place says whether the call will have y == x.
+ * arguments.  in_place says whether the call will have y == x.  The count
+ * reduction (k_band_counts, last) is listed as if counts were requested; a
+ * call without counts skips it and leaves its event pair unused.
  */
 int32_t dynconv_stack_launch_names(dynconv_shape s, const dynconv_block *blks, int32_t n_blocks,
                                    dynconv_dtype dt, int32_t flags, int32_t in_place,

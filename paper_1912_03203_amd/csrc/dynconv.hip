@@ -268,39 +268,50 @@ int fused_patch_count(dynconv_shape s, dynconv_dtype dt) {
     return s.n * p.nph * p.npw;
 }
 
+// Per-launch mask plumbing of one fused block: where its mask comes from
+// (mask_in, or computed in the kernel with the block's own mask unit and
+// written to mask_self), where the next block's mask goes, and where the
+// patches' active and dilated counts go.
+struct FusedMasks {
+    const uint8_t *mask_in = nullptr;
+    bool self = false;
+    uint8_t *mask_self = nullptr;
+    uint8_t *mask_next = nullptr;
+    int32_t *band_counts = nullptr;
+};
+
 template <typename T, bool DENSE, int MAXKS, int MAXMT, int MAXC>
 void launch_fused_k(const void *src, void *dst, dynconv_shape s, const dynconv_block *b,
-                    const uint8_t *mask_in, const dynconv_block *next, uint8_t *mask_next,
-                    int32_t *counts, hipStream_t st, Marks &mk) {
+                    const dynconv_block *next, const FusedMasks &fm, hipStream_t st, Marks &mk) {
     typedef typename PatchCfgOf<T, MAXC>::type CFG;
     const PatchGeom p = fused_geom_t<T, MAXC>(s);
     const int npatch = s.n * p.nph * p.npw;
     const int grid = (npatch + 7) / 8 * 8;  // whole groups of 8 (one per XCD)
     launch(mk, k_block_fused<T, DENSE, MAXKS, MAXMT, MAXC, CFG>, dim3(grid), dim3(CFG::kThreads), 0, st,
            static_cast<const T *>(src), static_cast<T *>(dst), s.n, s.h, s.w, s.c, b->c_hidden, p.R, p.Wu,
-           mask_in, static_cast<const T *>(b->w_expand), b->b_expand, b->act_expand,
+           fm.mask_in, fm.self ? b->w_mask : nullptr, b->b_mask, fm.mask_self,
+           static_cast<const T *>(b->w_expand), b->b_expand, b->act_expand,
            static_cast<const T *>(b->w_dw), b->b_dw, b->act_dw,
            static_cast<const T *>(b->w_project), b->b_project, b->act_project,
            next ? next->w_mask : nullptr, next ? next->b_mask : 0.0f,
-           next ? mask_next : nullptr, counts);
+           next ? fm.mask_next : nullptr, fm.band_counts);
 }
 
 template <typename T, bool DENSE>
 void launch_fused(const void *src, void *dst, dynconv_shape s, const dynconv_block *b,
-                  const uint8_t *mask_in, const dynconv_block *next, uint8_t *mask_next,
-                  int32_t *counts, hipStream_t st, Marks &mk) {
+                  const dynconv_block *next, const FusedMasks &fm, hipStream_t st, Marks &mk) {
     if (s.c <= 32)
-        launch_fused_k<T, DENSE, 1, 2, 32>(src, dst, s, b, mask_in, next, mask_next, counts, st, mk);
+        launch_fused_k<T, DENSE, 1, 2, 32>(src, dst, s, b, next, fm, st, mk);
     else
-        launch_fused_k<T, DENSE, 2, 4, 64>(src, dst, s, b, mask_in, next, mask_next, counts, st, mk);
+        launch_fused_k<T, DENSE, 2, 4, 64>(src, dst, s, b, next, fm, st, mk);
 }
 
 void dispatch_fused(dynconv_dtype dt, bool dense, const void *src, void *dst, dynconv_shape s,
-                    const dynconv_block *b, const uint8_t *mask_in, const dynconv_block *next,
-                    uint8_t *mask_next, int32_t *counts, hipStream_t st, Marks &mk) {
-#define DC_FUSED(T)                                                                          \
-    (dense ? launch_fused<T, true>(src, dst, s, b, nullptr, nullptr, nullptr, nullptr, st, mk) \
-           : launch_fused<T, false>(src, dst, s, b, mask_in, next, mask_next, counts, st, mk))
+                    const dynconv_block *b, const dynconv_block *next, const FusedMasks &fm,
+                    hipStream_t st, Marks &mk) {
+#define DC_FUSED(T)                                                                  \
+    (dense ? launch_fused<T, true>(src, dst, s, b, nullptr, FusedMasks{}, st, mk)    \
+           : launch_fused<T, false>(src, dst, s, b, next, fm, st, mk))
     if (dt == DYNCONV_F32) DC_FUSED(float);
     else if (dt == DYNCONV_F16) DC_FUSED(half_t);
     else DC_FUSED(bf16_t);
@@ -407,18 +418,20 @@ void stack_walk(const void *x, void *y, dynconv_shape s, dynconv_dtype dt, const
         };
         const int nbands = fused_patch_count(s, dt);
         int32_t *band_counts = reinterpret_cast<int32_t *>(base + L.bands);
-        if (!dense && plan.note("k_mask"))
-            dispatch_mask(dt, src, s, blks[0].w_mask, blks[0].b_mask, mask_of(0), nullptr, st, mk);
         for (int32_t b = 0; b < n_blocks; ++b) {
             void *dst = ((n_blocks - 1 - b) % 2 == 0) ? y : tb;
             const dynconv_block *next = (b + 1 < n_blocks) ? &blks[b + 1] : nullptr;
-            if (plan.note("k_block_fused"))
-                dispatch_fused(dt, dense, src, dst, s, &blks[b], mask_of(b), next,
-                               next ? mask_of(b + 1) : nullptr,
-                               band_counts + static_cast<size_t>(2) * nbands * b, st, mk);
+            FusedMasks fm;
+            fm.self = (b == 0);  // block 0 runs its own mask unit on the staged x
+            fm.mask_in = (b == 0) ? nullptr : mask_of(b);
+            fm.mask_self = mask_of(0);
+            fm.mask_next = next ? mask_of(b + 1) : nullptr;
+            fm.band_counts = band_counts + static_cast<size_t>(2) * nbands * b;
+            if (plan.note("k_block_fused")) dispatch_fused(dt, dense, src, dst, s, &blks[b], next, fm, st, mk);
             src = dst;
         }
-        if (!dense && plan.note("k_band_counts"))
+        // P, P_d per block only on request (listed in every plan)
+        if (!dense && (counts || !plan.exec) && plan.note("k_band_counts"))
             launch(mk, k_band_counts, dim3(n_blocks), dim3(kBlock), 0, st,
                    static_cast<const int32_t *>(band_counts), nbands, cnt_all);
         return;

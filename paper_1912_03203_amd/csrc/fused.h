@@ -33,6 +33,8 @@
 // Input and output must be different buffers: neighbouring patches read the
 // positions next to this one as their ring.  Patch i writes its active and
 // dilated counts to band_counts[2i], [2i+1]; k_band_counts sums them.
+// The first block of a stack may compute its own mask (wm_self) from the
+// staged x instead of reading one.
 #pragma once
 
 #include "kernels.h"
@@ -223,6 +225,7 @@ template <typename T, bool DENSE, int MAXKS, int MAXMT, int MAXC, class CFG>
 __global__ void __launch_bounds__(CFG::kThreads) __attribute__((amdgpu_waves_per_eu(CFG::kWpe)))
 k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int W, int C, int E,
               int R, int Wu, const uint8_t *__restrict__ mask_in,
+              const float *__restrict__ wm_self, float bm_self, uint8_t *__restrict__ mask_self,
               const T *__restrict__ w1, const float *__restrict__ b1, int act1,
               const T *__restrict__ w2, const float *__restrict__ b2, int act2,
               const T *__restrict__ w3, const float *__restrict__ b3, int act3,
@@ -237,10 +240,10 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
     const int wave = tid / kWave, lane = tid % kWave;
     const int r = lane % 16, g = lane / 16;
 
-    // Patch index, XCD-aware: workgroup i runs on XCD i % 8, so consecutive
-    // patches (which share ring rows and columns) go to the same XCD.
     const int nph = (H + R - 1) / R, npw = (W + Wu - 1) / Wu;
     const int npatch = N * nph * npw;
+    // XCD-aware: workgroup i runs on XCD i % 8, so consecutive patches
+    // (which share ring rows and columns) go to the same XCD.
     const int per_xcd = (npatch + 7) / 8;
     const int patch = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
     if (patch >= npatch) return;  // uniform per workgroup
@@ -290,11 +293,32 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
     }
 
     // ---- 1. mask words, dilation, lists
+    if (!DENSE && wm_self) __syncthreads();  // the region's x, for the block's own mask unit
     for (int rr = wave; rr < nreg; rr += NW) {
         const int hh = h0 - 1 + rr;
         bool bit = false;
-        if (hh >= 0 && hh < H && lane < WP && ((img_cols >> lane) & 1ull))
-            bit = DENSE ? true : mask_in[(img + hh) * W + (w0 - 1 + lane)] != 0;
+        if (hh >= 0 && hh < H && lane < WP && ((img_cols >> lane) & 1ull)) {
+            if (DENSE) {
+                bit = true;
+            } else if (wm_self) {
+                // the mask unit (Eq. 2, Eq. 8 at zero noise) on the staged x: the
+                // fp32 multiply-add chain of k_mask, channels ascending from +0,
+                // then the bias, strict threshold
+                const T *row = &L.xs[rr * WP + lane][0];
+                float a = 0.0f;
+                for (int c0 = 0; c0 < C; c0 += 8) {
+                    float v[8];
+                    io<T>::load8(row + c0, v);
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) a = __builtin_fmaf(wm_self[c0 + u], v[u], a);
+                }
+                bit = (a + bm_self) > 0.0f;
+                if (mask_self && rr >= 1 && rr <= rows_out && lane >= 1 && lane <= cols_out)
+                    mask_self[(img + hh) * W + (w0 - 1 + lane)] = bit ? 1 : 0;
+            } else {
+                bit = mask_in[(img + hh) * W + (w0 - 1 + lane)] != 0;
+            }
+        }
         const uint64_t b = __ballot(bit);
         if (lane == 0) L.gw[rr] = b;
     }

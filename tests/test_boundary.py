@@ -163,9 +163,9 @@ def test_stack_validation(lib):
     assert f(FAKE, FAKE, s, 1, nomask, 1, 0, None, None, FAKE, need1, None) == ERR_NULL
     assert lib.dynconv_stack_workspace_bytes(s, blocks, 0, 1, 0) == 0
     pf = lib.dynconv_stack_forward_profiled
-    ev = (ctypes.c_void_p * 8)(*([FAKE] * 8))
-    # 1 mask launch + 3 block launches + 1 count reduction need 10 events
-    assert pf(FAKE, FAKE, s, 1, blocks, 3, 0, None, None, FAKE, fused, None, ev, 8) == ERR_ARG
+    ev = (ctypes.c_void_p * 6)(*([FAKE] * 6))
+    # 3 block launches (the first runs its own mask unit) + 1 count reduction need 8 events
+    assert pf(FAKE, FAKE, s, 1, blocks, 3, 0, None, None, FAKE, fused, None, ev, 6) == ERR_ARG
     assert pf(FAKE, FAKE, s, 1, blocks, 3, 0, None, None, FAKE, fused, None, None, 8) == ERR_NULL
 
 
@@ -179,14 +179,13 @@ def test_stack_launch_plans(lib):
         lib.dynconv_stack_launch_names(shape, arr, n, 1, flags, in_place, out, total)
         return [x.decode() for x in out]
 
-    assert names(0, 0) == ["k_mask"] + ["k_block_fused"] * 8 + ["k_band_counts"]
+    assert names(0, 0) == ["k_block_fused"] * 8 + ["k_band_counts"]
     assert names(1, 1) == ["k_block_fused"] * 8
-    assert names(0, 1, n=3) == ["k_copy16", "k_mask"] + ["k_block_fused"] * 3 + ["k_band_counts"]
+    assert names(0, 1, n=3) == ["k_copy16"] + ["k_block_fused"] * 3 + ["k_band_counts"]
     assert names(2, 1) == ["k_mask", "k_rowcount", "k_rowscan", "k_compact", "k_expand",
                            "k_dw_project"] * 8
     assert names(3, 0) == ["k_copy16"] + ["k_expand", "k_dw_project"] * 8
-    assert names(0, 1, shape=dc.Shape(2, 8, 300, 32), n=2) == ["k_mask"] + ["k_block_fused"] * 2 + \
-        ["k_band_counts"]
+    assert names(0, 1, shape=dc.Shape(2, 8, 300, 32), n=2) == ["k_block_fused"] * 2 + ["k_band_counts"]
     arr72 = (dc.Block * 2)(*([fake_block(C=72)] * 2))
     total = lib.dynconv_stack_launch_names(dc.Shape(2, 8, 8, 72), arr72, 2, 1, 0, 1, None, 0)
     out = (ctypes.c_char_p * total)()

@@ -68,7 +68,7 @@ def test_fused_block_parity(case):
     wts = inputs.block_weights(rng, C, E, dtype=dtype)
     o = util.oracle_calibrated_block(x, wts, density, dtype)
     g = run_stack(x, [wts], [o["b_m"]], dtype)
-    assert g["names"] == ["k_mask", "k_block_fused", "k_band_counts"]
+    assert g["names"] == ["k_block_fused", "k_band_counts"]
     assert g["masks"][0].cpu().numpy().tobytes() == o["G"].tobytes()
     assert tuple(int(v) for v in g["counts"][0].cpu()) == (o["A"].size, o["D"].size)
     check_block_output(host(g["y"]), x, o["y"], o["G"], dtype)
