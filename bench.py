@@ -23,6 +23,8 @@ Also reported on the same JSON line:
                 bounded sample of the same workload
   sweep         per-block latency of the 32 x 56x56x24 (hidden 144) fp16 block
                 at densities 0.1 .. 0.9, sparse and dense
+  chain         the same stack through the kernel chain (the per-block calls'
+                kernels), sparse and dense, with per-kernel HBM fractions
 """
 from __future__ import annotations
 
@@ -294,6 +296,38 @@ def cpu_baseline(inputs, wl, x0_np, blocks_np, density, budget_s=12.0):
                       "gather/scatter block; fp64 C loops, one thread); %.1f s" % (S, wl.n, len(blocks_np), t)}
 
 
+def chain_report(dc, torch, wl, x0, sparse_blocks, dense_blocks, counts, use_graph, steps, warmup,
+                 profile_steps):
+    """The same stack through the kernel chain (mask, row counts, row scan,
+    compaction, gather+expand, depthwise+project+scatter; and expand +
+    depthwise-project over all positions for dense): step times and, per
+    kernel, the average duration, algorithmic bytes and HBM fraction."""
+    sp = Runner(dc, torch, x0, sparse_blocks, dc.STACK_UNFUSED, use_graph, wl.blocks)
+    dn = Runner(dc, torch, x0, dense_blocks, dc.STACK_UNFUSED | dc.STACK_DENSE, use_graph, wl.blocks)
+    t_sp = sp.timed(steps, warmup)
+    t_dn = dn.timed(steps, warmup)
+    c_chain = sp.read_counts().cpu().numpy()
+    if not np.array_equal(c_chain, counts):
+        raise RuntimeError("kernel chain and one-launch blocks disagree on the counts")
+    s = 2 if wl.dtype != "f32" else 4
+    rows = wl.n * wl.h
+    out = {"sparse_ms_per_step": 1e3 * t_sp, "dense_ms_per_step": 1e3 * t_dn, "speedup_vs_dense": t_dn / t_sp,
+           "sparse_images_per_s": wl.n / t_sp, "kernels": {}}
+    for tag, runner, dense in (("sparse", sp, False), ("dense", dn, True)):
+        prof, _ = profile_kernels(dc, torch, runner, profile_steps)
+        for k, v in prof.items():
+            if dense:
+                b = float(algorithmic_bytes(k, True, s, wl.c, wl.e, wl.nhw, rows, wl.nhw, wl.nhw))
+            else:
+                b = float(np.mean([algorithmic_bytes(k, False, s, wl.c, wl.e, wl.nhw, rows, int(P), int(Pd))
+                                   for P, Pd in counts]))
+            gbs = b / (v["avg_us"] * 1e-6) / 1e9
+            out["kernels"]["%s %s" % (k, tag)] = {"avg_us": v["avg_us"], "launches": v["launches"],
+                                                  "algorithmic_bytes": b, "gbs": gbs,
+                                                  "hbm_frac": gbs / HBM_PEAK_GBS}
+    return out
+
+
 def density_sweep(dc, inputs, torch, steps, warmup, use_graph, flags):
     wl = inputs.WORKLOADS["mbv2_stage2_block_56x56x24_f16"]
     x_np, blocks_np, _ = inputs.make_block_inputs(wl, 0)
@@ -424,6 +458,7 @@ def main():
     ap.add_argument("--unfused", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-sweep", action="store_true")
+    ap.add_argument("--no-chain", action="store_true", help="skip the kernel-chain report")
     ap.add_argument("--profile-steps", type=int, default=20)
     ap.add_argument("--traffic-pass", action="store_true",
                     help="untimed launches for an HBM-counter run: a plain copy of known size, "
@@ -548,6 +583,10 @@ def main():
     if rec is not None:
         result["roofline"]["traffic"] = rec["sparse_bytes"]
         result["roofline"]["traffic_dense"] = rec["dense_bytes"]
+    if not args.no_chain and not args.unfused:
+        log("kernel chain")
+        result["chain"] = chain_report(dc, torch, wl, x0, sparse_blocks, dense_blocks, counts, use_graph,
+                                       min(args.steps, 50), min(args.warmup, 5), args.profile_steps)
     if not args.no_sweep:
         log("density sweep")
         result["sweep"] = density_sweep(dc, inputs, torch, min(args.steps, 100), min(args.warmup, 10),
