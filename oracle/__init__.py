@@ -196,3 +196,38 @@ def block_forward(x_nchw, wts, w_m, b_m, dilate_r=1):
     A, D, nbr = indices(G, Gd, N, H, W)
     y, _, _ = block_dense(x, wts, G)
     return {"G": G, "Gd": Gd, "A": A, "D": D, "nbr": nbr, "logits": logits, "y": y}
+
+
+def channel_shuffle2(z_nchw):
+    """Channel shuffle with two groups (ShuffleNetV2): view the channels as a
+    2 x (C/2) matrix, transpose it, flatten; output channel 2k is input
+    channel k, output channel 2k+1 is input channel C/2 + k."""
+    z = np.asarray(z_nchw)
+    N, C, H, W = z.shape
+    assert C % 2 == 0
+    return z.reshape(N, 2, C // 2, H, W).transpose(0, 2, 1, 3, 4).reshape(N, C, H, W)
+
+
+def shuffle_unit_forward(x_nchw, wts, w_m, b_m, dilate_r=1):
+    """ShuffleNetV2 stride-1 unit whose convolutional branch is a gated
+    residual block (Sec. 4.1.2: dynamic convolutions in the branch of the
+    non-strided units of ShuffleNetV2 with a residual connection).
+
+    The input's channels split into halves x1 | x2.  The branch is the gated
+    block of Eq. 3 on x2, with its own mask unit on x2:
+        b = x2 + G o F(x2),  F = 1x1 -> DW 3x3 -> 1x1 with the activations in
+        wts["acts"] (ShuffleNetV2: ReLU, none, ReLU);
+    then y = channel_shuffle(concat(x1, b), 2).
+
+    Returns dict with G, A, D, nbr (of the branch) and y [N, C, H, W] fp64."""
+    x = np.asarray(x_nchw)
+    N, C, H, W = x.shape
+    assert C % 2 == 0
+    cb = C // 2
+    x1 = np.asarray(x[:, :cb], np.float64)
+    x2 = np.ascontiguousarray(x[:, cb:])
+    r = block_forward(x2, wts, w_m, b_m, dilate_r)
+    y = channel_shuffle2(np.concatenate([x1, r["y"]], axis=1))
+    out = dict(r)
+    out["y"] = y
+    return out
