@@ -255,6 +255,62 @@ dynconv_status dynconv_stack_forward_profiled(const void *x, void *y, dynconv_sh
                                               void *stream, void *const *events,
                                               int32_t n_events);
 
+/*
+ * ShuffleNetV2 stride-1 units whose convolutional branch is a gated residual
+ * block (Sec. 4.1.2: dynamic convolutions in the branch of the non-strided
+ * units of ShuffleNetV2 with a residual connection; the branch is Eq. 3 with
+ * r = identity).  With cb = s.c / 2, unit u maps its input x_u to
+ *   x1 = x_u[..., 0 .. cb-1],  x2 = x_u[..., cb .. 2cb-1]
+ *   mask_u = dynconv_mask(x2 zero-extended to cp channels, branches[u].w_mask,
+ *                         branches[u].b_mask)
+ *   b  = x2 + F(x2) where mask_u is 1, b = x2 elsewhere, with F the branch
+ *        block (expand, depthwise 3x3, project with its activations;
+ *        ShuffleNetV2: RELU, NONE, RELU) on x2 zero-extended to cp channels,
+ *        of which the first cb outputs are kept
+ *   x_{u+1}[..., 2k] = x1[k],  x_{u+1}[..., 2k+1] = b[k]    (k < cb)
+ * i.e. channel_shuffle(concat(x1, b), 2), and y = x_{n_units}.
+ * cp = branches[u].c_in, the same for every unit, with cb <= cp, cp a
+ * multiple of 8 (so cb = 58 runs as cp = 64); the branch weights act on cp
+ * channels (the caller zero-pads PyTorch's cb-channel weights; since the
+ * padded input channels are zero, their weight columns do not matter, and
+ * outputs cb .. cp-1 are discarded).  c_hidden is a multiple of 16 (pad
+ * with zero weights).  Execution: the branch input is copied into compact
+ * cp-channel rows, the branch runs as one gated block (the one-launch kernel
+ * when cp <= 64, else the kernel chain), and one kernel writes the shuffled
+ * unit output together with the next unit's branch rows.
+ *   x, y   (device) NHWC, shape s (s.c even), dtype dt; must not overlap
+ *   branches (host array of n_units, device weights), 1 <= n_units <= 1024
+ *   flags  0 or DYNCONV_STACK_DENSE (every branch on all positions, no mask
+ *          units) / DYNCONV_STACK_UNFUSED; others: ERR_ARG
+ *   masks  (device) uint8 [n_units][N*H*W] or NULL: per-unit hard masks
+ *   counts (device) int32 [n_units][2] or NULL: per-unit P, P_d
+ *   ws     (device) dynconv_shuffle_stack_workspace_bytes bytes of scratch
+ * Errors as for dynconv_stack_forward; an odd s.c, cp < cb, or branch
+ * blocks of different c_in are DYNCONV_ERR_SHAPE.
+ */
+size_t dynconv_shuffle_stack_workspace_bytes(dynconv_shape s, const dynconv_block *branches,
+                                             int32_t n_units, dynconv_dtype dt, int32_t flags);
+
+dynconv_status dynconv_shuffle_stack_forward(const void *x, void *y, dynconv_shape s, dynconv_dtype dt,
+                                             const dynconv_block *branches, int32_t n_units,
+                                             int32_t flags, uint8_t *masks, int32_t *counts, void *ws,
+                                             size_t ws_bytes, void *stream);
+
+/* Launch sequence of dynconv_shuffle_stack_forward (as for
+ * dynconv_stack_launch_names; k_band_counts, when listed, is last). */
+int32_t dynconv_shuffle_stack_launch_names(dynconv_shape s, const dynconv_block *branches,
+                                           int32_t n_units, dynconv_dtype dt, int32_t flags,
+                                           const char **names, int32_t cap);
+
+/* dynconv_shuffle_stack_forward with per-kernel event pairs, as
+ * dynconv_stack_forward_profiled. */
+dynconv_status dynconv_shuffle_stack_forward_profiled(const void *x, void *y, dynconv_shape s,
+                                                      dynconv_dtype dt, const dynconv_block *branches,
+                                                      int32_t n_units, int32_t flags, uint8_t *masks,
+                                                      int32_t *counts, void *ws, size_t ws_bytes,
+                                                      void *stream, void *const *events,
+                                                      int32_t n_events);
+
 #ifdef __cplusplus
 }
 #endif

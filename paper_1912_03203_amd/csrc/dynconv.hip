@@ -11,6 +11,7 @@
 #include "dynconv.h"
 #include "fused.h"
 #include "kernels.h"
+#include "shuffle.h"
 
 using namespace dynconv;
 
@@ -471,6 +472,153 @@ void stack_walk(const void *x, void *y, dynconv_shape s, dynconv_dtype dt, const
     }
 }
 
+// ------------------------------------------------------------ ShuffleNetV2 units
+// The gated branch runs on cp-channel rows (x2 zero-extended, cp = the
+// branch block's c_in); two such buffers alternate.  Unit outputs alternate
+// between y and a full-row scratch buffer so that the last unit writes y.
+struct ShuffleLayout {
+    size_t xa, xb, full, inner, total;
+    StackLayout in;
+};
+
+dynconv_shape branch_shape(dynconv_shape s, const dynconv_block *br) {
+    dynconv_shape b = s;
+    b.c = br[0].c_in;
+    return b;
+}
+
+ShuffleLayout shuffle_layout(dynconv_shape s, const dynconv_block *br, int32_t n_units, dynconv_dtype dt,
+                             int32_t flags) {
+    const dynconv_shape bs = branch_shape(s, br);
+    const size_t npos = static_cast<size_t>(positions(s));
+    ShuffleLayout L{};
+    size_t off = 0;
+    L.xa = off;    off += align_up(npos * bs.c * dtype_size(dt));
+    L.xb = off;    off += align_up(npos * bs.c * dtype_size(dt));
+    L.full = off;  off += (n_units > 1) ? align_up(npos * s.c * dtype_size(dt)) : 0;
+    L.inner = off;
+    L.in = stack_layout(bs, br, n_units, dt, flags);
+    off += L.in.total;
+    L.total = off;
+    return L;
+}
+
+dynconv_status shuffle_checked(const void *x, void *y, dynconv_shape s, dynconv_dtype dt,
+                               const dynconv_block *br, int32_t n_units, int32_t flags) {
+    if (!x || !y || !br) return DYNCONV_ERR_NULL;
+    if (!dtype_ok(dt)) return DYNCONV_ERR_DTYPE;
+    if (n_units < 1 || n_units > kMaxBlocks) return DYNCONV_ERR_ARG;
+    if (flags & ~(kStackDense | kStackUnfused)) return DYNCONV_ERR_ARG;
+    if (dynconv_status st = check_shape(s, true)) return st;
+    if (s.c % 2 != 0) return DYNCONV_ERR_SHAPE;
+    const dynconv_shape bs = branch_shape(s, br);
+    if (bs.c < s.c / 2) return DYNCONV_ERR_SHAPE;
+    for (int32_t u = 0; u < n_units; ++u)
+        if (dynconv_status st = check_block(&br[u], bs, !(flags & kStackDense))) return st;
+    if (!aligned16(x) || !aligned16(y)) return DYNCONV_ERR_ALIGN;
+    const size_t bytes = static_cast<size_t>(positions(s)) * s.c * dtype_size(dt);
+    if (ranges_overlap(x, bytes, y, bytes)) return DYNCONV_ERR_SHAPE;
+    return DYNCONV_OK;
+}
+
+int shuffle_grid(int64_t npos) {
+    int64_t g = (npos + kShufRows - 1) / kShufRows;
+    if (g > 8192) g = 8192;
+    return static_cast<int>((g + 7) / 8 * 8);
+}
+
+void dispatch_split(dynconv_dtype dt, const void *x, void *xa, int64_t npos, int cb, int cp,
+                    hipStream_t st, Marks &mk) {
+#define DC_SPLIT(T)                                                                            \
+    launch(mk, k_shuffle_split<T>, dim3(shuffle_grid(npos)), dim3(kBlock), 0, st,             \
+           static_cast<const T *>(x), static_cast<T *>(xa), npos, cb, cp)
+    if (dt == DYNCONV_F32) DC_SPLIT(float);
+    else if (dt == DYNCONV_F16) DC_SPLIT(half_t);
+    else DC_SPLIT(bf16_t);
+#undef DC_SPLIT
+}
+
+void dispatch_merge(dynconv_dtype dt, const void *x, const void *br, void *y, void *xa, int64_t npos,
+                    int cb, int cp, hipStream_t st, Marks &mk) {
+#define DC_MERGE(T)                                                                            \
+    launch(mk, k_shuffle_merge<T>, dim3(shuffle_grid(npos)), dim3(kBlock), 0, st,             \
+           static_cast<const T *>(x), static_cast<const T *>(br), static_cast<T *>(y),       \
+           static_cast<T *>(xa), npos, cb, cp)
+    if (dt == DYNCONV_F32) DC_MERGE(float);
+    else if (dt == DYNCONV_F16) DC_MERGE(half_t);
+    else DC_MERGE(bf16_t);
+#undef DC_MERGE
+}
+
+void shuffle_walk(const void *x, void *y, dynconv_shape s, dynconv_dtype dt, const dynconv_block *br,
+                  int32_t n_units, int32_t flags, uint8_t *masks, int32_t *counts, char *base,
+                  const ShuffleLayout &SL, hipStream_t st, Marks &mk, Plan &plan) {
+    const bool dense = flags & kStackDense;
+    const dynconv_shape bs = branch_shape(s, br);
+    const int cb = s.c / 2, cp = bs.c;
+    const int64_t npos = positions(s);
+    const StackLayout &L = SL.in;
+    char *ib = base + SL.inner;
+    void *bufs[2] = {base + SL.xa, base + SL.xb};
+    void *full = base + SL.full;
+    int32_t *cnt_all = counts ? counts : reinterpret_cast<int32_t *>(ib + L.counts);
+    auto mask_of = [&](int32_t u) -> uint8_t * {
+        if (masks) return masks + static_cast<size_t>(u) * npos;
+        return reinterpret_cast<uint8_t *>(ib + L.masks);
+    };
+    auto out_of = [&](int32_t u) -> void * { return ((n_units - 1 - u) % 2 == 0) ? y : full; };
+    // branch input of unit u: bufs[0] for the one-launch block (its output
+    // goes to bufs[1]); bufs[u % 2] for the kernel chain, which runs in place
+    auto in_of = [&](int32_t u) -> void * { return L.fused ? bufs[0] : bufs[u % 2]; };
+
+    if (plan.note("k_shuffle_split")) dispatch_split(dt, x, in_of(0), npos, cb, cp, st, mk);
+    const int nbands = L.fused ? fused_patch_count(bs, dt) : 0;
+    int32_t *band_counts = reinterpret_cast<int32_t *>(ib + L.bands);
+    dynconv_indices idx;
+    idx.active = reinterpret_cast<int32_t *>(ib + L.active);
+    idx.dilated = reinterpret_cast<int32_t *>(ib + L.dilated);
+    idx.nbr = reinterpret_cast<int32_t *>(ib + L.nbr);
+    idx.capacity = npos;
+    for (int32_t u = 0; u < n_units; ++u) {
+        const void *xu = (u == 0) ? x : out_of(u - 1);
+        void *bin = in_of(u);
+        const void *bout = bin;
+        if (L.fused) {
+            FusedMasks fm;
+            if (!dense) {
+                fm.self = true;  // the unit's mask unit on the staged branch input
+                fm.mask_self = masks ? mask_of(u) : nullptr;
+                fm.band_counts = band_counts + static_cast<size_t>(2) * nbands * u;
+            }
+            bout = bufs[1];
+            if (plan.note("k_block_fused"))
+                dispatch_fused(dt, dense, bin, bufs[1], bs, &br[u], nullptr, fm, st, mk);
+        } else if (dense) {
+            bool run = plan.note("k_expand");
+            plan.note("k_dw_project");
+            if (run) dispatch_block(dt, bin, bin, bs, &br[u], nullptr, ib + L.hidden, st, mk);
+        } else {
+            idx.counts = cnt_all + 2 * u;
+            bool run = plan.note("k_mask");
+            plan.note("k_rowcount");
+            plan.note("k_rowscan");
+            plan.note("k_compact");
+            plan.note("k_expand");
+            plan.note("k_dw_project");
+            if (run) {
+                dispatch_mask(dt, bin, bs, br[u].w_mask, br[u].b_mask, mask_of(u), nullptr, st, mk);
+                launch_indices(mask_of(u), bs, 1, &idx, ib + L.scratch, st, mk);
+                dispatch_block(dt, bin, bin, bs, &br[u], &idx, ib + L.hidden, st, mk);
+            }
+        }
+        void *next_in = (u + 1 < n_units) ? in_of(u + 1) : nullptr;
+        if (plan.note("k_shuffle_merge")) dispatch_merge(dt, xu, bout, out_of(u), next_in, npos, cb, cp, st, mk);
+    }
+    if (L.fused && !dense && (counts || !plan.exec) && plan.note("k_band_counts"))
+        launch(mk, k_band_counts, dim3(n_units), dim3(kBlock), 0, st,
+               static_cast<const int32_t *>(band_counts), nbands, cnt_all);
+}
+
 }  // namespace
 
 // ================================================================ C ABI
@@ -625,6 +773,75 @@ dynconv_status dynconv_stack_forward_profiled(const void *x, void *y, dynconv_sh
                                               void *stream, void *const *events, int32_t n_events) {
     return stack_common(x, y, s, dt, blks, n_blocks, flags, masks, counts, ws, ws_bytes, stream,
                         events, n_events, true);
+}
+
+size_t dynconv_shuffle_stack_workspace_bytes(dynconv_shape s, const dynconv_block *branches,
+                                             int32_t n_units, dynconv_dtype dt, int32_t flags) {
+    if (!branches || n_units < 1 || n_units > kMaxBlocks || !dtype_ok(dt) ||
+        check_shape(s, true) != DYNCONV_OK || s.c % 2 != 0 || branches[0].c_in <= 0)
+        return 0;
+    return shuffle_layout(s, branches, n_units, dt, flags).total;
+}
+
+static dynconv_status shuffle_common(const void *x, void *y, dynconv_shape s, dynconv_dtype dt,
+                                     const dynconv_block *br, int32_t n_units, int32_t flags,
+                                     uint8_t *masks, int32_t *counts, void *ws, size_t ws_bytes,
+                                     void *stream, void *const *events, int32_t n_events,
+                                     bool profiled) {
+    if (dynconv_status st = shuffle_checked(x, y, s, dt, br, n_units, flags)) return st;
+    ShuffleLayout L = shuffle_layout(s, br, n_units, dt, flags);
+    if (!ws || ws_bytes < L.total) return DYNCONV_ERR_WORKSPACE;
+    if (!aligned16(ws)) return DYNCONV_ERR_ALIGN;
+    Marks mk;
+    if (profiled) {
+        Plan count{false, nullptr, 0};
+        Marks none;
+        shuffle_walk(x, y, s, dt, br, n_units, flags, masks, counts, nullptr, L, nullptr, none, count);
+        if (!events) return DYNCONV_ERR_NULL;
+        if (n_events < 2 * count.count) return DYNCONV_ERR_ARG;
+        for (int32_t i = 0; i < 2 * count.count; ++i)
+            if (!events[i]) return DYNCONV_ERR_NULL;
+        mk.ev = reinterpret_cast<hipEvent_t const *>(events);
+        mk.n = 2 * count.count;
+    }
+    (void)hipGetLastError();
+    Plan run{true, nullptr, 0};
+    shuffle_walk(x, y, s, dt, br, n_units, flags, masks, counts, static_cast<char *>(ws), L,
+                 static_cast<hipStream_t>(stream), mk, run);
+    return launch_status();
+}
+
+dynconv_status dynconv_shuffle_stack_forward(const void *x, void *y, dynconv_shape s, dynconv_dtype dt,
+                                             const dynconv_block *branches, int32_t n_units,
+                                             int32_t flags, uint8_t *masks, int32_t *counts, void *ws,
+                                             size_t ws_bytes, void *stream) {
+    return shuffle_common(x, y, s, dt, branches, n_units, flags, masks, counts, ws, ws_bytes, stream,
+                          nullptr, 0, false);
+}
+
+int32_t dynconv_shuffle_stack_launch_names(dynconv_shape s, const dynconv_block *branches,
+                                           int32_t n_units, dynconv_dtype dt, int32_t flags,
+                                           const char **names, int32_t cap) {
+    if (!branches || n_units < 1 || n_units > kMaxBlocks || !dtype_ok(dt) ||
+        check_shape(s, true) != DYNCONV_OK || s.c % 2 != 0 || branches[0].c_in <= 0 ||
+        (flags & ~(kStackDense | kStackUnfused)))
+        return -1;
+    ShuffleLayout L = shuffle_layout(s, branches, n_units, dt, flags);
+    Plan plan{false, names, names ? cap : 0};
+    Marks none;
+    shuffle_walk(nullptr, nullptr, s, dt, branches, n_units, flags, nullptr, nullptr, nullptr, L, nullptr,
+                 none, plan);
+    return plan.count;
+}
+
+dynconv_status dynconv_shuffle_stack_forward_profiled(const void *x, void *y, dynconv_shape s,
+                                                      dynconv_dtype dt, const dynconv_block *branches,
+                                                      int32_t n_units, int32_t flags, uint8_t *masks,
+                                                      int32_t *counts, void *ws, size_t ws_bytes,
+                                                      void *stream, void *const *events,
+                                                      int32_t n_events) {
+    return shuffle_common(x, y, s, dt, branches, n_units, flags, masks, counts, ws, ws_bytes, stream,
+                          events, n_events, true);
 }
 
 }  // extern "C"

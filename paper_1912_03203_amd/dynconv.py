@@ -28,7 +28,9 @@ EXPORTED = (
     "dynconv_status_str", "dynconv_version", "dynconv_mask", "dynconv_indices_workspace_bytes",
     "dynconv_build_indices", "dynconv_block_workspace_bytes", "dynconv_block_forward",
     "dynconv_stack_workspace_bytes", "dynconv_stack_forward", "dynconv_stack_launch_names",
-    "dynconv_stack_forward_profiled",
+    "dynconv_stack_forward_profiled", "dynconv_shuffle_stack_workspace_bytes",
+    "dynconv_shuffle_stack_forward", "dynconv_shuffle_stack_launch_names",
+    "dynconv_shuffle_stack_forward_profiled",
 )
 
 
@@ -98,6 +100,19 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
                                                    ctypes.POINTER(Block), i32, i32, vp, vp, vp, sz,
                                                    vp, ctypes.POINTER(ctypes.c_void_p), i32]
     lib.dynconv_stack_forward_profiled.restype = ctypes.c_int
+    lib.dynconv_shuffle_stack_workspace_bytes.argtypes = [Shape, ctypes.POINTER(Block), i32,
+                                                          ctypes.c_int, i32]
+    lib.dynconv_shuffle_stack_workspace_bytes.restype = sz
+    lib.dynconv_shuffle_stack_forward.argtypes = [vp, vp, Shape, ctypes.c_int, ctypes.POINTER(Block),
+                                                  i32, i32, vp, vp, vp, sz, vp]
+    lib.dynconv_shuffle_stack_forward.restype = ctypes.c_int
+    lib.dynconv_shuffle_stack_launch_names.argtypes = [Shape, ctypes.POINTER(Block), i32, ctypes.c_int,
+                                                       i32, ctypes.POINTER(ctypes.c_char_p), i32]
+    lib.dynconv_shuffle_stack_launch_names.restype = i32
+    lib.dynconv_shuffle_stack_forward_profiled.argtypes = [vp, vp, Shape, ctypes.c_int,
+                                                           ctypes.POINTER(Block), i32, i32, vp, vp, vp,
+                                                           sz, vp, ctypes.POINTER(ctypes.c_void_p), i32]
+    lib.dynconv_shuffle_stack_forward_profiled.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -227,6 +242,34 @@ def block_forward(x: torch.Tensor, y: torch.Tensor, blk: BlockWeights, idx, ws: 
     return y
 
 
+def round_up(v: int, m: int) -> int:
+    return (v + m - 1) // m * m
+
+
+def padded_branch_arrays(wts: dict) -> dict:
+    """A ShuffleNetV2 branch's weights (cb channels, hidden E) zero-padded to
+    the channel counts the library takes: cp = round_up(cb, 8) inputs and
+    outputs, round_up(E, 16) hidden channels.  Padded hidden channels have
+    zero weights and biases (their activations are 0 for NONE, RELU, RELU6),
+    padded outputs are discarded by the unit, padded inputs are zero."""
+    import numpy as np
+
+    E, cb = np.asarray(wts["w1"]).shape
+    cp, ep = round_up(cb, 8), round_up(E, 16)
+
+    def pad(a, shape):
+        a = np.asarray(a, np.float32)
+        out = np.zeros(shape, np.float32)
+        out[tuple(slice(0, n) for n in a.shape)] = a
+        return out
+
+    out = dict(wts)
+    out.update(w1=pad(wts["w1"], (ep, cp)), b1=pad(wts["b1"], (ep,)), w2=pad(wts["w2"], (ep, 9)),
+               b2=pad(wts["b2"], (ep,)), w3=pad(wts["w3"], (cp, ep)), b3=pad(wts["b3"], (cp,)),
+               w_m=pad(wts["w_m"], (cp,)))
+    return out
+
+
 def _blocks_array(blocks):
     arr = (Block * len(blocks))()
     for i, b in enumerate(blocks):
@@ -295,3 +338,53 @@ class Stack:
 def stack_forward(x: torch.Tensor, y: torch.Tensor, blocks, flags=0, masks=None, counts=None,
                   ws=None, stream=None):
     return Stack(x, y, blocks, flags, masks, counts, ws)(stream)
+
+
+class ShuffleStack:
+    """A prepared ShuffleNetV2 unit stack y = units(x) (dynconv_shuffle_stack_forward);
+    `branches` are BlockWeights on the padded channel counts (padded_branch_arrays).
+    x and y must not overlap."""
+
+    def __init__(self, x: torch.Tensor, y: torch.Tensor, branches, flags=0, masks=None, counts=None,
+                 ws=None):
+        self.lib = load()
+        self.x, self.y = x, y
+        self.branches = list(branches)
+        self.arr = _blocks_array(self.branches)
+        self.shape = shape_of(x)
+        self.dtype = dtype_code(x.dtype)
+        self.flags = int(flags)
+        need = self.lib.dynconv_shuffle_stack_workspace_bytes(self.shape, self.arr, len(self.branches),
+                                                              self.dtype, self.flags)
+        if need == 0:
+            raise DynconvError("dynconv_shuffle_stack_workspace_bytes rejected the units")
+        if ws is None:
+            ws = torch.empty(need, dtype=torch.uint8, device=x.device)
+        self.ws = ws
+        self.masks = masks
+        self.counts = counts
+
+    def launch_names(self):
+        lib = self.lib
+        args = (self.shape, self.arr, len(self.branches), self.dtype, self.flags)
+        total = lib.dynconv_shuffle_stack_launch_names(*args, None, 0)
+        if total < 0:
+            raise DynconvError("dynconv_shuffle_stack_launch_names rejected the units")
+        names = (ctypes.c_char_p * total)()
+        lib.dynconv_shuffle_stack_launch_names(*args, names, total)
+        return [n.decode() for n in names]
+
+    def _args(self, stream):
+        return (_ptr(self.x), _ptr(self.y), self.shape, self.dtype, self.arr, len(self.branches),
+                self.flags, _ptr(self.masks), _ptr(self.counts), _ptr(self.ws),
+                self.ws.numel() * self.ws.element_size(), _stream(stream))
+
+    def __call__(self, stream=None):
+        _check(self.lib.dynconv_shuffle_stack_forward(*self._args(stream)), "dynconv_shuffle_stack_forward")
+        return self.y
+
+    def profiled(self, events, stream=None):
+        arr = (ctypes.c_void_p * len(events))(*events)
+        _check(self.lib.dynconv_shuffle_stack_forward_profiled(*self._args(stream), arr, len(events)),
+               "dynconv_shuffle_stack_forward_profiled")
+        return self.y

@@ -20,6 +20,9 @@ Recipes (all from ``numpy.random.default_rng(seed)``):
 * Block weights: folded 1x1 / depthwise / 1x1 weights and biases ~ N(0, std)
   (std 0.1 unless stated), rounded once to the storage dtype; biases stay
   fp32.  Mask-unit weights ~ N(0, std) in fp32.
+* ShuffleNetV2 units: blob features over all c channels; the branch weights
+  as above on c/2 channels (hidden e), activations ReLU, none, ReLU; the mask
+  unit reads the branch half.
 * Mask bias for density d: b = -s_(k), where s are the bias-free fp32 logits
   of every position of the batch and s_(k) the k-th smallest (0-based),
   k = NHW - 1 - round(d * NHW).  With distinct logits exactly round(d * NHW)
@@ -50,6 +53,14 @@ class Workload:
     densities: tuple
     features: str  # "blobs" or "ellipses"
     weight_std: float = 0.1
+    # "mbv2": stride-1 inverted-residual blocks on all c channels;
+    # "shufflenet": ShuffleNetV2 stride-1 units, c = both halves, the gated
+    # branch (1x1, DW 3x3, 1x1 with ReLU, none, ReLU) on c/2 channels, hidden e
+    unit: str = "mbv2"
+
+    @property
+    def branch_c(self) -> int:
+        return self.c // 2 if self.unit == "shufflenet" else self.c
 
     @property
     def nhw(self) -> int:
@@ -67,7 +78,23 @@ WORKLOADS = {
     # Pose-style stack: 8 stride-1 blocks at 32 x 64x64x32, hidden 192, fp16.
     "pose_stack8_64x64x32_f16": Workload(
         "pose_stack8_64x64x32_f16", 32, 64, 64, 32, 192, "f16", 8, (0.25,), "ellipses"),
+    # ShuffleNetV2 1.0x stride-1 units, batch 64, bf16, density 0.3: one unit
+    # at each stage shape (latency) and the stage repeats (throughput).
+    "shufflenet_unit_28x28x116_bf16": Workload(
+        "shufflenet_unit_28x28x116_bf16", 64, 28, 28, 116, 58, "bf16", 1, (0.3,), "blobs",
+        unit="shufflenet"),
+    "shufflenet_unit_14x14x232_bf16": Workload(
+        "shufflenet_unit_14x14x232_bf16", 64, 14, 14, 232, 116, "bf16", 1, (0.3,), "blobs",
+        unit="shufflenet"),
+    "shufflenet_stage2_3units_28x28x116_bf16": Workload(
+        "shufflenet_stage2_3units_28x28x116_bf16", 64, 28, 28, 116, 58, "bf16", 3, (0.3,), "blobs",
+        unit="shufflenet"),
+    "shufflenet_stage3_7units_14x14x232_bf16": Workload(
+        "shufflenet_stage3_7units_14x14x232_bf16", 64, 14, 14, 232, 116, "bf16", 7, (0.3,), "blobs",
+        unit="shufflenet"),
 }
+
+SHUFFLE_ACTS = (1, 0, 1)  # ReLU after both 1x1 convolutions, none after the depthwise
 
 
 def rng_for(seed: int) -> np.random.Generator:
@@ -216,8 +243,11 @@ def make_block_inputs(workload: Workload, seed: int):
     else:
         x = blob_features(rng, wl.n, wl.h, wl.w, wl.c)
     x = round_to_storage(x, wl.dtype)
-    blocks = [block_weights(rng, wl.c, wl.e, dtype=wl.dtype, std=wl.weight_std)
+    blocks = [block_weights(rng, wl.branch_c, wl.e, dtype=wl.dtype, std=wl.weight_std)
               for _ in range(wl.blocks)]
+    if wl.unit == "shufflenet":
+        for blk in blocks:
+            blk["acts"] = SHUFFLE_ACTS
     if labels is not None:
         for blk, wm in zip(blocks, ellipse_mask_weights(rng, x, labels, wl.blocks)):
             blk["w_m"] = wm

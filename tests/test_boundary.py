@@ -193,3 +193,50 @@ def test_stack_launch_plans(lib):
     assert [x.decode() for x in out][:7] == [
         "k_mask", "k_rowcount", "k_rowscan", "k_compact", "k_expand", "k_dw_project", "k_mask"]
     assert lib.dynconv_stack_launch_names(s, arr, 0, 1, 0, 0, None, 0) == -1
+
+
+def test_shuffle_stack_validation_and_plans(lib):
+    """ShuffleNetV2 units: 116 channels split 58 | 58, the branch padded to 64
+    channels (hidden 64); bf16."""
+    s = dc.Shape(2, 28, 28, 116)
+    br = (dc.Block * 3)(*([fake_block(C=64, E=64, acts=(1, 0, 1))] * 3))
+    npos = 2 * 28 * 28
+
+    def up(v):
+        return (v + 255) // 256 * 256
+
+    ws = lib.dynconv_shuffle_stack_workspace_bytes(s, br, 3, 2, 0)
+    inner = lib.dynconv_stack_workspace_bytes(dc.Shape(2, 28, 28, 64), br, 3, 2, 0)
+    # two branch-row buffers, one full-row buffer (more than one unit), the block stack's scratch
+    assert ws == 2 * up(npos * 64 * 2) + up(npos * 116 * 2) + inner
+    one = lib.dynconv_shuffle_stack_workspace_bytes(s, br, 1, 2, 0)
+    assert one == 2 * up(npos * 64 * 2) + lib.dynconv_stack_workspace_bytes(dc.Shape(2, 28, 28, 64), br, 1, 2, 0)
+    f = lib.dynconv_shuffle_stack_forward
+    assert f(None, FAKE, s, 2, br, 3, 0, None, None, FAKE, ws, None) == ERR_NULL
+    assert f(FAKE, FAKE + (1 << 30), s, 2, br, 0, 0, None, None, FAKE, ws, None) == ERR_ARG
+    assert f(FAKE, FAKE + (1 << 30), s, 2, br, 3, 8, None, None, FAKE, ws, None) == ERR_ARG
+    assert f(FAKE, FAKE, s, 2, br, 3, 0, None, None, FAKE, ws, None) == ERR_SHAPE        # y == x
+    assert f(FAKE, FAKE + 4096, s, 2, br, 3, 0, None, None, FAKE, ws, None) == ERR_SHAPE  # overlap
+    assert f(FAKE, FAKE + (1 << 30), dc.Shape(2, 28, 28, 115), 2, br, 3, 0, None, None, FAKE, ws,
+             None) == ERR_SHAPE                                                          # odd channels
+    narrow = (dc.Block * 1)(fake_block(C=56, E=64))
+    assert f(FAKE, FAKE + (1 << 30), s, 2, narrow, 1, 0, None, None, FAKE, ws, None) == ERR_SHAPE  # cp < cb
+    mixed = (dc.Block * 2)(fake_block(C=64, E=64), fake_block(C=72, E=64))
+    assert f(FAKE, FAKE + (1 << 30), s, 2, mixed, 2, 0, None, None, FAKE, ws, None) == ERR_SHAPE
+    assert f(FAKE, FAKE + (1 << 30), s, 2, br, 3, 0, None, None, FAKE, ws - 1, None) == ERR_WORKSPACE
+
+    def names(flags, n=3, shape=s, arr=br):
+        total = lib.dynconv_shuffle_stack_launch_names(shape, arr, n, 2, flags, None, 0)
+        out = (ctypes.c_char_p * total)()
+        lib.dynconv_shuffle_stack_launch_names(shape, arr, n, 2, flags, out, total)
+        return [x.decode() for x in out]
+
+    assert names(0) == ["k_shuffle_split"] + ["k_block_fused", "k_shuffle_merge"] * 3 + ["k_band_counts"]
+    assert names(1, n=1) == ["k_shuffle_split", "k_block_fused", "k_shuffle_merge"]
+    assert names(2, n=1) == ["k_shuffle_split", "k_mask", "k_rowcount", "k_rowscan", "k_compact",
+                             "k_expand", "k_dw_project", "k_shuffle_merge"]
+    wide = (dc.Block * 2)(*([fake_block(C=120, E=128, acts=(1, 0, 1))] * 2))
+    assert names(1, n=2, shape=dc.Shape(2, 14, 14, 232), arr=wide) == [
+        "k_shuffle_split", "k_expand", "k_dw_project", "k_shuffle_merge", "k_expand", "k_dw_project",
+        "k_shuffle_merge"]
+    assert lib.dynconv_shuffle_stack_launch_names(s, br, 0, 2, 0, None, 0) == -1

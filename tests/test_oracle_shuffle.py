@@ -77,3 +77,18 @@ def test_partial_mask_comes_from_the_branch_half(orc):
     np.testing.assert_allclose(np.where(act, r["y"], 0), np.where(act, dense, 0), rtol=1e-12, atol=1e-12)
     assert np.where(act, 0, r["y"]).tobytes() == np.where(act, 0, plain).tobytes()
     assert r["y"][:, 0::2].tobytes() == np.ascontiguousarray(x[:, :cb]).tobytes()
+
+
+def test_chunked_helper_equals_the_unit_oracle(orc):
+    """The tests' chunked ShuffleNet helper reproduces shuffle_unit_forward."""
+    from paper_1912_03203_amd import inputs
+    from tests import util
+
+    rng = np.random.default_rng(5)
+    x = inputs.round_to_storage(inputs.blob_features(rng, 2, 7, 9, 20), "bf16")
+    w = inputs.block_weights(rng, 10, 16, dtype="bf16")
+    w["acts"] = SHUFFLE_ACTS
+    got = util.oracle_calibrated_shuffle(x, w, 0.4, "bf16")
+    ref = orc.shuffle_unit_forward(util.nchw(x), w, w["w_m"], got["b_m"])
+    assert np.array_equal(got["G"], ref["G"])
+    np.testing.assert_allclose(got["y"], util.nhwc(ref["y"]), rtol=1e-13, atol=1e-13)

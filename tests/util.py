@@ -88,3 +88,17 @@ def oracle_calibrated_block(x_nhwc_f32, wts, density, dtype, dilate=1):
     y_nhwc = nhwc(y)
     return {"b_m": b_m, "G": G, "A": A, "D": D, "nbr": nbr, "logits": logits, "y": y_nhwc,
             "y_store": inputs.round_to_storage(y_nhwc, dtype)}
+
+
+def oracle_calibrated_shuffle(x_nhwc_f32, wts, density, dtype):
+    """Oracle run of one ShuffleNetV2 unit (oracle.shuffle_unit_forward, with
+    the branch block run in chunks): the mask bias comes from the oracle's
+    bias-free logits of the branch half.  Returns the branch's dict plus
+    y (NHWC fp64, the shuffled unit output)."""
+    x = np.asarray(x_nhwc_f32, np.float32)
+    cb = x.shape[-1] // 2
+    r = oracle_calibrated_block(np.ascontiguousarray(x[..., cb:]), wts, density, dtype)
+    y = oracle.channel_shuffle2(np.concatenate([nchw(x[..., :cb]).astype(np.float64), nchw(r["y"])], axis=1))
+    out = dict(r)
+    out["y"] = nhwc(y)
+    return out
