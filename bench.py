@@ -25,6 +25,8 @@ Also reported on the same JSON line:
                 at densities 0.1 .. 0.9, sparse and dense
   chain         the same stack through the kernel chain (the per-block calls'
                 kernels), sparse and dense, with per-kernel HBM fractions
+  shufflenet    ShuffleNetV2 stride-1 units (gated branch) at 64 x 28x28x116 and
+                64 x 14x14x232, bf16, density 0.3: one unit and 3 / 7 units
 """
 from __future__ import annotations
 
@@ -139,15 +141,16 @@ class Runner:
     an inference caller runs it); read_counts() runs the same stack once more
     with the per-block counts P, P_d requested."""
 
-    def __init__(self, dc, torch, x0, blocks, flags, use_graph, n_blocks):
+    def __init__(self, dc, torch, x0, blocks, flags, use_graph, n_blocks, shuffle=False):
         self.torch = torch
         self.dc = dc
         self.x0 = x0
         self.blocks = blocks
         self.flags = flags
         self.n_blocks = n_blocks
+        self.cls = dc.ShuffleStack if shuffle else dc.Stack
         self.y = torch.empty_like(x0)
-        self.stack = dc.Stack(x0, self.y, blocks, flags=flags)
+        self.stack = self.cls(x0, self.y, blocks, flags=flags)
         # the count reduction is listed last but runs only when counts are requested
         names = self.stack.launch_names()
         self.names = names[:-1] if names and names[-1] == "k_band_counts" else names
@@ -166,7 +169,7 @@ class Runner:
             return None
         counts = torch.zeros(self.n_blocks, 2, dtype=torch.int32, device=self.x0.device)
         y = torch.empty_like(self.x0)
-        self.dc.Stack(self.x0, y, self.blocks, flags=self.flags, counts=counts)()
+        self.cls(self.x0, y, self.blocks, flags=self.flags, counts=counts)()
         torch.cuda.synchronize()
         if not torch.equal(y, self.y):
             raise RuntimeError("the stack with counts requested gave another output")
@@ -347,6 +350,94 @@ def density_sweep(dc, inputs, torch, steps, warmup, use_graph, flags):
     return {"workload": wl.name, "rows": rows}
 
 
+def calibrate_shuffle(dc, inputs, torch, x0_dev, branches_np, dt, density):
+    """Per-unit mask bias of a ShuffleNetV2 unit stack for the target density,
+    from the library's bias-free logits of each unit's branch rows (x2
+    zero-extended to the padded width), units run one after another."""
+    n, h, w, c = x0_dev.shape
+    cb = c // 2
+    x = x0_dev.clone()
+    logits = torch.empty(n * h * w, dtype=torch.float32, device=x.device)
+    out = []
+    for wts in branches_np:
+        blk = dc.BlockWeights.from_arrays(dc.padded_branch_arrays(wts), dt, device=x.device)
+        cp = blk.w_expand.shape[1]
+        x2 = torch.zeros(n, h, w, cp, dtype=x.dtype, device=x.device)
+        x2[..., :cb] = x[..., cb:]
+        dc.mask(x2, blk.w_mask, 0.0, logits=logits)
+        torch.cuda.synchronize()
+        blk.b_mask = float(inputs.percentile_bias(logits.cpu().numpy(), density))
+        y = torch.empty_like(x)
+        dc.ShuffleStack(x, y, [blk])()
+        x = y
+        out.append(blk)
+    torch.cuda.synchronize()
+    return out
+
+
+def shuffle_bytes(name, dense, s, C, cp, ep, npos, rows, P, Pd, last):
+    """Algorithmic bytes of one launch of the ShuffleNetV2 unit path (C
+    channels, branch rows of cp channels, hidden ep)."""
+    cb = C // 2
+    if name == "k_shuffle_split":
+        return npos * (cb + cp) * s
+    if name == "k_shuffle_merge":
+        return npos * (2 * cb + C) * s + (0 if last else npos * cp * s)
+    if name == "k_block_fused":  # branch rows in and out, the unit's own mask computed on chip
+        return 2 * npos * cp * s + 2 * ep * cp * s + 9 * ep * s + 4 * (2 * ep + cp)
+    return algorithmic_bytes(name, dense, s, cp, ep, npos, rows, P, Pd)
+
+
+def shufflenet_report(dc, inputs, torch, steps, warmup, use_graph, profile_steps):
+    """ShuffleNetV2 1.0x stride-1 units at 28x28x116 and 14x14x232 (batch 64,
+    bf16, density 0.3): one unit (latency) and the stage repeats (3 and 7
+    units, throughput), sparse against dense, with per-kernel HBM fractions."""
+    rows = []
+    for name in ("shufflenet_unit_28x28x116_bf16", "shufflenet_unit_14x14x232_bf16",
+                 "shufflenet_stage2_3units_28x28x116_bf16", "shufflenet_stage3_7units_14x14x232_bf16"):
+        wl = inputs.WORKLOADS[name]
+        d = wl.densities[0]
+        x_np, br_np, _ = inputs.make_block_inputs(wl, 0)
+        dt = dc.NAME_TO_DTYPE[wl.dtype]
+        x0 = torch.from_numpy(x_np).cuda().to(dt)
+        sp_b = calibrate_shuffle(dc, inputs, torch, x0, br_np, dt, d)
+        dn_b = [dc.BlockWeights.from_arrays(dc.padded_branch_arrays(w), dt) for w in br_np]
+        sp = Runner(dc, torch, x0, sp_b, 0, use_graph, wl.blocks, shuffle=True)
+        dn = Runner(dc, torch, x0, dn_b, dc.STACK_DENSE, use_graph, wl.blocks, shuffle=True)
+        t_sp = sp.timed(steps, warmup)
+        t_dn = dn.timed(steps, warmup)
+        counts = sp.read_counts().cpu().numpy()
+        s = 2 if wl.dtype != "f32" else 4
+        cp = sp_b[0].w_expand.shape[1]
+        ep = sp_b[0].w_expand.shape[0]
+        kern = {}
+        for tag, runner, dense in (("sparse", sp, False), ("dense", dn, True)):
+            prof, per_launch = profile_kernels(dc, torch, runner, profile_steps)
+            for k, v in prof.items():
+                if dense:
+                    b = float(np.mean([shuffle_bytes(k, True, s, wl.c, cp, ep, wl.nhw, wl.n * wl.h, wl.nhw, wl.nhw,
+                                                     u == wl.blocks - 1) for u in range(wl.blocks)]))
+                else:
+                    b = float(np.mean([shuffle_bytes(k, False, s, wl.c, cp, ep, wl.nhw, wl.n * wl.h, int(P), int(Pd),
+                                                     u == wl.blocks - 1) for u, (P, Pd) in enumerate(counts)]))
+                gbs = b / (v["avg_us"] * 1e-6) / 1e9
+                kern["%s %s" % (k, tag)] = {"avg_us": v["avg_us"], "launches": v["launches"],
+                                            "algorithmic_bytes": b, "gbs": gbs, "hbm_frac": gbs / HBM_PEAK_GBS}
+        dom = max((k for k in kern if k.endswith("sparse")),
+                  key=lambda k: kern[k]["avg_us"] * kern[k]["launches"])
+        rows.append({"workload": wl.name, "units": wl.blocks, "batch": wl.n, "density": d,
+                     "branch_channels_padded": cp, "hidden_padded": ep,
+                     "sparse_ms_per_step": 1e3 * t_sp, "dense_ms_per_step": 1e3 * t_dn,
+                     "sparse_images_per_s": wl.n / t_sp, "dense_images_per_s": wl.n / t_dn,
+                     "speedup_vs_dense": t_dn / t_sp, "per_unit_us": 1e6 * t_sp / wl.blocks,
+                     "active_frac": (counts[:, 0] / wl.nhw).tolist(),
+                     "dilated_frac": (counts[:, 1] / wl.nhw).tolist(),
+                     "sparse_launches": sp.names, "kernels": kern,
+                     "roofline": {"bound": "hbm", "kernel": dom, "achieved": kern[dom]["gbs"],
+                                  "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": kern[dom]["hbm_frac"]}})
+    return rows
+
+
 def traffic_pass(dc, torch, wl, x0, sparse_blocks, dense_blocks, reps=3):
     """Launch sequence for one HBM-counter run (FETCH_SIZE or WRITE_SIZE):
     (1) the kernel chain's plain copy (k_copy16, input -> output buffer, a
@@ -459,6 +550,7 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-chain", action="store_true", help="skip the kernel-chain report")
+    ap.add_argument("--no-shufflenet", action="store_true", help="skip the ShuffleNetV2 unit report")
     ap.add_argument("--profile-steps", type=int, default=20)
     ap.add_argument("--traffic-pass", action="store_true",
                     help="untimed launches for an HBM-counter run: a plain copy of known size, "
@@ -587,6 +679,10 @@ def main():
         log("kernel chain")
         result["chain"] = chain_report(dc, torch, wl, x0, sparse_blocks, dense_blocks, counts, use_graph,
                                        min(args.steps, 50), min(args.warmup, 5), args.profile_steps)
+    if not args.no_shufflenet:
+        log("shufflenet units")
+        result["shufflenet"] = shufflenet_report(dc, inputs, torch, min(args.steps, 100), min(args.warmup, 10),
+                                                 use_graph, args.profile_steps)
     if not args.no_sweep:
         log("density sweep")
         result["sweep"] = density_sweep(dc, inputs, torch, min(args.steps, 100), min(args.warmup, 10),
