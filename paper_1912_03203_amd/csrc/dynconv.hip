@@ -279,6 +279,9 @@ struct FusedMasks {
     uint8_t *mask_self = nullptr;
     uint8_t *mask_next = nullptr;
     int32_t *band_counts = nullptr;
+    // nonzero: the block is the branch of a ShuffleNetV2 unit with this many
+    // channels per half, reading and writing the unit's full rows
+    int shuffle_cb = 0;
 };
 
 template <typename T, bool DENSE, int MAXKS, int MAXMT, int MAXC>
@@ -288,9 +291,11 @@ void launch_fused_k(const void *src, void *dst, dynconv_shape s, const dynconv_b
     const PatchGeom p = fused_geom_t<T, MAXC>(s);
     const int npatch = s.n * p.nph * p.npw;
     const int grid = (npatch + 7) / 8 * 8;  // whole groups of 8 (one per XCD)
-    launch(mk, k_block_fused<T, DENSE, MAXKS, MAXMT, MAXC, CFG>, dim3(grid), dim3(CFG::kThreads), 0, st,
+    auto kern = fm.shuffle_cb ? k_block_fused<T, DENSE, MAXKS, MAXMT, MAXC, CFG, true>
+                              : k_block_fused<T, DENSE, MAXKS, MAXMT, MAXC, CFG, false>;
+    launch(mk, kern, dim3(grid), dim3(CFG::kThreads), 0, st,
            static_cast<const T *>(src), static_cast<T *>(dst), s.n, s.h, s.w, s.c, b->c_hidden, p.R, p.Wu,
-           fm.mask_in, fm.self ? b->w_mask : nullptr, b->b_mask, fm.mask_self,
+           fm.shuffle_cb, fm.mask_in, fm.self ? b->w_mask : nullptr, b->b_mask, fm.mask_self,
            static_cast<const T *>(b->w_expand), b->b_expand, b->act_expand,
            static_cast<const T *>(b->w_dw), b->b_dw, b->act_dw,
            static_cast<const T *>(b->w_project), b->b_project, b->act_project,
@@ -311,8 +316,10 @@ void dispatch_fused(dynconv_dtype dt, bool dense, const void *src, void *dst, dy
                     const dynconv_block *b, const dynconv_block *next, const FusedMasks &fm,
                     hipStream_t st, Marks &mk) {
 #define DC_FUSED(T)                                                                  \
-    (dense ? launch_fused<T, true>(src, dst, s, b, nullptr, FusedMasks{}, st, mk)    \
+    (dense ? launch_fused<T, true>(src, dst, s, b, nullptr, dense_fm, st, mk)        \
            : launch_fused<T, false>(src, dst, s, b, next, fm, st, mk))
+    FusedMasks dense_fm;
+    dense_fm.shuffle_cb = fm.shuffle_cb;
     if (dt == DYNCONV_F32) DC_FUSED(float);
     else if (dt == DYNCONV_F16) DC_FUSED(half_t);
     else DC_FUSED(bf16_t);
@@ -473,13 +480,24 @@ void stack_walk(const void *x, void *y, dynconv_shape s, dynconv_dtype dt, const
 }
 
 // ------------------------------------------------------------ ShuffleNetV2 units
-// The gated branch runs on cp-channel rows (x2 zero-extended, cp = the
-// branch block's c_in); two such buffers alternate.  Unit outputs alternate
-// between y and a full-row scratch buffer so that the last unit writes y.
+// Unit outputs alternate between y and a full-row scratch buffer so that the
+// last unit writes y.  When the branch takes the one-launch block and a half
+// row is whole 4-byte words, that kernel reads the branch half of the unit's
+// input rows and writes the shuffled output rows itself (one launch per
+// unit).  Otherwise the branch runs on compact cp-channel rows (x2
+// zero-extended, cp = the branch block's c_in), filled by k_shuffle_split /
+// k_shuffle_merge; two such buffers alternate.
 struct ShuffleLayout {
+    bool direct;
     size_t xa, xb, full, inner, total;
     StackLayout in;
 };
+
+bool shuffle_direct(dynconv_shape s, const dynconv_block *br, dynconv_dtype dt, int32_t flags) {
+    dynconv_shape bs = s;
+    bs.c = br[0].c_in;
+    return use_fused(bs, dt, flags) && (s.c / 2) * dtype_size(dt) % 4 == 0;
+}
 
 dynconv_shape branch_shape(dynconv_shape s, const dynconv_block *br) {
     dynconv_shape b = s;
@@ -492,9 +510,11 @@ ShuffleLayout shuffle_layout(dynconv_shape s, const dynconv_block *br, int32_t n
     const dynconv_shape bs = branch_shape(s, br);
     const size_t npos = static_cast<size_t>(positions(s));
     ShuffleLayout L{};
+    L.direct = shuffle_direct(s, br, dt, flags);
+    const size_t rows = L.direct ? 0 : align_up(npos * bs.c * dtype_size(dt));
     size_t off = 0;
-    L.xa = off;    off += align_up(npos * bs.c * dtype_size(dt));
-    L.xb = off;    off += align_up(npos * bs.c * dtype_size(dt));
+    L.xa = off;    off += rows;
+    L.xb = off;    off += rows;
     L.full = off;  off += (n_units > 1) ? align_up(npos * s.c * dtype_size(dt)) : 0;
     L.inner = off;
     L.in = stack_layout(bs, br, n_units, dt, flags);
@@ -571,9 +591,26 @@ void shuffle_walk(const void *x, void *y, dynconv_shape s, dynconv_dtype dt, con
     // goes to bufs[1]); bufs[u % 2] for the kernel chain, which runs in place
     auto in_of = [&](int32_t u) -> void * { return L.fused ? bufs[0] : bufs[u % 2]; };
 
-    if (plan.note("k_shuffle_split")) dispatch_split(dt, x, in_of(0), npos, cb, cp, st, mk);
     const int nbands = L.fused ? fused_patch_count(bs, dt) : 0;
     int32_t *band_counts = reinterpret_cast<int32_t *>(ib + L.bands);
+    if (SL.direct) {
+        for (int32_t u = 0; u < n_units; ++u) {
+            FusedMasks fm;
+            fm.shuffle_cb = cb;
+            if (!dense) {
+                fm.self = true;  // the unit's mask unit on the staged branch half
+                fm.mask_self = masks ? mask_of(u) : nullptr;
+                fm.band_counts = band_counts + static_cast<size_t>(2) * nbands * u;
+            }
+            const void *xu = (u == 0) ? x : out_of(u - 1);
+            if (plan.note("k_block_fused")) dispatch_fused(dt, dense, xu, out_of(u), bs, &br[u], nullptr, fm, st, mk);
+        }
+        if (!dense && (counts || !plan.exec) && plan.note("k_band_counts"))
+            launch(mk, k_band_counts, dim3(n_units), dim3(kBlock), 0, st,
+                   static_cast<const int32_t *>(band_counts), nbands, cnt_all);
+        return;
+    }
+    if (plan.note("k_shuffle_split")) dispatch_split(dt, x, in_of(0), npos, cb, cp, st, mk);
     dynconv_indices idx;
     idx.active = reinterpret_cast<int32_t *>(ib + L.active);
     idx.dilated = reinterpret_cast<int32_t *>(ib + L.dilated);

@@ -106,7 +106,7 @@ struct DwProjWeights {
     alignas(16) float b2[kChunk];
 };
 
-template <typename T, int MAXC, class CFG>
+template <typename T, int MAXC, class CFG, bool SHUF = false>
 struct PatchLds {
     static constexpr int kRows = kPatchMaxRows + 2;
     uint64_t nw[kRows];                 // needed slots per region row (bit = region column)
@@ -121,6 +121,8 @@ struct PatchLds {
     DwProjWeights<T, MAXC> wd;
     alignas(16) T xs[CFG::kRegion][MAXC + 8];       // x at region slots; own slots become y
     alignas(16) T h1r[CFG::kRegion + 1][kChunkPad]; // the slice in region layout + a spare row
+    // ShuffleNetV2 rows: the pass-through half of the own positions
+    alignas(16) T x1s[SHUF ? CFG::kOwn : 1][SHUF ? MAXC : 1];
 };
 
 // Cooperative global -> register -> LDS staging of one part of a slice's
@@ -221,10 +223,16 @@ struct DwProjStager {
     }
 };
 
-template <typename T, bool DENSE, int MAXKS, int MAXMT, int MAXC, class CFG>
+// SHUF: the block is the gated branch of a ShuffleNetV2 unit.  Input and
+// output rows then hold 2*cb channels; the block's input is the second half
+// of each input row (cb channels, zero-extended to C on chip), and each
+// output row is the channel shuffle of (first half of the input row, block
+// output): output channel 2k = input channel k, 2k+1 = block output k.
+// cb * sizeof(T) must be a multiple of 4.  Without SHUF, cb is unused.
+template <typename T, bool DENSE, int MAXKS, int MAXMT, int MAXC, class CFG, bool SHUF>
 __global__ void __launch_bounds__(CFG::kThreads) __attribute__((amdgpu_waves_per_eu(CFG::kWpe)))
 k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int W, int C, int E,
-              int R, int Wu, const uint8_t *__restrict__ mask_in,
+              int R, int Wu, int cb, const uint8_t *__restrict__ mask_in,
               const float *__restrict__ wm_self, float bm_self, uint8_t *__restrict__ mask_self,
               const T *__restrict__ w1, const float *__restrict__ b1, int act1,
               const T *__restrict__ w2, const float *__restrict__ b2, int act2,
@@ -235,7 +243,7 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
     constexpr int NW = CFG::kWaves, NT = CFG::kThreads, kRegion = CFG::kRegion;
     constexpr int kNeedTiles = ((kRegion + 15) / 16 + NW - 1) / NW;  // 16-slot tiles per wave
     constexpr int kActTiles = ((CFG::kOwn + 15) / 16 + NW - 1) / NW;
-    __shared__ PatchLds<T, MAXC, CFG> L;
+    __shared__ PatchLds<T, MAXC, CFG, SHUF> L;
     const int tid = threadIdx.x;
     const int wave = tid / kWave, lane = tid % kWave;
     const int r = lane % 16, g = lane / 16;
@@ -272,11 +280,15 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
     stA.load(w1, b1, C, E, 0, tid);
     stB.load(w2, w3, b2, C, E, 0, tid);
     for (int c = tid; c < C; c += NT) L.b3[c] = b3[c];
-    {
-        const int r_first = (h0 == 0) ? 1 : 0;
-        const int r_last = (h0 + rows_out < H) ? nreg - 1 : nreg - 2;
+    // x at the in-image region slots (one 16-byte load in flight per thread:
+    // measured faster here than batches of loads, which all patches would
+    // issue at once)
+    const int r_first = (h0 == 0) ? 1 : 0;
+    const int r_last = (h0 + rows_out < H) ? nreg - 1 : nreg - 2;
+    const int ncol = c_hi - c_lo;
+    if (!SHUF) {
         const int vpr = C / per16;                      // 16-byte pieces per position
-        const int per_row = (c_hi - c_lo) * vpr;
+        const int per_row = ncol * vpr;
         const int nvec = (r_last - r_first + 1) * per_row;
         for (int i = tid; i < nvec; i += NT) {
             const int rr = r_first + i / per_row, k = i % per_row;
@@ -284,6 +296,44 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
             const uint4 *src = reinterpret_cast<const uint4 *>(
                 xin + ((img + h0 - 1 + rr) * W + (w0 - 1 + c)) * C);
             *reinterpret_cast<uint4 *>(&L.xs[rr * WP + c][piece * per16]) = src[piece];
+        }
+    } else {
+        // unit rows in 4-byte words, in batches of 8 loads per thread: the
+        // second half (the block's input, zero past cb) of every in-image
+        // region position into xs, the first half of the own positions into x1s
+        constexpr int kB = 8;
+        constexpr int wpp = MAXC * static_cast<int>(sizeof(T)) / 4;         // words per staged row
+        constexpr int wrow = (MAXC + 8) * static_cast<int>(sizeof(T)) / 4;  // words per xs row
+        const int wreal = cb * static_cast<int>(sizeof(T)) / 4;
+        const int nvec = (r_last - r_first + 1) * ncol * wpp;
+        for (int i0 = tid; i0 < nvec; i0 += kB * NT) {
+            uint32_t v2[kB], v1[kB];
+            int d2[kB], d1[kB];
+#pragma unroll
+            for (int k = 0; k < kB; ++k) {
+                const int i = i0 + k * NT;
+                d2[k] = d1[k] = -1;
+                v2[k] = v1[k] = 0u;
+                if (i < nvec) {
+                    const int pos = i / wpp, wd = i % wpp;
+                    const int rr = r_first + pos / ncol, c = c_lo + pos % ncol;
+                    const uint32_t *row = reinterpret_cast<const uint32_t *>(
+                        xin + ((img + h0 - 1 + rr) * W + (w0 - 1 + c)) * (2 * cb));
+                    d2[k] = (rr * WP + c) * wrow + wd;
+                    if (wd < wreal) {
+                        v2[k] = row[wreal + wd];
+                        if (rr >= 1 && rr <= rows_out && c >= 1 && c <= cols_out) {
+                            v1[k] = row[wd];
+                            d1[k] = ((rr - 1) * cols_out + (c - 1)) * wpp + wd;
+                        }
+                    }
+                }
+            }
+#pragma unroll
+            for (int k = 0; k < kB; ++k) {
+                if (d2[k] >= 0) reinterpret_cast<uint32_t *>(&L.xs[0][0])[d2[k]] = v2[k];
+                if (d1[k] >= 0) reinterpret_cast<uint32_t *>(&L.x1s[0][0])[d1[k]] = v1[k];
+            }
         }
     }
     {   // zero region: slots outside the image are never written again
@@ -535,7 +585,22 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
         __syncthreads();
     }
     // ---- 4b. store the patch (inactive positions: x unchanged)
-    {
+    if (SHUF) {
+        // output rows: (first input half, block output) interleaved
+        typedef T pair_t __attribute__((ext_vector_type(2)));
+        const int nslot = rows_out * cols_out * MAXC;
+        for (int i = tid; i < nslot; i += NT) {
+            const int pos = i / MAXC, k = i % MAXC;
+            if (k < cb) {
+                const int rr = 1 + pos / cols_out, c = 1 + pos % cols_out;
+                const int64_t g = (img + h0 - 1 + rr) * W + (w0 - 1 + c);
+                pair_t v;
+                v.x = L.x1s[pos][k];
+                v.y = L.xs[rr * WP + c][k];
+                *reinterpret_cast<pair_t *>(yout + g * (2 * cb) + 2 * k) = v;
+            }
+        }
+    } else {
         const int vpr = C / per16;
         const int per_row = cols_out * vpr;
         const int nvec = rows_out * per_row;
@@ -547,7 +612,7 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
         }
     }
     // ---- 4c. the next block's mask unit on the stored values
-    if (mask_next) {
+    if (!SHUF && mask_next) {
         for (int i = tid; i < rows_out * cols_out; i += NT) {
             const int rr = 1 + i / cols_out, c = 1 + i % cols_out;
             const T *row = &L.xs[rr * WP + c][0];

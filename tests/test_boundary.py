@@ -207,10 +207,15 @@ def test_shuffle_stack_validation_and_plans(lib):
 
     ws = lib.dynconv_shuffle_stack_workspace_bytes(s, br, 3, 2, 0)
     inner = lib.dynconv_stack_workspace_bytes(dc.Shape(2, 28, 28, 64), br, 3, 2, 0)
-    # two branch-row buffers, one full-row buffer (more than one unit), the block stack's scratch
-    assert ws == 2 * up(npos * 64 * 2) + up(npos * 116 * 2) + inner
+    # the one-launch branch reads and writes full rows: one full-row buffer
+    # (more than one unit) and the block stack's scratch
+    assert ws == up(npos * 116 * 2) + inner
     one = lib.dynconv_shuffle_stack_workspace_bytes(s, br, 1, 2, 0)
-    assert one == 2 * up(npos * 64 * 2) + lib.dynconv_stack_workspace_bytes(dc.Shape(2, 28, 28, 64), br, 1, 2, 0)
+    assert one == lib.dynconv_stack_workspace_bytes(dc.Shape(2, 28, 28, 64), br, 1, 2, 0)
+    # the kernel chain runs on two compact branch-row buffers
+    chain = lib.dynconv_shuffle_stack_workspace_bytes(s, br, 3, 2, 2)
+    assert chain == 2 * up(npos * 64 * 2) + up(npos * 116 * 2) + \
+        lib.dynconv_stack_workspace_bytes(dc.Shape(2, 28, 28, 64), br, 3, 2, 2)
     f = lib.dynconv_shuffle_stack_forward
     assert f(None, FAKE, s, 2, br, 3, 0, None, None, FAKE, ws, None) == ERR_NULL
     assert f(FAKE, FAKE + (1 << 30), s, 2, br, 0, 0, None, None, FAKE, ws, None) == ERR_ARG
@@ -231,8 +236,13 @@ def test_shuffle_stack_validation_and_plans(lib):
         lib.dynconv_shuffle_stack_launch_names(shape, arr, n, 2, flags, out, total)
         return [x.decode() for x in out]
 
-    assert names(0) == ["k_shuffle_split"] + ["k_block_fused", "k_shuffle_merge"] * 3 + ["k_band_counts"]
-    assert names(1, n=1) == ["k_shuffle_split", "k_block_fused", "k_shuffle_merge"]
+    assert names(0) == ["k_block_fused"] * 3 + ["k_band_counts"]
+    assert names(1, n=1) == ["k_block_fused"]
+    # 9-channel bf16 halves are not whole 4-byte words: compact branch rows
+    odd = (dc.Block * 2)(*([fake_block(C=16, E=16, acts=(1, 0, 1))] * 2))
+    assert names(0, n=2, shape=dc.Shape(1, 6, 6, 18), arr=odd) == [
+        "k_shuffle_split", "k_block_fused", "k_shuffle_merge", "k_block_fused", "k_shuffle_merge",
+        "k_band_counts"]
     assert names(2, n=1) == ["k_shuffle_split", "k_mask", "k_rowcount", "k_rowscan", "k_compact",
                              "k_expand", "k_dw_project", "k_shuffle_merge"]
     wide = (dc.Block * 2)(*([fake_block(C=120, E=128, acts=(1, 0, 1))] * 2))

@@ -79,6 +79,8 @@ UNIT_CASES = [
     ("fp32_16ch", "f32", (1, 8, 8, 16, 16), 0.5, 4),
     ("fp32_c116", "f32", (1, 7, 7, 116, 58), 0.4, 5),
     ("ragged_bf16_w33", "bf16", (3, 5, 33, 44, 40), 0.3, 6),
+    ("odd_half_bf16", "bf16", (2, 6, 10, 18, 16), 0.5, 7),   # 9-channel halves: compact branch rows
+    ("odd_half_f32", "f32", (2, 5, 9, 18, 16), 0.5, 8),      # 36-byte halves: full rows
 ]
 
 
@@ -133,7 +135,10 @@ def test_shuffle_stack_matches_unit_calls(dtype, shape, nu):
     b0 = float(inputs.percentile_bias(s, 0.3))
     biases = [b0] * nu
     stack = run_units(x, ws, biases, dtype)
-    assert stack["names"][0] == "k_shuffle_split" and stack["names"].count("k_shuffle_merge") == nu
+    if C // 2 <= 64:  # one launch per unit, reading and writing the unit's rows
+        assert stack["names"][:nu] == ["k_block_fused"] * nu
+    else:             # compact branch rows and the kernel chain
+        assert stack["names"][0] == "k_shuffle_split" and stack["names"].count("k_shuffle_merge") == nu
     cur = x
     for u in range(nu):
         one = run_units(cur, [ws[u]], [biases[u]], dtype)
