@@ -27,6 +27,10 @@ Also reported on the same JSON line:
                 kernels), sparse and dense, with per-kernel HBM fractions
   shufflenet    ShuffleNetV2 stride-1 units (gated branch) at 64 x 28x28x116 and
                 64 x 14x14x232, bf16, density 0.3: one unit and 3 / 7 units
+  bandwidth_probes
+                the chain's mask / gather+expand / depthwise+scatter kernels and
+                the one-launch block at batches moving >= 512 MB per kernel,
+                cache flushed before each call, against a 1 GiB copy
 """
 from __future__ import annotations
 
@@ -438,6 +442,87 @@ def shufflenet_report(dc, inputs, torch, steps, warmup, use_graph, profile_steps
     return rows
 
 
+def bandwidth_probes(dc, inputs, torch, reps=5):
+    """HBM-scale timing of the bandwidth-bound kernels.  At the benchmark
+    shapes a kernel moves 10-70 MB, which the 256 MB Infinity Cache holds; here
+    the batch is scaled until each probed kernel moves at least 512 MB, and a
+    512 MB scratch buffer is rewritten before every call so that its data
+    comes from HBM.  Reference: a 1 GiB device-to-device copy (2 GiB moved)."""
+    out = {}
+    scratch = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+
+    def flush():
+        scratch.fill_(1)
+
+    # copy bandwidth
+    a = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ts = []
+    for _ in range(reps):
+        flush()
+        e0.record()
+        b.copy_(a)
+        e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1) * 1e-3)
+    copy_gbs = 2 * a.numel() / min(ts) / 1e9
+    out["copy"] = {"bytes": 2 * a.numel(), "best_us": 1e6 * min(ts), "gbs": copy_gbs,
+                   "hbm_frac": copy_gbs / HBM_PEAK_GBS}
+    del a, b
+
+    def probe(tag, wl, rep, flags, density, kernels):
+        x_np, blocks_np, _ = inputs.make_block_inputs(wl, 0)
+        dt = dc.NAME_TO_DTYPE[wl.dtype]
+        base = torch.from_numpy(x_np).cuda().to(dt)
+        blk = calibrate(dc, inputs, torch, base, blocks_np[:1], dt, density)[0] if density else \
+            dc.BlockWeights.from_arrays(blocks_np[0], dt)
+        x = base.repeat(rep, 1, 1, 1).contiguous()
+        y = torch.empty_like(x)
+        counts = torch.zeros(1, 2, dtype=torch.int32, device="cuda")
+        st = dc.Stack(x, y, [blk], flags=flags, counts=None if flags & dc.STACK_DENSE else counts)
+        names = st.launch_names()
+        ev = HipEvents(torch, 2 * len(names))
+        best = {}
+        try:
+            for _ in range(reps):
+                flush()
+                st.profiled(ev.ev)
+                torch.cuda.synchronize()
+                for i, n in enumerate(names):
+                    if n in kernels:
+                        t = ev.elapsed_ms(2 * i, 2 * i + 1) * 1e-3
+                        best[n] = min(best.get(n, t), t)
+        finally:
+            ev.close()
+        npos = x.shape[0] * x.shape[1] * x.shape[2]
+        rows = x.shape[0] * x.shape[1]
+        s = 2 if wl.dtype != "f32" else 4
+        dense = bool(flags & dc.STACK_DENSE)
+        P, Pd = (npos, npos) if dense else (int(v) for v in counts[0].cpu())
+        for n, t in best.items():
+            nb = algorithmic_bytes(n, dense, s, wl.c, wl.e, npos, rows, P, Pd, last=True)
+            if n == "k_block_fused" and not dense:
+                nb -= npos  # a one-block stack computes its own mask: no mask read
+            out["%s %s" % (n, tag)] = {"batch": x.shape[0], "density": None if dense else P / npos,
+                                       "dilated": None if dense else Pd / npos, "bytes": nb,
+                                       "best_us": 1e6 * t, "gbs": nb / t / 1e9,
+                                       "hbm_frac": nb / t / 1e9 / HBM_PEAK_GBS,
+                                       "copy_frac": nb / t / 1e9 / copy_gbs}
+        del x, y
+
+    stage2 = inputs.WORKLOADS["mbv2_stage2_block_56x56x24_f16"]
+    pose = inputs.WORKLOADS["pose_stack8_64x64x32_f16"]
+    chain = ("k_mask", "k_expand", "k_dw_project")
+    probe("dense, 2048 x 56x56x24", stage2, 64, dc.STACK_UNFUSED | dc.STACK_DENSE, None, chain)
+    probe("sparse d=0.25, 2048 x 56x56x24", stage2, 64, dc.STACK_UNFUSED, 0.25, chain)
+    probe("dense, 1024 x 64x64x32", pose, 32, dc.STACK_DENSE, None, ("k_block_fused",))
+    probe("sparse d=0.25, 1024 x 64x64x32", pose, 32, 0, 0.25, ("k_block_fused",))
+    del scratch
+    torch.cuda.empty_cache()
+    return out
+
+
 def traffic_pass(dc, torch, wl, x0, sparse_blocks, dense_blocks, reps=3):
     """Launch sequence for one HBM-counter run (FETCH_SIZE or WRITE_SIZE):
     (1) the kernel chain's plain copy (k_copy16, input -> output buffer, a
@@ -551,6 +636,7 @@ def main():
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--no-chain", action="store_true", help="skip the kernel-chain report")
     ap.add_argument("--no-shufflenet", action="store_true", help="skip the ShuffleNetV2 unit report")
+    ap.add_argument("--no-probes", action="store_true", help="skip the HBM-scale bandwidth probes")
     ap.add_argument("--profile-steps", type=int, default=20)
     ap.add_argument("--traffic-pass", action="store_true",
                     help="untimed launches for an HBM-counter run: a plain copy of known size, "
@@ -679,6 +765,9 @@ def main():
         log("kernel chain")
         result["chain"] = chain_report(dc, torch, wl, x0, sparse_blocks, dense_blocks, counts, use_graph,
                                        min(args.steps, 50), min(args.warmup, 5), args.profile_steps)
+    if not args.no_probes:
+        log("bandwidth probes")
+        result["bandwidth_probes"] = bandwidth_probes(dc, inputs, torch)
     if not args.no_shufflenet:
         log("shufflenet units")
         result["shufflenet"] = shufflenet_report(dc, inputs, torch, min(args.steps, 100), min(args.warmup, 10),
