@@ -125,6 +125,19 @@ struct PatchLds {
     alignas(16) T x1s[SHUF ? CFG::kOwn : 1][SHUF ? MAXC : 1];
 };
 
+// Inclusive prefix sum over the 64 lanes of a wave with DPP row operations:
+// shifts by 1, 2, 4, 8 within each row of 16 lanes, then lane 15 of rows 0
+// and 2 added into rows 1 and 3, then lane 31 into rows 2 and 3.
+__device__ __forceinline__ int wave_scan_incl(int v) {
+    v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, false);  // row_shr:1
+    v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, false);  // row_shr:2
+    v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xf, 0xf, false);  // row_shr:4
+    v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xf, 0xf, false);  // row_shr:8
+    v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xa, 0xf, false);  // row_bcast:15
+    v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xc, 0xf, false);  // row_bcast:31
+    return v;
+}
+
 // Cooperative global -> register -> LDS staging of one part of a slice's
 // weights: each thread owns kSlots 16-byte pieces (zero beyond E).
 template <typename T, int MAXC, int NT>
@@ -170,13 +183,19 @@ struct ExpandStager {
 template <typename T, int MAXC, int NT>
 struct DwProjStager {
     static constexpr int kPer16 = 16 / static_cast<int>(sizeof(T));
-    static constexpr int kPieces = MAXC * kChunk / kPer16 + kChunk * 9 / kPer16 + kChunk / 4;
+    static constexpr int kPieces = MAXC * kChunk / kPer16 + kChunk / 4;
     static constexpr int kSlots = (kPieces + NT - 1) / NT;
+    static constexpr int kTaps = kChunk * 9;                 // depthwise weights of a slice
+    static constexpr int kTapSlots = (kTaps + NT - 1) / NT;
     uint4 v[kSlots];
-    // pieces: w3 rows (C x 32), then w2 (32 channels x 9 taps, read as [e][9]), then b2
+    T t[kTapSlots];
+    // 16-byte pieces: w3 rows (C x 32), then b2.  Depthwise weights: one
+    // element per thread (slice element j = 9 e + k of w2 [E][9]), stored
+    // transposed as w2[k][e]: a load and a 2-byte store per thread, so no
+    // thread packs values whose loads are still in flight.
     __device__ __forceinline__ void load(const T *w2, const T *w3, const float *b2, int C, int E, int ec,
                                          int tid) {
-        const int n3 = C * kChunk / kPer16, n2 = kChunk * 9 / kPer16;
+        const int n3 = C * kChunk / kPer16;
         const int e_base = ec * kChunk;
 #pragma unroll
         for (int sl = 0; sl < kSlots; ++sl) {
@@ -186,49 +205,39 @@ struct DwProjStager {
                 const int c = p / (kChunk / kPer16), e = (p % (kChunk / kPer16)) * kPer16;
                 if (e_base + e < E)
                     val = *reinterpret_cast<const uint4 *>(w3 + static_cast<int64_t>(c) * E + e_base + e);
-            } else if (p < n3 + n2) {
-                // w2 [E][9] for the slice's 32 channels is 288 contiguous elements;
-                // E - e_base is a multiple of 16, so no piece straddles E
-                const int first = (p - n3) * kPer16;
-                if (first / 9 < E - e_base)
-                    val = *reinterpret_cast<const uint4 *>(w2 + static_cast<int64_t>(e_base) * 9 + first);
-            } else if (p < n3 + n2 + kChunk / 4) {
-                const int e = (p - n3 - n2) * 4;
+            } else if (p < n3 + kChunk / 4) {
+                const int e = (p - n3) * 4;
                 if (e_base + e < E) val = *reinterpret_cast<const uint4 *>(b2 + e_base + e);
             }
             v[sl] = val;
         }
+#pragma unroll
+        for (int sl = 0; sl < kTapSlots; ++sl) {
+            const int j = tid + sl * NT;
+            t[sl] = static_cast<T>(0.0f);
+            if (j < kTaps && e_base + j / 9 < E) t[sl] = w2[static_cast<int64_t>(e_base) * 9 + j];
+        }
     }
     __device__ __forceinline__ void store(DwProjWeights<T, MAXC> &dst, int C, int E, int ec, int tid) const {
-        const int n3 = C * kChunk / kPer16, n2 = kChunk * 9 / kPer16;
-        const int e_lim = E - ec * kChunk;
+        const int n3 = C * kChunk / kPer16;
 #pragma unroll
         for (int sl = 0; sl < kSlots; ++sl) {
             const int p = tid + sl * NT;
             if (p < n3) {
                 const int c = p / (kChunk / kPer16), e = (p % (kChunk / kPer16)) * kPer16;
                 *reinterpret_cast<uint4 *>(&dst.w3[c][e]) = v[sl];
-            } else if (p < n3 + n2) {
-                const T *vals = reinterpret_cast<const T *>(&v[sl]);
-#pragma unroll
-                for (int u = 0; u < kPer16; ++u) {
-                    const int idx = (p - n3) * kPer16 + u;  // = e * 9 + k
-                    const int e = idx / 9, k = idx % 9;
-                    dst.w2[k][e] = (e < e_lim) ? vals[u] : static_cast<T>(0.0f);
-                }
-            } else if (p < n3 + n2 + kChunk / 4) {
-                *reinterpret_cast<uint4 *>(&dst.b2[(p - n3 - n2) * 4]) = v[sl];
+            } else if (p < n3 + kChunk / 4) {
+                *reinterpret_cast<uint4 *>(&dst.b2[(p - n3) * 4]) = v[sl];
             }
+        }
+#pragma unroll
+        for (int sl = 0; sl < kTapSlots; ++sl) {
+            const int j = tid + sl * NT;
+            if (j < kTaps) dst.w2[j % 9][j / 9] = t[sl];
         }
     }
 };
 
-// SHUF: the block is the gated branch of a ShuffleNetV2 unit.  Input and
-// output rows then hold 2*cb channels; the block's input is the second half
-// of each input row (cb channels, zero-extended to C on chip), and each
-// output row is the channel shuffle of (first half of the input row, block
-// output): output channel 2k = input channel k, 2k+1 = block output k.
-// cb * sizeof(T) must be a multiple of 4.  Without SHUF, cb is unused.
 template <typename T, bool DENSE, int MAXKS, int MAXMT, int MAXC, class CFG, bool SHUF>
 __global__ void __launch_bounds__(CFG::kThreads) __attribute__((amdgpu_waves_per_eu(CFG::kWpe)))
 k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int W, int C, int E,
@@ -393,16 +402,11 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
             L.aw[rr] = a;
             L.nw[rr] = nwd;
         }
-        // inclusive scans of the per-row counts across the wave
+        // inclusive scans of the per-row counts across the wave, both counts
+        // in one 32-bit value (each total is at most 52 x 64 < 2^16)
         const int cn = __popcll(nwd), ca = __popcll(a);
-        int sn = cn, sa = ca;
-        for (int off = 1; off < kWave; off <<= 1) {
-            const int tn = __shfl_up(sn, off), ta = __shfl_up(sa, off);
-            if (lane >= off) {
-                sn += tn;
-                sa += ta;
-            }
-        }
+        const int s2 = wave_scan_incl(cn | (ca << 16));
+        const int sn = s2 & 0xffff, sa = s2 >> 16;
         if (rr < nreg) {
             L.need_off[rr] = sn - cn;
             L.act_off[rr] = sa - ca;
@@ -414,11 +418,8 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
         if (!DENSE && band_counts) {
             // this patch's active and dilated counts (a plain store per patch:
             // atomics on one address from every XCD serialise)
-            int pa = ca, pd = __popcll(dil_own);
-            for (int off = 32; off > 0; off >>= 1) {
-                pa += __shfl_down(pa, off);
-                pd += __shfl_down(pd, off);
-            }
+            const int pa = __builtin_amdgcn_readlane(sa, kWave - 1);
+            const int pd = __builtin_amdgcn_readlane(wave_scan_incl(__popcll(dil_own)), kWave - 1);
             if (lane == 0) *reinterpret_cast<int2 *>(band_counts + 2 * patch) = make_int2(pa, pd);
         }
     }
