@@ -59,6 +59,10 @@ def _load():
     i32 = ctypes.c_int
     lib.oracle_mask.argtypes = [P, i32, i32, i32, i32, P, ctypes.c_float, P, P]
     lib.oracle_mask.restype = None
+    lib.oracle_mask_gsoftmax.argtypes = [P, i32, i32, i32, i32, P, ctypes.c_float, P, P]
+    lib.oracle_mask_gsoftmax.restype = None
+    lib.oracle_gsoftmax_decisions.argtypes = [P, ctypes.c_int64, P]
+    lib.oracle_gsoftmax_decisions.restype = None
     lib.oracle_dilate.argtypes = [P, i32, i32, i32, i32, P]
     lib.oracle_dilate.restype = None
     lib.oracle_indices.argtypes = [P, P, i32, i32, i32, P, P, P, P]
@@ -96,6 +100,29 @@ def mask(x_nchw, w_m, b_m):
     lib.oracle_mask(_ptr(x), N, C, H, W, _ptr(w), ctypes.c_float(float(np.float32(b_m))),
                     _ptr(G), _ptr(m))
     return G, m
+
+
+def mask_gsoftmax(x_nchw, w_m, b_m):
+    """Mask unit with the G-Softmax hard decision at inference (Sec. 3.1.2:
+    Eq. 5 with zero noise and tau = 1 over the probabilities of Eq. 6-7),
+    fp32.  Returns (G uint8 [N*H*W], logits fp32 [N*H*W])."""
+    lib = _load()
+    x = _c(x_nchw, np.float32)
+    N, C, H, W = x.shape
+    G = np.empty(N * H * W, np.uint8)
+    m = np.empty(N * H * W, np.float32)
+    lib.oracle_mask_gsoftmax(_ptr(x), N, C, H, W, _ptr(_c(w_m, np.float32)), ctypes.c_float(b_m),
+                             _ptr(G), _ptr(m))
+    return G, m
+
+
+def gsoftmax_decisions(m):
+    """The G-Softmax hard decision of each fp32 logit m (uint8)."""
+    lib = _load()
+    m = _c(m, np.float32).reshape(-1)
+    z = np.empty(m.size, np.uint8)
+    lib.oracle_gsoftmax_decisions(_ptr(m), ctypes.c_int64(m.size), _ptr(z))
+    return z
 
 
 def dilate(G, N, H, W, r=1):

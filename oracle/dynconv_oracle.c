@@ -71,6 +71,44 @@ void oracle_mask(const float *x, int N, int C, int H, int W,
 }
 
 /*
+ * The G-Softmax variant of the hard decision at inference (Sec. 3.1.2):
+ * the class probabilities of Eq. 6 and Eq. 7, pi_1 = sigmoid(m) and
+ * pi_2 = 1 - pi_1, go through the Gumbel-Softmax of Eq. 5 with the noise
+ * fixed to zero and tau = 1, i.e. a softmax over log(pi_1), log(pi_2); the
+ * position is executed when the first class exceeds 1/2.  fp32 throughout,
+ * with the C library's expf and logf.
+ */
+static int gsoftmax_decision(float m)
+{
+    float p1 = 1.0f / (1.0f + expf(-m));
+    float p2 = 1.0f - p1;
+    float e1 = expf(logf(p1));
+    float e2 = expf(logf(p2));
+    return (e1 / (e1 + e2)) > 0.5f;
+}
+
+void oracle_mask_gsoftmax(const float *x, int N, int C, int H, int W,
+                          const float *w_m, float b_m, uint8_t *G, float *logits)
+{
+    for (int n = 0; n < N; ++n)
+        for (int h = 0; h < H; ++h)
+            for (int w = 0; w < W; ++w) {
+                float acc = 0.0f;
+                for (int c = 0; c < C; ++c)
+                    acc = fmaf(w_m[c], x[nchw(n, c, h, w, C, H, W)], acc);
+                float m = acc + b_m;
+                size_t i = ((size_t)n * H + h) * W + w;
+                if (logits) logits[i] = m;
+                G[i] = (uint8_t)gsoftmax_decision(m);
+            }
+}
+
+void oracle_gsoftmax_decisions(const float *m, int64_t n, uint8_t *z)
+{
+    for (int64_t i = 0; i < n; ++i) z[i] = (uint8_t)gsoftmax_decision(m[i]);
+}
+
+/*
  * Mask dilation (Sec. 3.2, "Mask dilation"): G_dilated is the morphological
  * dilation of G with a (2r+1) x (2r+1) square, clipped to each image (it
  * never reaches into the next image of the batch).

@@ -146,3 +146,46 @@ def test_percentile_bias_gives_exact_density(orc, density):
     b = inputs.percentile_bias(s, density)
     G, _ = orc.mask(xc, w, b)
     assert int(G.sum()) == inputs.density_count(density, s.size)
+
+
+# ------------------------------------------------------------------ G-Softmax decision
+def test_gsoftmax_decision_is_the_sign_outside_the_rounding_band(orc):
+    """In exact arithmetic the G-Softmax decision (Eq. 5 at zero noise and
+    tau = 1 over the probabilities of Eq. 6-7) is sigmoid(m) > 1/2, i.e.
+    m > 0.  fp32 rounding of sigmoid(m) near 1/2 can only matter for |m| below
+    a few ulps of 1 (about 1e-7): outside |m| < 2^-20 the decision must be the
+    sign, over a log-spaced sweep of both signs, and the extremes and NaN."""
+    mags = np.float32(2.0) ** np.arange(-20, 127, 0.25, dtype=np.float64).astype(np.float32)
+    m = np.concatenate([mags, -mags, np.array([np.inf, -np.inf, np.nan], np.float32)])
+    z = orc.gsoftmax_decisions(m)
+    with np.errstate(invalid="ignore"):
+        want = (m > 0).astype(np.uint8)
+    assert np.array_equal(z, want)
+
+
+def test_gsoftmax_decision_against_float64_evaluation(orc):
+    """The same formula in float64 (with numpy's exp and log) decides the
+    same way for every |m| >= 2^-20, on random logits of both signs."""
+    rng = np.random.default_rng(17)
+    m = (rng.normal(0, 1, 20000) * 10.0 ** rng.uniform(-6, 3, 20000)).astype(np.float32)
+    m = m[np.abs(m) >= 2.0 ** -20]
+    with np.errstate(over="ignore"):
+        p1 = 1.0 / (1.0 + np.exp(-m.astype(np.float64)))
+    with np.errstate(divide="ignore"):
+        e1, e2 = np.exp(np.log(p1)), np.exp(np.log1p(-p1))
+    want = (e1 / (e1 + e2) > 0.5).astype(np.uint8)
+    assert np.array_equal(orc.gsoftmax_decisions(m), want)
+
+
+def test_gsoftmax_mask_unit_shares_the_logits(orc):
+    """The G-Softmax mask unit computes the same pinned fp32 logits as the
+    G-Binary one and applies the G-Softmax decision to each."""
+    rng = np.random.default_rng(23)
+    x = rng.normal(0, 1, (2, 8, 5, 7)).astype(np.float32)
+    w = rng.normal(0, 0.3, 8).astype(np.float32)
+    G1, m1 = orc.mask(x, w, 0.05)
+    G2, m2 = orc.mask_gsoftmax(x, w, 0.05)
+    assert m1.tobytes() == m2.tobytes()
+    assert np.array_equal(G2, orc.gsoftmax_decisions(m2))
+    band = np.abs(m1) < 2.0 ** -20
+    assert np.array_equal(G1[~band], G2[~band])
