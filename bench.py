@@ -27,6 +27,7 @@ Also reported on the same JSON line:
                 kernels), sparse and dense, with per-kernel HBM fractions
   shufflenet    ShuffleNetV2 stride-1 units (gated branch) at 64 x 28x28x116 and
                 64 x 14x14x232, bf16, density 0.3: one unit and 3 / 7 units
+  mask_variants the stack with G-Softmax mask units against G-Binary ones
   bandwidth_probes
                 the chain's mask / gather+expand / depthwise+scatter kernels and
                 the one-launch block at batches moving >= 512 MB per kernel,
@@ -332,6 +333,21 @@ def chain_report(dc, torch, wl, x0, sparse_blocks, dense_blocks, counts, use_gra
             out["kernels"]["%s %s" % (k, tag)] = {"avg_us": v["avg_us"], "launches": v["launches"],
                                                   "algorithmic_bytes": b, "gbs": gbs,
                                                   "hbm_frac": gbs / HBM_PEAK_GBS}
+    return out
+
+
+def mask_variants(dc, torch, wl, x0, sparse_blocks, t_gbinary, use_graph, steps, warmup, profile_steps):
+    """The stack with G-Softmax mask units (Sec. 3.1.2, Table 1's G-Softmax
+    row) beside the G-Binary stack: step time, and the chain's mask-unit
+    kernel in both modes."""
+    gs = Runner(dc, torch, x0, sparse_blocks, dc.STACK_GSOFTMAX, use_graph, wl.blocks)
+    t_gs = gs.timed(steps, warmup)
+    out = {"gbinary_ms_per_step": 1e3 * t_gbinary, "gsoftmax_ms_per_step": 1e3 * t_gs,
+           "gsoftmax_images_per_s": wl.n / t_gs, "gsoftmax_over_gbinary": t_gs / t_gbinary}
+    for tag, flags in (("gbinary", dc.STACK_UNFUSED), ("gsoftmax", dc.STACK_UNFUSED | dc.STACK_GSOFTMAX)):
+        r = Runner(dc, torch, x0, sparse_blocks, flags, False, wl.blocks)
+        prof, _ = profile_kernels(dc, torch, r, profile_steps)
+        out["chain_k_mask_us_" + tag] = prof["k_mask"]["avg_us"]
     return out
 
 
@@ -765,6 +781,10 @@ def main():
         log("kernel chain")
         result["chain"] = chain_report(dc, torch, wl, x0, sparse_blocks, dense_blocks, counts, use_graph,
                                        min(args.steps, 50), min(args.warmup, 5), args.profile_steps)
+    if not args.unfused:
+        log("mask variants")
+        result["mask_variants"] = mask_variants(dc, torch, wl, x0, sparse_blocks, t_sp, use_graph,
+                                                min(args.steps, 100), min(args.warmup, 10), args.profile_steps)
     if not args.no_probes:
         log("bandwidth probes")
         result["bandwidth_probes"] = bandwidth_probes(dc, inputs, torch)

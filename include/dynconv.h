@@ -141,6 +141,22 @@ dynconv_status dynconv_mask(const void *x, dynconv_shape s, dynconv_dtype dt,
                             const float *w_mask, float b_mask,
                             uint8_t *mask, float *logits, void *stream);
 
+/*
+ * The same mask unit with the G-Softmax hard decision at inference
+ * (Sec. 3.1.2, the variant of Table 1 that keeps the softmax and the
+ * logarithms): with m as above (fp32),
+ *   p1 = 1 / (1 + exp(-m)),  p2 = 1 - p1          (Eq. 6, Eq. 7)
+ *   y1 = exp(log p1) / (exp(log p1) + exp(log p2))  (Eq. 5, zero noise, tau = 1)
+ *   mask[i] = y1 > 1/2 ? 1 : 0
+ * in fp32 with the device's expf and logf.  In exact arithmetic y1 = p1 and
+ * the decision equals dynconv_mask's; in fp32 the two differ only where the
+ * rounding of p1 near 1/2 decides, i.e. for |m| below about 1e-7.
+ * Arguments, logits and errors as dynconv_mask.
+ */
+dynconv_status dynconv_mask_gsoftmax(const void *x, dynconv_shape s, dynconv_dtype dt,
+                                     const float *w_mask, float b_mask, uint8_t *mask, float *logits,
+                                     void *stream);
+
 /* Workspace bytes that dynconv_build_indices needs for shape s. */
 size_t dynconv_indices_workspace_bytes(dynconv_shape s);
 
@@ -184,6 +200,7 @@ dynconv_status dynconv_block_forward(const void *x, void *y, dynconv_shape s, dy
 /* Flags of dynconv_stack_forward. */
 #define DYNCONV_STACK_DENSE 1   /* every block on all positions (Eq. 1), no mask units */
 #define DYNCONV_STACK_UNFUSED 2 /* force the multi-kernel chain (mask, index maps, block) */
+#define DYNCONV_STACK_GSOFTMAX 4 /* mask units decide as dynconv_mask_gsoftmax (Sec. 3.1.2) */
 
 /* Workspace bytes that dynconv_stack_forward needs for these blocks and flags. */
 size_t dynconv_stack_workspace_bytes(dynconv_shape s, const dynconv_block *blks,
@@ -217,7 +234,8 @@ size_t dynconv_stack_workspace_bytes(dynconv_shape s, const dynconv_block *blks,
  *   y      (device) NHWC output; y == x runs in place, other overlap is
  *          DYNCONV_ERR_SHAPE
  *   blks   (host array of n_blocks, device weights), 1 <= n_blocks <= 1024
- *   flags  0 or DYNCONV_STACK_DENSE / DYNCONV_STACK_UNFUSED (others: ERR_ARG)
+ *   flags  0 or DYNCONV_STACK_DENSE / DYNCONV_STACK_UNFUSED / DYNCONV_STACK_GSOFTMAX
+ *          (others: ERR_ARG)
  *   masks  (device) uint8 [n_blocks][N*H*W] or NULL: per-block hard masks
  *   counts (device) int32 [n_blocks][2] or NULL: per-block P, P_d
  *   ws     (device) dynconv_stack_workspace_bytes bytes of scratch
@@ -281,7 +299,7 @@ dynconv_status dynconv_stack_forward_profiled(const void *x, void *y, dynconv_sh
  *   x, y   (device) NHWC, shape s (s.c even), dtype dt; must not overlap
  *   branches (host array of n_units, device weights), 1 <= n_units <= 1024
  *   flags  0 or DYNCONV_STACK_DENSE (every branch on all positions, no mask
- *          units) / DYNCONV_STACK_UNFUSED; others: ERR_ARG
+ *          units) / DYNCONV_STACK_UNFUSED / DYNCONV_STACK_GSOFTMAX; others: ERR_ARG
  *   masks  (device) uint8 [n_units][N*H*W] or NULL: per-unit hard masks
  *   counts (device) int32 [n_units][2] or NULL: per-unit P, P_d
  *   ws     (device) dynconv_shuffle_stack_workspace_bytes bytes of scratch

@@ -145,11 +145,11 @@ size_t hidden_bytes(dynconv_shape s, int E, dynconv_dtype dt) {
 // ------------------------------------------------------------ launches
 template <typename T>
 void launch_mask(const void *x, dynconv_shape s, const float *w_m, float b_m, uint8_t *mask,
-                 float *logits, hipStream_t st, Marks &mk) {
+                 float *logits, int mode, hipStream_t st, Marks &mk) {
     int64_t n = positions(s);
     int grid = static_cast<int>((n + kBlock - 1) / kBlock);
     launch(mk, k_mask<T>, dim3(grid), dim3(kBlock), 0, st, static_cast<const T *>(x), n, s.c, w_m,
-           b_m, mask, logits);
+           b_m, mask, logits, mode);
 }
 
 void launch_indices(const uint8_t *mask, dynconv_shape s, int dilate, const dynconv_indices *idx,
@@ -244,10 +244,10 @@ void launch_copy(const void *src, void *dst, size_t bytes, hipStream_t st, Marks
 }
 
 void dispatch_mask(dynconv_dtype dt, const void *x, dynconv_shape s, const float *w_m, float b_m,
-                   uint8_t *mask, float *logits, hipStream_t st, Marks &mk) {
-    if (dt == DYNCONV_F32) launch_mask<float>(x, s, w_m, b_m, mask, logits, st, mk);
-    else if (dt == DYNCONV_F16) launch_mask<half_t>(x, s, w_m, b_m, mask, logits, st, mk);
-    else launch_mask<bf16_t>(x, s, w_m, b_m, mask, logits, st, mk);
+                   uint8_t *mask, float *logits, int mode, hipStream_t st, Marks &mk) {
+    if (dt == DYNCONV_F32) launch_mask<float>(x, s, w_m, b_m, mask, logits, mode, st, mk);
+    else if (dt == DYNCONV_F16) launch_mask<half_t>(x, s, w_m, b_m, mask, logits, mode, st, mk);
+    else launch_mask<bf16_t>(x, s, w_m, b_m, mask, logits, mode, st, mk);
 }
 
 // ------------------------------------------------------------ fused block
@@ -282,6 +282,7 @@ struct FusedMasks {
     // nonzero: the block is the branch of a ShuffleNetV2 unit with this many
     // channels per half, reading and writing the unit's full rows
     int shuffle_cb = 0;
+    int mask_mode = 0;  // hard decision of the mask units (mask_decision)
 };
 
 template <typename T, bool DENSE, int MAXKS, int MAXMT, int MAXC>
@@ -300,7 +301,7 @@ void launch_fused_k(const void *src, void *dst, dynconv_shape s, const dynconv_b
            static_cast<const T *>(b->w_dw), b->b_dw, b->act_dw,
            static_cast<const T *>(b->w_project), b->b_project, b->act_project,
            next ? next->w_mask : nullptr, next ? next->b_mask : 0.0f,
-           next ? fm.mask_next : nullptr, fm.band_counts);
+           next ? fm.mask_next : nullptr, fm.band_counts, fm.mask_mode);
 }
 
 template <typename T, bool DENSE>
@@ -336,6 +337,10 @@ void dispatch_block(dynconv_dtype dt, const void *x, void *y, dynconv_shape s, c
 // ------------------------------------------------------------ stacks
 constexpr int32_t kStackDense = 1;
 constexpr int32_t kStackUnfused = 2;
+constexpr int32_t kStackGSoftmax = 4;
+constexpr int32_t kStackFlags = kStackDense | kStackUnfused | kStackGSoftmax;
+
+int mask_mode_of(int32_t flags) { return (flags & kStackGSoftmax) ? 1 : 0; }
 
 // The one-launch block kernel covers up to 64 channels; wider blocks run the
 // unfused kernel chain.
@@ -381,7 +386,7 @@ dynconv_status stack_checked(const void *x, void *y, dynconv_shape s, dynconv_dt
     if (!x || !y || !blks) return DYNCONV_ERR_NULL;
     if (!dtype_ok(dt)) return DYNCONV_ERR_DTYPE;
     if (n_blocks < 1 || n_blocks > kMaxBlocks) return DYNCONV_ERR_ARG;
-    if (flags & ~(kStackDense | kStackUnfused)) return DYNCONV_ERR_ARG;
+    if (flags & ~kStackFlags) return DYNCONV_ERR_ARG;
     if (dynconv_status st = check_shape(s, true)) return st;
     for (int32_t b = 0; b < n_blocks; ++b)
         if (dynconv_status st = check_block(&blks[b], s, !(flags & kStackDense))) return st;
@@ -430,6 +435,7 @@ void stack_walk(const void *x, void *y, dynconv_shape s, dynconv_dtype dt, const
             void *dst = ((n_blocks - 1 - b) % 2 == 0) ? y : tb;
             const dynconv_block *next = (b + 1 < n_blocks) ? &blks[b + 1] : nullptr;
             FusedMasks fm;
+            fm.mask_mode = mask_mode_of(flags);
             fm.self = (b == 0);  // block 0 runs its own mask unit on the staged x
             fm.mask_in = (b == 0) ? nullptr : mask_of(b);
             fm.mask_self = mask_of(0);
@@ -472,7 +478,7 @@ void stack_walk(const void *x, void *y, dynconv_shape s, dynconv_dtype dt, const
         plan.note("k_expand");
         plan.note("k_dw_project");
         if (run) {
-            dispatch_mask(dt, y, s, blks[b].w_mask, blks[b].b_mask, mask_b, nullptr, st, mk);
+            dispatch_mask(dt, y, s, blks[b].w_mask, blks[b].b_mask, mask_b, nullptr, mask_mode_of(flags), st, mk);
             launch_indices(mask_b, s, 1, &idx, scratch, st, mk);
             dispatch_block(dt, y, y, s, &blks[b], &idx, h1, st, mk);
         }
@@ -528,7 +534,7 @@ dynconv_status shuffle_checked(const void *x, void *y, dynconv_shape s, dynconv_
     if (!x || !y || !br) return DYNCONV_ERR_NULL;
     if (!dtype_ok(dt)) return DYNCONV_ERR_DTYPE;
     if (n_units < 1 || n_units > kMaxBlocks) return DYNCONV_ERR_ARG;
-    if (flags & ~(kStackDense | kStackUnfused)) return DYNCONV_ERR_ARG;
+    if (flags & ~kStackFlags) return DYNCONV_ERR_ARG;
     if (dynconv_status st = check_shape(s, true)) return st;
     if (s.c % 2 != 0) return DYNCONV_ERR_SHAPE;
     const dynconv_shape bs = branch_shape(s, br);
@@ -596,6 +602,7 @@ void shuffle_walk(const void *x, void *y, dynconv_shape s, dynconv_dtype dt, con
     if (SL.direct) {
         for (int32_t u = 0; u < n_units; ++u) {
             FusedMasks fm;
+            fm.mask_mode = mask_mode_of(flags);
             fm.shuffle_cb = cb;
             if (!dense) {
                 fm.self = true;  // the unit's mask unit on the staged branch half
@@ -622,6 +629,7 @@ void shuffle_walk(const void *x, void *y, dynconv_shape s, dynconv_dtype dt, con
         const void *bout = bin;
         if (L.fused) {
             FusedMasks fm;
+            fm.mask_mode = mask_mode_of(flags);
             if (!dense) {
                 fm.self = true;  // the unit's mask unit on the staged branch input
                 fm.mask_self = masks ? mask_of(u) : nullptr;
@@ -643,7 +651,8 @@ void shuffle_walk(const void *x, void *y, dynconv_shape s, dynconv_dtype dt, con
             plan.note("k_expand");
             plan.note("k_dw_project");
             if (run) {
-                dispatch_mask(dt, bin, bs, br[u].w_mask, br[u].b_mask, mask_of(u), nullptr, st, mk);
+                dispatch_mask(dt, bin, bs, br[u].w_mask, br[u].b_mask, mask_of(u), nullptr, mask_mode_of(flags),
+                              st, mk);
                 launch_indices(mask_of(u), bs, 1, &idx, ib + L.scratch, st, mk);
                 dispatch_block(dt, bin, bin, bs, &br[u], &idx, ib + L.hidden, st, mk);
             }
@@ -679,8 +688,8 @@ const char *dynconv_status_str(dynconv_status status) {
 
 const char *dynconv_version(void) { return "dynconv-mi355x 0.1 (gfx950)"; }
 
-dynconv_status dynconv_mask(const void *x, dynconv_shape s, dynconv_dtype dt, const float *w_mask,
-                            float b_mask, uint8_t *mask, float *logits, void *stream) {
+static dynconv_status mask_common(const void *x, dynconv_shape s, dynconv_dtype dt, const float *w_mask,
+                                  float b_mask, uint8_t *mask, float *logits, int mode, void *stream) {
     if (!x || !w_mask || !mask) return DYNCONV_ERR_NULL;
     if (!dtype_ok(dt)) return DYNCONV_ERR_DTYPE;
     if (dynconv_status st = check_shape(s, true)) return st;
@@ -688,8 +697,19 @@ dynconv_status dynconv_mask(const void *x, dynconv_shape s, dynconv_dtype dt, co
     if (!aligned16(x)) return DYNCONV_ERR_ALIGN;
     (void)hipGetLastError();
     Marks mk;
-    dispatch_mask(dt, x, s, w_mask, b_mask, mask, logits, static_cast<hipStream_t>(stream), mk);
+    dispatch_mask(dt, x, s, w_mask, b_mask, mask, logits, mode, static_cast<hipStream_t>(stream), mk);
     return launch_status();
+}
+
+dynconv_status dynconv_mask(const void *x, dynconv_shape s, dynconv_dtype dt, const float *w_mask,
+                            float b_mask, uint8_t *mask, float *logits, void *stream) {
+    return mask_common(x, s, dt, w_mask, b_mask, mask, logits, 0, stream);
+}
+
+dynconv_status dynconv_mask_gsoftmax(const void *x, dynconv_shape s, dynconv_dtype dt,
+                                     const float *w_mask, float b_mask, uint8_t *mask, float *logits,
+                                     void *stream) {
+    return mask_common(x, s, dt, w_mask, b_mask, mask, logits, 1, stream);
 }
 
 size_t dynconv_indices_workspace_bytes(dynconv_shape s) {
@@ -793,7 +813,7 @@ int32_t dynconv_stack_launch_names(dynconv_shape s, const dynconv_block *blks, i
                                    dynconv_dtype dt, int32_t flags, int32_t in_place,
                                    const char **names, int32_t cap) {
     if (!blks || n_blocks < 1 || n_blocks > kMaxBlocks || !dtype_ok(dt) ||
-        check_shape(s, true) != DYNCONV_OK || (flags & ~(kStackDense | kStackUnfused)))
+        check_shape(s, true) != DYNCONV_OK || (flags & ~kStackFlags))
         return -1;
     StackLayout L = stack_layout(s, blks, n_blocks, dt, flags);
     Plan plan{false, names, names ? cap : 0};
@@ -861,7 +881,7 @@ int32_t dynconv_shuffle_stack_launch_names(dynconv_shape s, const dynconv_block 
                                            const char **names, int32_t cap) {
     if (!branches || n_units < 1 || n_units > kMaxBlocks || !dtype_ok(dt) ||
         check_shape(s, true) != DYNCONV_OK || s.c % 2 != 0 || branches[0].c_in <= 0 ||
-        (flags & ~(kStackDense | kStackUnfused)))
+        (flags & ~kStackFlags))
         return -1;
     ShuffleLayout L = shuffle_layout(s, branches, n_units, dt, flags);
     Plan plan{false, names, names ? cap : 0};

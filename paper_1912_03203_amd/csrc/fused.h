@@ -34,7 +34,8 @@
 // positions next to this one as their ring.  Patch i writes its active and
 // dilated counts to band_counts[2i], [2i+1]; k_band_counts sums them.
 // The first block of a stack may compute its own mask (wm_self) from the
-// staged x instead of reading one.
+// staged x instead of reading one.  mask_mode selects the hard decision
+// (mask_decision: G-Binary or G-Softmax).
 #pragma once
 
 #include "kernels.h"
@@ -247,7 +248,7 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
               const T *__restrict__ w2, const float *__restrict__ b2, int act2,
               const T *__restrict__ w3, const float *__restrict__ b3, int act3,
               const float *__restrict__ wm_next, float bm_next, uint8_t *__restrict__ mask_next,
-              int32_t *__restrict__ band_counts) {
+              int32_t *__restrict__ band_counts, int mask_mode) {
     typedef mma<T> M;
     constexpr int NW = CFG::kWaves, NT = CFG::kThreads, kRegion = CFG::kRegion;
     constexpr int kNeedTiles = ((kRegion + 15) / 16 + NW - 1) / NW;  // 16-slot tiles per wave
@@ -371,7 +372,7 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
 #pragma unroll
                     for (int u = 0; u < 8; ++u) a = __builtin_fmaf(wm_self[c0 + u], v[u], a);
                 }
-                bit = (a + bm_self) > 0.0f;
+                bit = mask_decision(a + bm_self, mask_mode);
                 if (mask_self && rr >= 1 && rr <= rows_out && lane >= 1 && lane <= cols_out)
                     mask_self[(img + hh) * W + (w0 - 1 + lane)] = bit ? 1 : 0;
             } else {
@@ -625,7 +626,7 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
                 for (int u = 0; u < 8; ++u) a = __builtin_fmaf(wm_next[c0 + u], v[u], a);
             }
             const float m = a + bm_next;
-            mask_next[(img + h0 - 1 + rr) * W + (w0 - 1 + c)] = (m > 0.0f) ? 1 : 0;
+            mask_next[(img + h0 - 1 + rr) * W + (w0 - 1 + c)] = mask_decision(m, mask_mode) ? 1 : 0;
         }
     }
 }

@@ -198,10 +198,24 @@ __device__ __forceinline__ float activate(float v, int kind) {
 // ------------------------------------------------------------------- K1 mask
 // One lane per position: an fp32 fused multiply-add chain over the channels in
 // ascending order from +0, then the bias, then the strict threshold m > 0.
+// Hard decision of the mask unit at inference.  mode 0 (G-Binary, Eq. 8 with
+// the Gumbel noise fixed to zero): m > 0.  mode 1 (G-Softmax, Sec. 3.1.2):
+// the probabilities of Eq. 6 and Eq. 7, sigmoid(m) and 1 - sigmoid(m), go
+// through the Gumbel-Softmax of Eq. 5 at zero noise and tau = 1 (a softmax
+// over their logarithms) and the position runs when the first class exceeds
+// 1/2.  Both agree except where fp32 rounding decides, near m = 0.
+__device__ __forceinline__ bool mask_decision(float m, int mode) {
+    if (mode == 0) return m > 0.0f;
+    const float p1 = 1.0f / (1.0f + expf(-m));
+    const float p2 = 1.0f - p1;
+    const float e1 = expf(logf(p1)), e2 = expf(logf(p2));
+    return e1 / (e1 + e2) > 0.5f;
+}
+
 template <typename T>
 __global__ void __launch_bounds__(kBlock)
 k_mask(const T *__restrict__ x, int64_t npix, int C, const float *__restrict__ w_m, float b_m,
-       uint8_t *__restrict__ mask, float *__restrict__ logits) {
+       uint8_t *__restrict__ mask, float *__restrict__ logits, int mode) {
     int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
     if (i >= npix) return;
     const T *row = x + i * C;
@@ -213,7 +227,7 @@ k_mask(const T *__restrict__ x, int64_t npix, int C, const float *__restrict__ w
         for (int u = 0; u < 8; ++u) acc = __builtin_fmaf(w_m[c0 + u], v[u], acc);
     }
     float m = acc + b_m;
-    mask[i] = (m > 0.0f) ? 1 : 0;
+    mask[i] = mask_decision(m, mode) ? 1 : 0;
     if (logits) logits[i] = m;
 }
 

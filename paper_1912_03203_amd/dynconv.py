@@ -18,14 +18,15 @@ LIB_PATH = os.path.join(_HERE, "libdynconv.so")
 
 F32, F16, BF16 = 0, 1, 2
 ACT_NONE, ACT_RELU, ACT_RELU6 = 0, 1, 2
-STACK_DENSE, STACK_UNFUSED = 1, 2
+STACK_DENSE, STACK_UNFUSED, STACK_GSOFTMAX = 1, 2, 4
 
 _TORCH_DTYPE = {F32: torch.float32, F16: torch.float16, BF16: torch.bfloat16}
 _CODE = {torch.float32: F32, torch.float16: F16, torch.bfloat16: BF16}
 NAME_TO_DTYPE = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}
 
 EXPORTED = (
-    "dynconv_status_str", "dynconv_version", "dynconv_mask", "dynconv_indices_workspace_bytes",
+    "dynconv_status_str", "dynconv_version", "dynconv_mask", "dynconv_mask_gsoftmax",
+    "dynconv_indices_workspace_bytes",
     "dynconv_build_indices", "dynconv_block_workspace_bytes", "dynconv_block_forward",
     "dynconv_stack_workspace_bytes", "dynconv_stack_forward", "dynconv_stack_launch_names",
     "dynconv_stack_forward_profiled", "dynconv_shuffle_stack_workspace_bytes",
@@ -78,6 +79,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.dynconv_version.restype = ctypes.c_char_p
     lib.dynconv_mask.argtypes = [vp, Shape, ctypes.c_int, vp, ctypes.c_float, vp, vp, vp]
     lib.dynconv_mask.restype = ctypes.c_int
+    lib.dynconv_mask_gsoftmax.argtypes = [vp, Shape, ctypes.c_int, vp, ctypes.c_float, vp, vp, vp]
+    lib.dynconv_mask_gsoftmax.restype = ctypes.c_int
     lib.dynconv_indices_workspace_bytes.argtypes = [Shape]
     lib.dynconv_indices_workspace_bytes.restype = sz
     lib.dynconv_build_indices.argtypes = [vp, Shape, i32, ctypes.POINTER(Indices), vp, sz, vp]
@@ -200,15 +203,17 @@ class IndexBuffers:
 
 
 # ------------------------------------------------------------------ calls
-def mask(x: torch.Tensor, w_mask: torch.Tensor, b_mask: float, out=None, logits=None, stream=None):
-    """Hard mask of one block (uint8 [N*H*W]); optional fp32 logits."""
+def mask(x: torch.Tensor, w_mask: torch.Tensor, b_mask: float, out=None, logits=None, stream=None,
+         gsoftmax=False):
+    """Hard mask of one block (uint8 [N*H*W]); optional fp32 logits.  With
+    gsoftmax the G-Softmax decision (dynconv_mask_gsoftmax) is taken."""
     lib = load()
     n, h, w, _ = x.shape
     if out is None:
         out = torch.empty(n * h * w, dtype=torch.uint8, device=x.device)
-    _check(lib.dynconv_mask(_ptr(x), shape_of(x), dtype_code(x.dtype), _ptr(w_mask),
-                            ctypes.c_float(b_mask), _ptr(out), _ptr(logits), _stream(stream)),
-           "dynconv_mask")
+    fn = lib.dynconv_mask_gsoftmax if gsoftmax else lib.dynconv_mask
+    _check(fn(_ptr(x), shape_of(x), dtype_code(x.dtype), _ptr(w_mask), ctypes.c_float(b_mask), _ptr(out),
+              _ptr(logits), _stream(stream)), "dynconv_mask")
     return out
 
 

@@ -57,9 +57,10 @@ def fake_block(C=32, E=192, Co=None, acts=(2, 2, 0), **over):
     return b
 
 
-def test_mask_validation(lib):
+@pytest.mark.parametrize("entry", ["dynconv_mask", "dynconv_mask_gsoftmax"])
+def test_mask_validation(lib, entry):
     s = dc.Shape(2, 8, 8, 32)
-    f = lib.dynconv_mask
+    f = getattr(lib, entry)
     assert f(None, s, 1, FAKE, 0.0, FAKE, None, None) == ERR_NULL
     assert f(FAKE, s, 1, None, 0.0, FAKE, None, None) == ERR_NULL
     assert f(FAKE, s, 1, FAKE, 0.0, None, None, None) == ERR_NULL
@@ -154,7 +155,7 @@ def test_stack_validation(lib):
     assert f(FAKE, None, s, 1, blocks, 3, 0, None, None, FAKE, need, None) == ERR_NULL
     assert f(FAKE, FAKE, s, 1, blocks, 0, 0, None, None, FAKE, need, None) == ERR_ARG
     assert f(FAKE, FAKE, s, 1, blocks, 1025, 0, None, None, FAKE, need, None) == ERR_ARG
-    assert f(FAKE, FAKE, s, 1, blocks, 3, 4, None, None, FAKE, need, None) == ERR_ARG
+    assert f(FAKE, FAKE, s, 1, blocks, 3, 8, None, None, FAKE, need, None) == ERR_ARG
     assert f(FAKE, FAKE, s, 1, blocks, 3, 2, None, None, FAKE, need - 1, None) == ERR_WORKSPACE
     assert f(FAKE, FAKE, s, 1, blocks, 3, 0, None, None, FAKE, fused - 1, None) == ERR_WORKSPACE
     assert f(FAKE, FAKE + 64, s, 1, blocks, 3, 0, None, None, FAKE, fused, None) == ERR_SHAPE
