@@ -258,3 +258,6 @@ def shuffle_unit_forward(x_nchw, wts, w_m, b_m, dilate_r=1):
     out = dict(r)
     out["y"] = y
     return out
+
+
+from .network import conv1x1, conv3x3, dense_block, dwconv3x3, network_forward  # noqa: E402,F401

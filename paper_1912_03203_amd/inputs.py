@@ -252,3 +252,52 @@ def make_block_inputs(workload: Workload, seed: int):
         for blk, wm in zip(blocks, ellipse_mask_weights(rng, x, labels, wl.blocks)):
             blk["w_m"] = wm
     return x, blocks, labels
+
+
+# ------------------------------------------------------------------ whole networks
+# MobileNetV2 1.0x: the stem, then (expansion t, width c, repeats n, stride s)
+# per stage, then the final 1x1 convolution to 1280.
+MBV2_STEM = 32
+MBV2_STAGES = ((1, 16, 1, 1), (6, 24, 2, 2), (6, 32, 3, 2), (6, 64, 4, 2), (6, 96, 3, 1), (6, 160, 3, 2),
+               (6, 320, 1, 1))
+MBV2_LAST = 1280
+
+
+def mbv2_layers(rng, dtype="f16", std=0.05, mask_std=0.1, in_c=3):
+    """Folded-BN weights of a MobileNetV2 feature extractor as a layer list
+    (dicts; PyTorch layouts, storage-rounded weights, fp32 biases).  Every
+    block with stride 1 and equal input and output widths is gated: it carries
+    a mask unit w_m and "gated": True."""
+    def wgt(*shape):
+        return round_to_storage(rng.normal(0.0, std, size=shape), dtype)
+
+    def bias(n):
+        return rng.normal(0.0, std, size=n).astype(np.float32)
+
+    layers = [{"kind": "conv3x3", "w": wgt(MBV2_STEM, in_c, 3, 3), "b": bias(MBV2_STEM), "stride": 2, "act": 2}]
+    c_in = MBV2_STEM
+    for t, c, n, s in MBV2_STAGES:
+        for i in range(n):
+            stride = s if i == 0 else 1
+            e = c_in * t
+            layer = {"kind": "block", "stride": stride, "acts": (2, 2, 0),
+                     "w1": wgt(e, c_in) if t != 1 else None, "b1": bias(e) if t != 1 else None,
+                     "w2": wgt(e, 9), "b2": bias(e), "w3": wgt(c, e), "b3": bias(c)}
+            if stride == 1 and c_in == c:
+                layer["gated"] = True
+                layer["w_m"] = rng.normal(0.0, mask_std, size=c_in).astype(np.float32)
+            layers.append(layer)
+            c_in = c
+    layers.append({"kind": "conv1x1", "w": wgt(MBV2_LAST, c_in), "b": bias(MBV2_LAST), "act": 2})
+    return layers
+
+
+def make_network_inputs(seed, n, h, w, dtype="f16", density_range=(0.2, 0.6)):
+    """Smooth random blob images (3 channels), the MobileNetV2 layer list and a
+    target density per gated block ~ U[density_range]."""
+    rng = rng_for(seed)
+    x = round_to_storage(blob_features(rng, n, h, w, 3), dtype)
+    layers = mbv2_layers(rng, dtype)
+    ngated = sum(1 for l in layers if l.get("gated"))
+    dens = rng.uniform(density_range[0], density_range[1], size=ngated)
+    return x, layers, dens
