@@ -329,6 +329,93 @@ dynconv_status dynconv_shuffle_stack_forward_profiled(const void *x, void *y, dy
                                                       void *stream, void *const *events,
                                                       int32_t n_events);
 
+/*
+ * Whole networks: a MobileNetV2 feature extractor whose stride-1 residual
+ * blocks are gated (Sec. 3.1.1: every residual block gets its own mask unit;
+ * Sec. 4.1.2: dynamic convolutions in MobileNetV2, with the stem, the strided
+ * and the width-changing blocks evaluated at every position).
+ */
+typedef enum {
+    DYNCONV_LAYER_CONV3X3 = 0, /* full 3x3 convolution, zero padding 1 (the stem) */
+    DYNCONV_LAYER_BLOCK = 1,   /* inverted-residual block */
+    DYNCONV_LAYER_CONV1X1 = 2  /* pointwise convolution */
+} dynconv_layer_kind;
+
+/*
+ * One layer (host struct, device weights; PyTorch layouts in the storage
+ * dtype, fp32 biases):
+ *   CONV3X3  w [c_out][c_in][3][3], b [c_out], act, stride 1 or 2;
+ *            y[o][i][j] = act(sum w[o][c][kh][kw] x[c][s*i+kh-1][s*j+kw-1] + b[o]),
+ *            output (H-1)/stride+1 x (W-1)/stride+1; 1 <= c_in <= 16,
+ *            c_out a multiple of 8, 9*c_in*c_out + c_out <= 16384
+ *   CONV1X1  w [c_out][c_in], b [c_out], act; c_in, c_out multiples of 8
+ *   BLOCK    blk: expansion 1x1 (w_expand NULL for an expansion factor of 1,
+ *            then c_hidden = c_in), depthwise 3x3 with `stride`, projection
+ *            1x1, each with its activation; the block adds its input when
+ *            stride is 1 and c_in == c_out (Eq. 1, r = identity).
+ *            gated = 1 (stride 1, c_in == c_out, w_expand present): the gated
+ *            block of Eq. 3 with blk's mask unit, executed as
+ *            dynconv_stack_forward executes one block (constraints of
+ *            dynconv_block apply); gated = 0: every position.
+ * c_in/c_out of BLOCK layers are blk.c_in/blk.c_out; the layer's own c_in,
+ * c_out, w, b, act are for the convolutions.
+ */
+typedef struct {
+    int32_t kind;
+    int32_t stride;
+    int32_t gated;
+    int32_t c_in, c_out;
+    const void *w;
+    const float *b;
+    int32_t act;
+    dynconv_block blk;
+} dynconv_layer;
+
+/* Output shape of a layer list applied to `in` (its c = the first layer's
+ * c_in); errors as dynconv_network_forward's validation. */
+dynconv_status dynconv_network_output_shape(dynconv_shape in, const dynconv_layer *layers, int32_t n_layers,
+                                            dynconv_shape *out);
+
+/* Workspace bytes of dynconv_network_forward (0 for invalid arguments). */
+size_t dynconv_network_workspace_bytes(dynconv_shape in, const dynconv_layer *layers, int32_t n_layers,
+                                       dynconv_dtype dt, int32_t flags);
+
+/*
+ * y = layers(x), one stream, no host synchronisation.
+ *   x      (device) NHWC input, shape `in`, dtype dt
+ *   y      (device) NHWC output of dynconv_network_output_shape; must not
+ *          overlap x
+ *   layers (host array of n_layers, device weights), 1 <= n_layers <= 1024
+ *   flags  0 / DYNCONV_STACK_DENSE (gated blocks on every position, no mask
+ *          units) / DYNCONV_STACK_UNFUSED / DYNCONV_STACK_GSOFTMAX (as for
+ *          dynconv_stack_forward; others: ERR_ARG)
+ *   masks  (device) uint8 or NULL: the hard masks of the gated blocks in
+ *          layer order, each N*H*W of that block's resolution, concatenated
+ *   counts (device) int32 [number of gated blocks][2] or NULL: P, P_d
+ *   ws     (device) dynconv_network_workspace_bytes bytes of scratch
+ * Every layer is validated before anything is enqueued (ERR_SHAPE for a
+ * width that does not chain, ERR_UNSUPPORTED for widths the kernels do not
+ * take, ERR_ARG for a bad kind, stride or activation).
+ */
+dynconv_status dynconv_network_forward(const void *x, void *y, dynconv_shape in, dynconv_dtype dt,
+                                       const dynconv_layer *layers, int32_t n_layers, int32_t flags,
+                                       uint8_t *masks, int32_t *counts, void *ws, size_t ws_bytes,
+                                       void *stream);
+
+/* Launch sequence of dynconv_network_forward, as dynconv_stack_launch_names;
+ * with_counts says whether the call will pass counts (each gated block then
+ * ends with its count reduction). */
+int32_t dynconv_network_launch_names(dynconv_shape in, const dynconv_layer *layers, int32_t n_layers,
+                                     dynconv_dtype dt, int32_t flags, int32_t with_counts, const char **names,
+                                     int32_t cap);
+
+/* dynconv_network_forward with per-kernel event pairs, as
+ * dynconv_stack_forward_profiled. */
+dynconv_status dynconv_network_forward_profiled(const void *x, void *y, dynconv_shape in, dynconv_dtype dt,
+                                                const dynconv_layer *layers, int32_t n_layers, int32_t flags,
+                                                uint8_t *masks, int32_t *counts, void *ws, size_t ws_bytes,
+                                                void *stream, void *const *events, int32_t n_events);
+
 #ifdef __cplusplus
 }
 #endif

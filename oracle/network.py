@@ -86,7 +86,7 @@ def dense_block(x, layer):
     return conv1x1(h, layer["w3"], layer["b3"], acts[2], residual=res)
 
 
-def network_forward(x_nchw, layers, biases=None, round_to=None):
+def network_forward(x_nchw, layers, biases=None, round_to=None, keep_inputs=False):
     """Forward through a layer list.  Layer kinds:
       "conv3x3": w [O][C][3][3], b, stride, act
       "block":   w1/b1 (or w1 None), w2/b2, w3/b3, stride; gated blocks
@@ -97,13 +97,16 @@ def network_forward(x_nchw, layers, biases=None, round_to=None):
     with masked output); with biases None every gated block runs dense.
     round_to(a) (optional) rounds each layer's output to the storage type
     before the next layer, as the device stores it.  Returns (y, gates) with
-    gates a list of dicts (G, A, D, input x) per gated block."""
+    gates a list of dicts (G, A, D, input x) per gated block; with
+    keep_inputs, (y, gates, inputs) with every layer's input."""
     from . import block_forward
 
     x = np.asarray(x_nchw, np.float64)
     gates = []
+    inputs_ = []
     gi = 0
     for layer in layers:
+        inputs_.append(x)
         kind = layer["kind"]
         if kind == "conv3x3":
             x = conv3x3(x, layer["w"], layer["b"], layer["stride"], layer["act"])
@@ -121,4 +124,6 @@ def network_forward(x_nchw, layers, biases=None, round_to=None):
             x = dense_block(x, layer)
         if round_to is not None:
             x = round_to(x)
+    if keep_inputs:
+        return x, gates, inputs_
     return x, gates

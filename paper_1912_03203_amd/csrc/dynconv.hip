@@ -6,12 +6,14 @@
 #include <hip/hip_runtime.h>
 
 #include <stdint.h>
+#include <algorithm>
 #include <string.h>
 
 #include "dynconv.h"
 #include "fused.h"
 #include "kernels.h"
 #include "shuffle.h"
+#include "dense.h"
 
 using namespace dynconv;
 
@@ -403,6 +405,7 @@ struct Plan {
     const char **names;
     int32_t cap;
     int32_t count = 0;
+    bool list_counts = true;  // a plan without execution lists the count reduction
     bool note(const char *name) {
         if (names && count < cap) names[count] = name;
         ++count;
@@ -445,7 +448,7 @@ void stack_walk(const void *x, void *y, dynconv_shape s, dynconv_dtype dt, const
             src = dst;
         }
         // P, P_d per block only on request (listed in every plan)
-        if (!dense && (counts || !plan.exec) && plan.note("k_band_counts"))
+        if (!dense && (counts || (!plan.exec && plan.list_counts)) && plan.note("k_band_counts"))
             launch(mk, k_band_counts, dim3(n_blocks), dim3(kBlock), 0, st,
                    static_cast<const int32_t *>(band_counts), nbands, cnt_all);
         return;
@@ -612,7 +615,7 @@ void shuffle_walk(const void *x, void *y, dynconv_shape s, dynconv_dtype dt, con
             const void *xu = (u == 0) ? x : out_of(u - 1);
             if (plan.note("k_block_fused")) dispatch_fused(dt, dense, xu, out_of(u), bs, &br[u], nullptr, fm, st, mk);
         }
-        if (!dense && (counts || !plan.exec) && plan.note("k_band_counts"))
+        if (!dense && (counts || (!plan.exec && plan.list_counts)) && plan.note("k_band_counts"))
             launch(mk, k_band_counts, dim3(n_units), dim3(kBlock), 0, st,
                    static_cast<const int32_t *>(band_counts), nbands, cnt_all);
         return;
@@ -660,9 +663,217 @@ void shuffle_walk(const void *x, void *y, dynconv_shape s, dynconv_dtype dt, con
         void *next_in = (u + 1 < n_units) ? in_of(u + 1) : nullptr;
         if (plan.note("k_shuffle_merge")) dispatch_merge(dt, xu, bout, out_of(u), next_in, npos, cb, cp, st, mk);
     }
-    if (L.fused && !dense && (counts || !plan.exec) && plan.note("k_band_counts"))
+    if (L.fused && !dense && (counts || (!plan.exec && plan.list_counts)) && plan.note("k_band_counts"))
         launch(mk, k_band_counts, dim3(n_units), dim3(kBlock), 0, st,
                static_cast<const int32_t *>(band_counts), nbands, cnt_all);
+}
+
+// ------------------------------------------------------------ whole networks
+// A layer list (dynconv_layer) run on one stream: dense layers with the
+// kernels of dense.h, gated blocks as one-block stacks.  Activations
+// alternate between two buffers sized for the largest layer output; the
+// last layer writes y.  Dense blocks keep their expanded tensor (H1, input
+// resolution) and depthwise output (H2, output resolution) in two more
+// buffers.
+constexpr int kMaxLayers = 1024;
+
+struct LayerShapes {
+    dynconv_shape in, out;
+    int hidden;  // dense blocks: hidden width
+};
+
+dynconv_status layer_shape(const dynconv_layer &L, dynconv_shape in, LayerShapes &o, bool need_mask) {
+    o.in = in;
+    o.out = in;
+    o.hidden = 0;
+    if (L.kind == DYNCONV_LAYER_CONV3X3) {
+        if (!L.w || !L.b) return DYNCONV_ERR_NULL;
+        if (L.c_in != in.c || L.c_in < 1 || L.c_in > 16) return DYNCONV_ERR_SHAPE;
+        if (L.stride != 1 && L.stride != 2) return DYNCONV_ERR_ARG;
+        if (L.c_out < 8 || L.c_out > 256 || L.c_out % 8) return DYNCONV_ERR_UNSUPPORTED;
+        if (9 * L.c_in * L.c_out + L.c_out > 16384) return DYNCONV_ERR_UNSUPPORTED;  // fp32 weights in 64 KB of LDS
+        if (L.act < DYNCONV_ACT_NONE || L.act > DYNCONV_ACT_RELU6) return DYNCONV_ERR_ARG;
+        o.out.h = (in.h - 1) / L.stride + 1;
+        o.out.w = (in.w - 1) / L.stride + 1;
+        o.out.c = L.c_out;
+        return DYNCONV_OK;
+    }
+    if (L.kind == DYNCONV_LAYER_CONV1X1) {
+        if (!L.w || !L.b) return DYNCONV_ERR_NULL;
+        if (L.c_in != in.c) return DYNCONV_ERR_SHAPE;
+        if (L.c_in < 8 || L.c_in % 8 || L.c_out < 8 || L.c_out % 8 || L.c_out > 4096)
+            return DYNCONV_ERR_UNSUPPORTED;
+        if (L.act < DYNCONV_ACT_NONE || L.act > DYNCONV_ACT_RELU6) return DYNCONV_ERR_ARG;
+        if (!aligned16(L.w)) return DYNCONV_ERR_ALIGN;
+        o.out.c = L.c_out;
+        return DYNCONV_OK;
+    }
+    if (L.kind != DYNCONV_LAYER_BLOCK) return DYNCONV_ERR_ARG;
+    const dynconv_block &b = L.blk;
+    if (L.stride != 1 && L.stride != 2) return DYNCONV_ERR_ARG;
+    if (b.c_in != in.c) return DYNCONV_ERR_SHAPE;
+    if (L.gated) {
+        if (L.stride != 1 || b.c_out != b.c_in) return DYNCONV_ERR_UNSUPPORTED;
+        if (dynconv_status st = check_block(&b, in, need_mask)) return st;
+        if (!b.w_expand) return DYNCONV_ERR_NULL;
+        return DYNCONV_OK;
+    }
+    if (!b.w_dw || !b.b_dw || !b.w_project || !b.b_project) return DYNCONV_ERR_NULL;
+    if (b.w_expand && !b.b_expand) return DYNCONV_ERR_NULL;
+    const int E = b.w_expand ? b.c_hidden : b.c_in;
+    if (!b.w_expand && b.c_hidden != b.c_in) return DYNCONV_ERR_SHAPE;
+    if (b.c_in % 8 || b.c_out % 8 || E % 8 || b.c_in < 8 || b.c_out < 8 || E > 4096 || b.c_out > 4096)
+        return DYNCONV_ERR_UNSUPPORTED;
+    for (int a : {b.act_expand, b.act_dw, b.act_project})
+        if (a < DYNCONV_ACT_NONE || a > DYNCONV_ACT_RELU6) return DYNCONV_ERR_ARG;
+    if ((b.w_expand && !aligned16(b.w_expand)) || !aligned16(b.w_project)) return DYNCONV_ERR_ALIGN;
+    o.out.h = (in.h - 1) / L.stride + 1;
+    o.out.w = (in.w - 1) / L.stride + 1;
+    o.out.c = b.c_out;
+    o.hidden = E;
+    return DYNCONV_OK;
+}
+
+struct NetLayout {
+    size_t act0, act1, h1, h2, masks, counts, inner, total;
+    size_t act_bytes, inner_bytes;
+    int ngated;
+};
+
+dynconv_status net_plan(dynconv_shape in, const dynconv_layer *layers, int32_t n, dynconv_dtype dt,
+                        int32_t flags, bool need_mask, NetLayout *NL, dynconv_shape *out_shape,
+                        size_t *mask_total) {
+    const size_t sz = dtype_size(dt);
+    size_t act = 0, h1 = 0, h2 = 0, inner = 0, mtot = 0;
+    int ngated = 0;
+    dynconv_shape cur = in;
+    for (int32_t i = 0; i < n; ++i) {
+        LayerShapes ls;
+        if (dynconv_status st = layer_shape(layers[i], cur, ls, need_mask)) return st;
+        if (dynconv_status st = check_shape(ls.out, true)) return st;
+        const size_t npos_in = static_cast<size_t>(positions(ls.in));
+        const size_t npos_out = static_cast<size_t>(positions(ls.out));
+        act = std::max(act, npos_out * ls.out.c * sz);
+        if (layers[i].kind == DYNCONV_LAYER_BLOCK && layers[i].gated) {
+            ++ngated;
+            mtot += npos_in;
+            inner = std::max(inner, stack_layout(ls.in, &layers[i].blk, 1, dt, flags).total);
+        } else if (layers[i].kind == DYNCONV_LAYER_BLOCK) {
+            if (layers[i].blk.w_expand) h1 = std::max(h1, npos_in * ls.hidden * sz);
+            h2 = std::max(h2, npos_out * ls.hidden * sz);
+        }
+        cur = ls.out;
+    }
+    if (out_shape) *out_shape = cur;
+    if (mask_total) *mask_total = mtot;
+    if (NL) {
+        size_t off = 0;
+        NL->act_bytes = act;
+        NL->act0 = off; off += align_up(act);
+        NL->act1 = off; off += align_up(act);
+        NL->h1 = off;   off += align_up(h1);
+        NL->h2 = off;   off += align_up(h2);
+        NL->masks = off; off += align_up(mtot);
+        NL->counts = off; off += align_up(8 * static_cast<size_t>(ngated));
+        NL->inner = off; off += inner;
+        NL->inner_bytes = inner;
+        NL->total = off;
+        NL->ngated = ngated;
+    }
+    return DYNCONV_OK;
+}
+
+int elem_grid(int64_t lanes) {
+    int64_t g = (lanes + kBlock - 1) / kBlock;
+    if (g > 16384) g = 16384;
+    if (g < 1) g = 1;
+    return static_cast<int>(g);
+}
+
+template <typename T>
+void launch_conv1x1(const void *x, int64_t P, int C, const void *w, const float *b, int O, int act,
+                    const void *res, void *y, hipStream_t st, Marks &mk) {
+    const int64_t tiles = ((P + kPwTile - 1) / kPwTile) * ((O + kPwTile - 1) / kPwTile);
+    const int grid = static_cast<int>(tiles < 16384 ? tiles : 16384);
+    launch(mk, k_conv1x1<T>, dim3(grid), dim3(kBlock), 0, st, static_cast<const T *>(x), P, C,
+           static_cast<const T *>(w), b, O, act, static_cast<const T *>(res), static_cast<T *>(y));
+}
+
+template <typename T>
+void launch_dwconv(const void *x, dynconv_shape in, dynconv_shape out, int C, int stride, const void *w,
+                   const float *b, int act, void *y, hipStream_t st, Marks &mk) {
+    const size_t lds = (9 * C * sizeof(T) + 15) / 16 * 16 + 4 * C;
+    launch(mk, k_dwconv3x3<T>, dim3(elem_grid(positions(out) * (C / 8))), dim3(kBlock), lds, st,
+           static_cast<const T *>(x), in.n, in.h, in.w, C, stride, static_cast<const T *>(w), b, act,
+           static_cast<T *>(y), out.h, out.w);
+}
+
+template <typename T>
+void launch_conv3x3(const void *x, dynconv_shape in, dynconv_shape out, const dynconv_layer &L, void *y,
+                    hipStream_t st, Marks &mk) {
+    const size_t lds = 4 * (9 * L.c_in * L.c_out + L.c_out);
+    launch(mk, k_conv3x3<T>, dim3(elem_grid(positions(out) * (L.c_out / 8))), dim3(kBlock), lds, st,
+           static_cast<const T *>(x), in.n, in.h, in.w, L.c_in, L.stride, static_cast<const T *>(L.w), L.b,
+           L.c_out, L.act, static_cast<T *>(y), out.h, out.w);
+}
+
+#define DC_TYPED(dt, call)                                  \
+    do {                                                    \
+        if ((dt) == DYNCONV_F32) { typedef float T; call; }  \
+        else if ((dt) == DYNCONV_F16) { typedef half_t T; call; } \
+        else { typedef bf16_t T; call; }                    \
+    } while (0)
+
+void net_walk(const void *x, void *y, dynconv_shape in, dynconv_dtype dt, const dynconv_layer *layers,
+              int32_t n, int32_t flags, uint8_t *masks, int32_t *counts, char *base, const NetLayout &NL,
+              hipStream_t st, Marks &mk, Plan &plan) {
+    void *bufs[2] = {base + NL.act0, base + NL.act1};
+    void *h1 = base + NL.h1, *h2 = base + NL.h2;
+    char *inner = base + NL.inner;
+    dynconv_shape cur = in;
+    const void *src = x;
+    size_t moff = 0;
+    int gi = 0;
+    for (int32_t i = 0; i < n; ++i) {
+        const dynconv_layer &L = layers[i];
+        LayerShapes ls;
+        layer_shape(L, cur, ls, false);
+        void *dst = (i == n - 1) ? y : bufs[i % 2];
+        if (L.kind == DYNCONV_LAYER_CONV3X3) {
+            if (plan.note("k_conv3x3")) DC_TYPED(dt, launch_conv3x3<T>(src, ls.in, ls.out, L, dst, st, mk));
+        } else if (L.kind == DYNCONV_LAYER_CONV1X1) {
+            if (plan.note("k_conv1x1"))
+                DC_TYPED(dt, launch_conv1x1<T>(src, positions(ls.in), L.c_in, L.w, L.b, L.c_out, L.act, nullptr,
+                                               dst, st, mk));
+        } else if (L.gated) {
+            StackLayout SL = stack_layout(ls.in, &L.blk, 1, dt, flags);
+            uint8_t *mk_l = masks ? masks + moff : nullptr;
+            int32_t *ct_l = counts ? counts + 2 * gi : nullptr;
+            stack_walk(src, dst, ls.in, dt, &L.blk, 1, flags, mk_l, ct_l, inner, SL, st, mk, plan, false);
+            moff += static_cast<size_t>(positions(ls.in));
+            ++gi;
+        } else {
+            const dynconv_block &b = L.blk;
+            const void *hin = src;
+            if (b.w_expand) {
+                if (plan.note("k_conv1x1"))
+                    DC_TYPED(dt, launch_conv1x1<T>(src, positions(ls.in), b.c_in, b.w_expand, b.b_expand,
+                                                   ls.hidden, b.act_expand, nullptr, h1, st, mk));
+                hin = h1;
+            }
+            dynconv_shape hs = ls.in;
+            hs.c = ls.hidden;
+            if (plan.note("k_dwconv3x3"))
+                DC_TYPED(dt, launch_dwconv<T>(hin, hs, ls.out, ls.hidden, L.stride, b.w_dw, b.b_dw, b.act_dw, h2,
+                                              st, mk));
+            const bool resid = L.stride == 1 && b.c_in == b.c_out;
+            if (plan.note("k_conv1x1"))
+                DC_TYPED(dt, launch_conv1x1<T>(h2, positions(ls.out), ls.hidden, b.w_project, b.b_project,
+                                               b.c_out, b.act_project, resid ? src : nullptr, dst, st, mk));
+        }
+        src = dst;
+        cur = ls.out;
+    }
 }
 
 }  // namespace
@@ -899,6 +1110,95 @@ dynconv_status dynconv_shuffle_stack_forward_profiled(const void *x, void *y, dy
                                                       int32_t n_events) {
     return shuffle_common(x, y, s, dt, branches, n_units, flags, masks, counts, ws, ws_bytes, stream,
                           events, n_events, true);
+}
+
+dynconv_status dynconv_network_output_shape(dynconv_shape in, const dynconv_layer *layers, int32_t n_layers,
+                                            dynconv_shape *out) {
+    if (!layers || !out) return DYNCONV_ERR_NULL;
+    if (n_layers < 1 || n_layers > kMaxLayers) return DYNCONV_ERR_ARG;
+    if (dynconv_status st = check_shape(in, true)) return st;
+    return net_plan(in, layers, n_layers, DYNCONV_F16, 0, false, nullptr, out, nullptr);
+}
+
+size_t dynconv_network_workspace_bytes(dynconv_shape in, const dynconv_layer *layers, int32_t n_layers,
+                                       dynconv_dtype dt, int32_t flags) {
+    if (!layers || n_layers < 1 || n_layers > kMaxLayers || !dtype_ok(dt) || check_shape(in, true) != DYNCONV_OK ||
+        (flags & ~kStackFlags))
+        return 0;
+    NetLayout NL;
+    if (net_plan(in, layers, n_layers, dt, flags, false, &NL, nullptr, nullptr) != DYNCONV_OK) return 0;
+    return NL.total;
+}
+
+static dynconv_status net_common(const void *x, void *y, dynconv_shape in, dynconv_dtype dt,
+                                 const dynconv_layer *layers, int32_t n, int32_t flags, uint8_t *masks,
+                                 int32_t *counts, void *ws, size_t ws_bytes, void *stream,
+                                 void *const *events, int32_t n_events, bool profiled) {
+    if (!x || !y || !layers) return DYNCONV_ERR_NULL;
+    if (!dtype_ok(dt)) return DYNCONV_ERR_DTYPE;
+    if (n < 1 || n > kMaxLayers) return DYNCONV_ERR_ARG;
+    if (flags & ~kStackFlags) return DYNCONV_ERR_ARG;
+    if (dynconv_status st = check_shape(in, true)) return st;
+    NetLayout NL;
+    dynconv_shape out;
+    if (dynconv_status st = net_plan(in, layers, n, dt, flags, !(flags & kStackDense), &NL, &out, nullptr))
+        return st;
+    if (!aligned16(x) || !aligned16(y)) return DYNCONV_ERR_ALIGN;
+    const size_t in_bytes = static_cast<size_t>(positions(in)) * in.c * dtype_size(dt);
+    const size_t out_bytes = static_cast<size_t>(positions(out)) * out.c * dtype_size(dt);
+    if (ranges_overlap(x, in_bytes, y, out_bytes)) return DYNCONV_ERR_SHAPE;
+    if (!ws || ws_bytes < NL.total) return DYNCONV_ERR_WORKSPACE;
+    if (!aligned16(ws)) return DYNCONV_ERR_ALIGN;
+    Marks mk;
+    if (profiled) {
+        Plan count{false, nullptr, 0};
+        count.list_counts = counts != nullptr;
+        Marks none;
+        net_walk(x, y, in, dt, layers, n, flags, masks, counts, nullptr, NL, nullptr, none, count);
+        if (!events) return DYNCONV_ERR_NULL;
+        if (n_events < 2 * count.count) return DYNCONV_ERR_ARG;
+        for (int32_t i = 0; i < 2 * count.count; ++i)
+            if (!events[i]) return DYNCONV_ERR_NULL;
+        mk.ev = reinterpret_cast<hipEvent_t const *>(events);
+        mk.n = 2 * count.count;
+    }
+    (void)hipGetLastError();
+    Plan run{true, nullptr, 0};
+    net_walk(x, y, in, dt, layers, n, flags, masks, counts, static_cast<char *>(ws), NL,
+             static_cast<hipStream_t>(stream), mk, run);
+    return launch_status();
+}
+
+dynconv_status dynconv_network_forward(const void *x, void *y, dynconv_shape in, dynconv_dtype dt,
+                                       const dynconv_layer *layers, int32_t n_layers, int32_t flags,
+                                       uint8_t *masks, int32_t *counts, void *ws, size_t ws_bytes,
+                                       void *stream) {
+    return net_common(x, y, in, dt, layers, n_layers, flags, masks, counts, ws, ws_bytes, stream, nullptr, 0,
+                      false);
+}
+
+int32_t dynconv_network_launch_names(dynconv_shape in, const dynconv_layer *layers, int32_t n_layers,
+                                     dynconv_dtype dt, int32_t flags, int32_t with_counts, const char **names,
+                                     int32_t cap) {
+    if (!layers || n_layers < 1 || n_layers > kMaxLayers || !dtype_ok(dt) || check_shape(in, true) != DYNCONV_OK ||
+        (flags & ~kStackFlags))
+        return -1;
+    NetLayout NL;
+    if (net_plan(in, layers, n_layers, dt, flags, false, &NL, nullptr, nullptr) != DYNCONV_OK) return -1;
+    Plan plan{false, names, names ? cap : 0};
+    plan.list_counts = with_counts != 0;
+    Marks none;
+    net_walk(nullptr, nullptr, in, dt, layers, n_layers, flags, nullptr, nullptr, nullptr, NL, nullptr, none,
+             plan);
+    return plan.count;
+}
+
+dynconv_status dynconv_network_forward_profiled(const void *x, void *y, dynconv_shape in, dynconv_dtype dt,
+                                                const dynconv_layer *layers, int32_t n_layers, int32_t flags,
+                                                uint8_t *masks, int32_t *counts, void *ws, size_t ws_bytes,
+                                                void *stream, void *const *events, int32_t n_events) {
+    return net_common(x, y, in, dt, layers, n_layers, flags, masks, counts, ws, ws_bytes, stream, events,
+                      n_events, true);
 }
 
 }  // extern "C"

@@ -31,7 +31,9 @@ EXPORTED = (
     "dynconv_stack_workspace_bytes", "dynconv_stack_forward", "dynconv_stack_launch_names",
     "dynconv_stack_forward_profiled", "dynconv_shuffle_stack_workspace_bytes",
     "dynconv_shuffle_stack_forward", "dynconv_shuffle_stack_launch_names",
-    "dynconv_shuffle_stack_forward_profiled",
+    "dynconv_shuffle_stack_forward_profiled", "dynconv_network_output_shape",
+    "dynconv_network_workspace_bytes", "dynconv_network_forward", "dynconv_network_launch_names",
+    "dynconv_network_forward_profiled",
 )
 
 
@@ -49,6 +51,15 @@ class Block(ctypes.Structure):
         ("act_expand", ctypes.c_int32), ("act_dw", ctypes.c_int32), ("act_project", ctypes.c_int32),
         ("w_mask", ctypes.c_void_p), ("b_mask", ctypes.c_float),
     ]
+
+
+class Layer(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("stride", ctypes.c_int32), ("gated", ctypes.c_int32),
+                ("c_in", ctypes.c_int32), ("c_out", ctypes.c_int32), ("w", ctypes.c_void_p),
+                ("b", ctypes.c_void_p), ("act", ctypes.c_int32), ("blk", Block)]
+
+
+LAYER_CONV3X3, LAYER_BLOCK, LAYER_CONV1X1 = 0, 1, 2
 
 
 class Indices(ctypes.Structure):
@@ -116,6 +127,20 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
                                                            ctypes.POINTER(Block), i32, i32, vp, vp, vp,
                                                            sz, vp, ctypes.POINTER(ctypes.c_void_p), i32]
     lib.dynconv_shuffle_stack_forward_profiled.restype = ctypes.c_int
+    lib.dynconv_network_output_shape.argtypes = [Shape, ctypes.POINTER(Layer), i32, ctypes.POINTER(Shape)]
+    lib.dynconv_network_output_shape.restype = ctypes.c_int
+    lib.dynconv_network_workspace_bytes.argtypes = [Shape, ctypes.POINTER(Layer), i32, ctypes.c_int, i32]
+    lib.dynconv_network_workspace_bytes.restype = sz
+    lib.dynconv_network_forward.argtypes = [vp, vp, Shape, ctypes.c_int, ctypes.POINTER(Layer), i32, i32, vp,
+                                            vp, vp, sz, vp]
+    lib.dynconv_network_forward.restype = ctypes.c_int
+    lib.dynconv_network_launch_names.argtypes = [Shape, ctypes.POINTER(Layer), i32, ctypes.c_int, i32, i32,
+                                                 ctypes.POINTER(ctypes.c_char_p), i32]
+    lib.dynconv_network_launch_names.restype = i32
+    lib.dynconv_network_forward_profiled.argtypes = [vp, vp, Shape, ctypes.c_int, ctypes.POINTER(Layer), i32,
+                                                     i32, vp, vp, vp, sz, vp, ctypes.POINTER(ctypes.c_void_p),
+                                                     i32]
+    lib.dynconv_network_forward_profiled.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -392,4 +417,115 @@ class ShuffleStack:
         arr = (ctypes.c_void_p * len(events))(*events)
         _check(self.lib.dynconv_shuffle_stack_forward_profiled(*self._args(stream), arr, len(events)),
                "dynconv_shuffle_stack_forward_profiled")
+        return self.y
+
+
+class NetworkWeights:
+    """Device copies of a layer list (dicts as paper_1912_03203_amd.inputs
+    builds them) and the C layer array pointing at them; gated blocks get
+    their mask biases from `biases` (one per gated block, in order)."""
+
+    def __init__(self, layers, dtype, biases=None, device="cuda"):
+        self.keep = []
+        self.arr = (Layer * len(layers))()
+        gi = 0
+
+        def dev(a, dt):
+            t = torch.as_tensor(a).to(device=device, dtype=dt).contiguous()
+            self.keep.append(t)
+            return t
+
+        for i, L in enumerate(layers):
+            if L["kind"] in ("conv3x3", "conv1x1"):
+                w = dev(L["w"], dtype)
+                b = dev(L["b"], torch.float32)
+                kind = LAYER_CONV3X3 if L["kind"] == "conv3x3" else LAYER_CONV1X1
+                self.arr[i] = Layer(kind, int(L.get("stride", 1)), 0, int(w.shape[1]), int(w.shape[0]),
+                                    w.data_ptr(), b.data_ptr(), int(L["act"]), Block())
+                continue
+            acts = L.get("acts", (ACT_RELU6, ACT_RELU6, ACT_NONE))
+            w2 = dev(L["w2"], dtype).reshape(-1, 9).contiguous()
+            self.keep.append(w2)
+            b2 = dev(L["b2"], torch.float32)
+            w3 = dev(L["w3"], dtype)
+            b3 = dev(L["b3"], torch.float32)
+            E = int(w2.shape[0])
+            c_out = int(w3.shape[0])
+            if L.get("w1") is not None:
+                w1 = dev(L["w1"], dtype)
+                b1 = dev(L["b1"], torch.float32)
+                c_in, w1p, b1p = int(w1.shape[1]), w1.data_ptr(), b1.data_ptr()
+            else:
+                c_in, w1p, b1p = E, None, None
+            gated = 1 if L.get("gated") else 0
+            wm_p, bm = None, 0.0
+            if gated:
+                wm = dev(L["w_m"], torch.float32)
+                wm_p = wm.data_ptr()
+                bm = float(biases[gi]) if biases is not None else 0.0
+                gi += 1
+            blk = Block(c_in, E, c_out, w1p, b1p, w2.data_ptr(), b2.data_ptr(), w3.data_ptr(), b3.data_ptr(),
+                        int(acts[0]), int(acts[1]), int(acts[2]), wm_p, bm)
+            self.arr[i] = Layer(LAYER_BLOCK, int(L["stride"]), gated, c_in, c_out, None, None, 0, blk)
+        self.n = len(layers)
+        self.ngated = gi if biases is not None else sum(1 for L in layers if L.get("gated"))
+
+    def set_bias(self, gated_index, value):
+        gi = 0
+        for i in range(self.n):
+            if self.arr[i].gated:
+                if gi == gated_index:
+                    self.arr[i].blk.b_mask = float(value)
+                    return
+                gi += 1
+        raise IndexError(gated_index)
+
+
+def network_output_shape(shape: Shape, net: NetworkWeights) -> Shape:
+    out = Shape()
+    _check(load().dynconv_network_output_shape(shape, net.arr, net.n, ctypes.byref(out)),
+           "dynconv_network_output_shape")
+    return out
+
+
+class Network:
+    """A prepared whole-network call y = layers(x) (dynconv_network_forward).
+    x and y must not overlap; y has the shape network_output_shape gives."""
+
+    def __init__(self, x: torch.Tensor, y: torch.Tensor, net: NetworkWeights, flags=0, masks=None, counts=None,
+                 ws=None):
+        self.lib = load()
+        self.x, self.y, self.net = x, y, net
+        self.shape = shape_of(x)
+        self.dtype = dtype_code(x.dtype)
+        self.flags = int(flags)
+        need = self.lib.dynconv_network_workspace_bytes(self.shape, net.arr, net.n, self.dtype, self.flags)
+        if need == 0:
+            raise DynconvError("dynconv_network_workspace_bytes rejected the network")
+        self.ws = torch.empty(need, dtype=torch.uint8, device=x.device) if ws is None else ws
+        self.masks = masks
+        self.counts = counts
+
+    def launch_names(self):
+        args = (self.shape, self.net.arr, self.net.n, self.dtype, self.flags, 1 if self.counts is not None else 0)
+        total = self.lib.dynconv_network_launch_names(*args, None, 0)
+        if total < 0:
+            raise DynconvError("dynconv_network_launch_names rejected the network")
+        names = (ctypes.c_char_p * total)()
+        self.lib.dynconv_network_launch_names(*args, names, total)
+        return [n.decode() for n in names]
+
+    def _args(self, stream):
+        return (_ptr(self.x), _ptr(self.y), self.shape, self.dtype, self.net.arr, self.net.n, self.flags,
+                _ptr(self.masks), _ptr(self.counts), _ptr(self.ws), self.ws.numel() * self.ws.element_size(),
+                _stream(stream))
+
+    def __call__(self, stream=None):
+        _check(self.lib.dynconv_network_forward(*self._args(stream)), "dynconv_network_forward")
+        return self.y
+
+    def profiled(self, events, stream=None):
+        arr = (ctypes.c_void_p * len(events))(*events)
+        _check(self.lib.dynconv_network_forward_profiled(*self._args(stream), arr, len(events)),
+               "dynconv_network_forward_profiled")
         return self.y
