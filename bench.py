@@ -28,6 +28,8 @@ Also reported on the same JSON line:
   shufflenet    ShuffleNetV2 stride-1 units (gated branch) at 64 x 28x28x116 and
                 64 x 14x14x232, bf16, density 0.3: one unit and 3 / 7 units
   mask_variants the stack with G-Softmax mask units against G-Binary ones
+  network       a whole MobileNetV2 (64 x 224x224x3 -> 7x7x1280, fp16) with its 10
+                stride-1 residual blocks gated, densities ~ U[0.2, 0.6], and dense
   bandwidth_probes
                 the chain's mask / gather+expand / depthwise+scatter kernels and
                 the one-launch block at batches moving >= 512 MB per kernel,
@@ -146,15 +148,20 @@ class Runner:
     an inference caller runs it); read_counts() runs the same stack once more
     with the per-block counts P, P_d requested."""
 
-    def __init__(self, dc, torch, x0, blocks, flags, use_graph, n_blocks, shuffle=False):
+    def __init__(self, dc, torch, x0, blocks, flags, use_graph, n_blocks, shuffle=False, network=False):
         self.torch = torch
         self.dc = dc
         self.x0 = x0
         self.blocks = blocks
         self.flags = flags
         self.n_blocks = n_blocks
-        self.cls = dc.ShuffleStack if shuffle else dc.Stack
-        self.y = torch.empty_like(x0)
+        if network:
+            self.cls = dc.Network
+            out = dc.network_output_shape(dc.shape_of(x0), blocks)
+            self.y = torch.empty(out.n, out.h, out.w, out.c, dtype=x0.dtype, device=x0.device)
+        else:
+            self.cls = dc.ShuffleStack if shuffle else dc.Stack
+            self.y = torch.empty_like(x0)
         self.stack = self.cls(x0, self.y, blocks, flags=flags)
         # the count reduction is listed last but runs only when counts are requested
         names = self.stack.launch_names()
@@ -173,7 +180,7 @@ class Runner:
         if self.flags & self.dc.STACK_DENSE:
             return None
         counts = torch.zeros(self.n_blocks, 2, dtype=torch.int32, device=self.x0.device)
-        y = torch.empty_like(self.x0)
+        y = torch.empty_like(self.y)
         self.cls(self.x0, y, self.blocks, flags=self.flags, counts=counts)()
         torch.cuda.synchronize()
         if not torch.equal(y, self.y):
@@ -458,6 +465,72 @@ def shufflenet_report(dc, inputs, torch, steps, warmup, use_graph, profile_steps
     return rows
 
 
+def calibrate_network(dc, inputs, torch, x0, layers, dens, dt):
+    """Mask bias of every gated block of a whole network for its target
+    density, from the library's bias-free logits of the block's input, the
+    layers run one after another (offline, before timing)."""
+    cur = x0
+    biases = []
+    gi = 0
+    for L in layers:
+        one = dc.NetworkWeights([L], dt, biases=[0.0] if L.get("gated") else None)
+        if L.get("gated"):
+            n, h, w, c = cur.shape
+            logits = torch.empty(n * h * w, dtype=torch.float32, device=cur.device)
+            w_m = torch.from_numpy(np.asarray(L["w_m"], np.float32)).to(cur.device)
+            dc.mask(cur, w_m, 0.0, logits=logits)
+            torch.cuda.synchronize()
+            b = float(inputs.percentile_bias(logits.cpu().numpy(), dens[gi]))
+            biases.append(b)
+            one.set_bias(0, b)
+            gi += 1
+        out = dc.network_output_shape(dc.shape_of(cur), one)
+        nxt = torch.empty(out.n, out.h, out.w, out.c, dtype=cur.dtype, device=cur.device)
+        dc.Network(cur, nxt, one)()
+        cur = nxt
+    torch.cuda.synchronize()
+    return biases
+
+
+def network_report(dc, inputs, torch, steps, warmup, use_graph, profile_steps):
+    """Whole MobileNetV2 feature extractor (batch 64, 224x224x3 -> 7x7x1280,
+    fp16): 17 blocks, the 10 stride-1 residual blocks gated with densities
+    ~ U[0.2, 0.6], against the same network run dense."""
+    n, h, w = 64, 224, 224
+    x_np, layers, dens = inputs.make_network_inputs(0, n, h, w, dtype="f16")
+    dt = torch.float16
+    x0 = torch.from_numpy(x_np).cuda().to(dt)
+    biases = calibrate_network(dc, inputs, torch, x0, layers, dens, dt)
+    sp_net = dc.NetworkWeights(layers, dt, biases=biases)
+    dn_net = dc.NetworkWeights(layers, dt, biases=None)
+    ng = sp_net.ngated
+    sp = Runner(dc, torch, x0, sp_net, 0, use_graph, ng, network=True)
+    dn = Runner(dc, torch, x0, dn_net, dc.STACK_DENSE, use_graph, ng, network=True)
+    t_sp = sp.timed(steps, warmup)
+    t_dn = dn.timed(steps, warmup)
+    counts = sp.read_counts().cpu().numpy()
+    npos = []
+    sh = dc.shape_of(x0)
+    for L in layers:
+        one = dc.NetworkWeights([L], dt, biases=[0.0] if L.get("gated") else None)
+        if L.get("gated"):
+            npos.append(sh.n * sh.h * sh.w)
+        sh = dc.network_output_shape(sh, one)
+    prof_sp, _ = profile_kernels(dc, torch, sp, profile_steps)
+    prof_dn, _ = profile_kernels(dc, torch, dn, profile_steps)
+
+    def top(prof):
+        return {k: {"avg_us": v["avg_us"], "launches": v["launches"], "total_us": v["total_us"]}
+                for k, v in sorted(prof.items(), key=lambda kv: -kv[1]["total_us"])}
+    return {"workload": "mobilenetv2_224_b64_f16", "batch": n, "input": [h, w, 3], "output": [sh.h, sh.w, sh.c],
+            "gated_blocks": ng, "target_density": dens.tolist(),
+            "active_frac": [float(c[0]) / p for c, p in zip(counts, npos)],
+            "dilated_frac": [float(c[1]) / p for c, p in zip(counts, npos)],
+            "sparse_ms_per_step": 1e3 * t_sp, "dense_ms_per_step": 1e3 * t_dn,
+            "sparse_images_per_s": n / t_sp, "dense_images_per_s": n / t_dn, "speedup_vs_dense": t_dn / t_sp,
+            "kernels_sparse": top(prof_sp), "kernels_dense": top(prof_dn)}
+
+
 def bandwidth_probes(dc, inputs, torch, reps=5):
     """HBM-scale timing of the bandwidth-bound kernels.  At the benchmark
     shapes a kernel moves 10-70 MB, which the 256 MB Infinity Cache holds; here
@@ -653,6 +726,7 @@ def main():
     ap.add_argument("--no-chain", action="store_true", help="skip the kernel-chain report")
     ap.add_argument("--no-shufflenet", action="store_true", help="skip the ShuffleNetV2 unit report")
     ap.add_argument("--no-probes", action="store_true", help="skip the HBM-scale bandwidth probes")
+    ap.add_argument("--no-network", action="store_true", help="skip the whole-MobileNetV2 report")
     ap.add_argument("--profile-steps", type=int, default=20)
     ap.add_argument("--traffic-pass", action="store_true",
                     help="untimed launches for an HBM-counter run: a plain copy of known size, "
@@ -785,6 +859,10 @@ def main():
         log("mask variants")
         result["mask_variants"] = mask_variants(dc, torch, wl, x0, sparse_blocks, t_sp, use_graph,
                                                 min(args.steps, 100), min(args.warmup, 10), args.profile_steps)
+    if not args.no_network:
+        log("whole network")
+        result["network"] = network_report(dc, inputs, torch, min(args.steps, 30), min(args.warmup, 5), use_graph,
+                                           min(args.profile_steps, 5))
     if not args.no_probes:
         log("bandwidth probes")
         result["bandwidth_probes"] = bandwidth_probes(dc, inputs, torch)
