@@ -27,6 +27,11 @@ Also reported on the same JSON line:
                 kernels), sparse and dense, with per-kernel HBM fractions
   shufflenet    ShuffleNetV2 stride-1 units (gated branch) at 64 x 28x28x116 and
                 64 x 14x14x232, bf16, density 0.3: one unit and 3 / 7 units
+  timing_protocol
+                per-call median / p10 / p90 of the step, 200 calls per mode in
+                alternating sparse / dense groups of 20
+  cpu_baseline_parallel
+                the oracle over the batch's images on all host cores (<= 16)
   mask_variants the stack with G-Softmax mask units against G-Binary ones
   network       a whole MobileNetV2 (64 x 224x224x3 -> 7x7x1280, fp16) with its 10
                 stride-1 residual blocks gated, densities ~ U[0.2, 0.6], and dense
@@ -309,6 +314,91 @@ def cpu_baseline(inputs, wl, x0_np, blocks_np, density, budget_s=12.0):
     return {"value": S / t, "unit": "images/s", "cores": 1, "kind": "oracle",
             "sample": "%d of %d images through all %d blocks (mask, dilation, index maps, "
                       "gather/scatter block; fp64 C loops, one thread); %.1f s" % (S, wl.n, len(blocks_np), t)}
+
+
+def cpu_baseline_parallel(inputs, wl, x0_np, blocks_np, density, budget_s=8.0):
+    """The same oracle run over the images of the batch in parallel (images
+    are independent; the oracle's C loops run outside the interpreter lock),
+    one thread per host core this process may use (at most 16), the batch
+    repeated until the run takes about budget_s seconds.  Biases are
+    calibrated on the batch first (untimed)."""
+    import os
+    from concurrent.futures import ThreadPoolExecutor
+
+    import oracle
+    threads = max(1, min(16, len(os.sched_getaffinity(0))))
+    x = np.ascontiguousarray(x0_np.transpose(0, 3, 1, 2)).astype(np.float64)
+    biases = []
+    cur = x
+    for wts in blocks_np:
+        _, sl = oracle.mask(cur.astype(np.float32), wts["w_m"], 0.0)
+        b = inputs.percentile_bias(sl, density)
+        biases.append(b)
+        N, C, H, W = cur.shape
+        G, _ = oracle.mask(cur.astype(np.float32), wts["w_m"], b)
+        A, D, nbr = oracle.indices(G, oracle.dilate(G, N, H, W, 1), N, H, W)
+        y, _, _ = oracle.block_sparse(cur, wts, A, D, nbr)
+        cur = np.ascontiguousarray(inputs.round_to_storage(y.transpose(0, 2, 3, 1), wl.dtype).transpose(0, 3, 1, 2))
+
+    def one(i):
+        xi = x[i:i + 1]
+        for b, wts in enumerate(blocks_np):
+            _, _, H, W = xi.shape
+            G, _ = oracle.mask(xi.astype(np.float32), wts["w_m"], biases[b])
+            A, D, nbr = oracle.indices(G, oracle.dilate(G, 1, H, W, 1), 1, H, W)
+            y, _, _ = oracle.block_sparse(xi, wts, A, D, nbr)
+            xi = np.ascontiguousarray(inputs.round_to_storage(y.transpose(0, 2, 3, 1), wl.dtype).transpose(0, 3, 1, 2))
+        return 0
+
+    with ThreadPoolExecutor(threads) as pool:
+        t0 = time.perf_counter()
+        list(pool.map(one, range(x.shape[0])))
+        t1 = time.perf_counter() - t0
+        reps = int(max(1, round(budget_s / max(t1, 1e-3))))
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            list(pool.map(one, range(x.shape[0])))
+        t = time.perf_counter() - t0
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"value": reps * x.shape[0] / t, "unit": "images/s", "cores": threads, "kind": "oracle",
+            "cpu": model,
+            "sample": "all %d images x %d repeats through all %d blocks, one image per task on %d threads; %.1f s"
+                      % (x.shape[0], reps, len(blocks_np), threads, t)}
+
+
+def timing_protocol(torch, sp, dn, groups=10, per=20, warm=20):
+    """Per-call times of the graph-replayed step: after `warm` calls per mode,
+    alternating groups of `per` sparse and `per` dense calls (groups x per
+    per mode), each call between two events; median, p10, p90 in us."""
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(per)]
+    for _ in range(warm):
+        sp.step()
+        dn.step()
+    torch.cuda.synchronize()
+    res = {"sparse": [], "dense": []}
+    for _ in range(groups):
+        for tag, r in (("sparse", sp), ("dense", dn)):
+            for i in range(per):
+                ev[i][0].record()
+                r.step()
+                ev[i][1].record()
+            torch.cuda.synchronize()
+            res[tag] += [1e3 * ev[i][0].elapsed_time(ev[i][1]) for i in range(per)]
+    out = {"calls_per_mode": groups * per, "group": per}
+    for tag, v in res.items():
+        a = np.asarray(v)
+        out[tag] = {"median_us": float(np.median(a)), "p10_us": float(np.percentile(a, 10)),
+                    "p90_us": float(np.percentile(a, 90))}
+    out["speedup_median"] = out["dense"]["median_us"] / out["sparse"]["median_us"]
+    return out
 
 
 def chain_report(dc, torch, wl, x0, sparse_blocks, dense_blocks, counts, use_graph, steps, warmup,
@@ -851,6 +941,8 @@ def main():
     if rec is not None:
         result["roofline"]["traffic"] = rec["sparse_bytes"]
         result["roofline"]["traffic_dense"] = rec["dense_bytes"]
+    log("timing protocol")
+    result["timing_protocol"] = timing_protocol(torch, sp, dn)
     if not args.no_chain and not args.unfused:
         log("kernel chain")
         result["chain"] = chain_report(dc, torch, wl, x0, sparse_blocks, dense_blocks, counts, use_graph,
@@ -877,6 +969,8 @@ def main():
     if not args.no_cpu:
         log("cpu baseline (oracle)")
         result["cpu_baseline"] = cpu_baseline(inputs, wl, x_np, blocks_np, args.density)
+        log("cpu baseline (oracle, all host cores)")
+        result["cpu_baseline_parallel"] = cpu_baseline_parallel(inputs, wl, x_np, blocks_np, args.density)
     print(json.dumps(result), flush=True)
 
 
