@@ -178,15 +178,18 @@ template <typename T, bool DENSE, int MAXKS>
 void launch_expand_k(const void *x, dynconv_shape s, const dynconv_block *b, const int32_t *dil,
                      const int32_t *counts, void *h1, hipStream_t st, Marks &mk) {
     int64_t rows = positions(s);
-    const size_t lds = expand_lds_bytes<T>(b->c_in, b->c_hidden);
-    if (lds <= kMaxDynLds)
-        launch(mk, k_expand<T, DENSE, MAXKS, true>, dim3(grid_for_rows(rows)), dim3(kBlock), lds, st,
-               static_cast<const T *>(x), b->c_in, b->c_hidden, static_cast<const T *>(b->w_expand),
-               b->b_expand, b->act_expand, dil, counts, rows, static_cast<T *>(h1));
-    else
-        launch(mk, k_expand<T, DENSE, MAXKS, false>, dim3(grid_for_rows(rows)), dim3(kBlock), 0, st,
-               static_cast<const T *>(x), b->c_in, b->c_hidden, static_cast<const T *>(b->w_expand),
-               b->b_expand, b->act_expand, dil, counts, rows, static_cast<T *>(h1));
+    // hidden-channel slabs whose expansion weights and biases fit in LDS
+    int eslab = b->c_hidden;
+    if (expand_lds_bytes<T>(b->c_in, eslab) > kMaxDynLds) {
+        const size_t per_ch = (b->c_in + 8) * sizeof(T) + 4;
+        eslab = static_cast<int>((kMaxDynLds - 16) / per_ch) / 16 * 16;
+    }
+    const int nslabs = (b->c_hidden + eslab - 1) / eslab;
+    const int gps = grid_for_rows(rows);
+    const size_t lds = expand_lds_bytes<T>(b->c_in, eslab);
+    launch(mk, k_expand<T, DENSE, MAXKS, true>, dim3(gps * nslabs), dim3(kBlock), lds, st,
+           static_cast<const T *>(x), b->c_in, b->c_hidden, static_cast<const T *>(b->w_expand),
+           b->b_expand, b->act_expand, dil, counts, rows, static_cast<T *>(h1), eslab, gps);
 }
 
 template <typename T, bool DENSE>

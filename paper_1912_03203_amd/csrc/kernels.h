@@ -437,7 +437,8 @@ template <typename T, bool DENSE, int MAXKS, bool LDSW>
 __global__ void __launch_bounds__(kBlock)
 k_expand(const T *__restrict__ x, int C, int E, const T *__restrict__ w1,
          const float *__restrict__ b1, int act1, const int32_t *__restrict__ dil,
-         const int32_t *__restrict__ counts, int64_t dense_rows, T *__restrict__ h1) {
+         const int32_t *__restrict__ counts, int64_t dense_rows, T *__restrict__ h1, int eslab,
+         int grid_per_slab) {
     typedef mma<T> M;
     extern __shared__ __align__(16) unsigned char ex_lds[];
     // sparse: P_d from the device, clamped to the capacity N*H*W (= dense_rows)
@@ -446,7 +447,13 @@ k_expand(const T *__restrict__ x, int C, int E, const T *__restrict__ w1,
     const int r = lane % 16, g = lane / 16;
     const int64_t ntiles = (nrows + 15) / 16;
     const int nks = (C + 31) / 32;
-    const int nmt = E / 16;
+    // hidden channels e_base .. e_base + e_cnt - 1 (a slab whose expansion
+    // weights fit in LDS; workgroups are grouped by slab)
+    const int slab = blockIdx.x / grid_per_slab;
+    const int bx = blockIdx.x % grid_per_slab;
+    const int e_base = slab * eslab;
+    const int e_cnt = min(eslab, E - e_base);
+    const int nmt = e_cnt / 16;
     const float lo1 = act_lo(act1), hi1 = act_hi(act1);
     // row dense_rows (one past the capacity) stays zero: the depthwise reads it
     // for neighbours outside the image or the dilated list
@@ -455,20 +462,20 @@ k_expand(const T *__restrict__ x, int C, int E, const T *__restrict__ w1,
     // XCD-aware order: workgroup i runs on XCD i % 8; each XCD walks its own
     // contiguous range of tiles (gridDim.x is a multiple of 8)
     const int64_t per_xcd = (ntiles + 7) / 8;
-    const int64_t xcd = blockIdx.x % 8, slot = blockIdx.x / 8, nslot = gridDim.x / 8;
+    const int64_t xcd = bx % 8, slot = bx / 8, nslot = grid_per_slab / 8;
     if (slot * kWavesPerBlock >= per_xcd) return;  // uniform per workgroup
     const int cs = C + 8;  // LDS row stride of the weights
     T *w1s = reinterpret_cast<T *>(ex_lds);
-    float *b1s = reinterpret_cast<float *>(ex_lds + ((static_cast<size_t>(E) * cs * sizeof(T) + 15) & ~size_t(15)));
+    float *b1s = reinterpret_cast<float *>(ex_lds + ((static_cast<size_t>(e_cnt) * cs * sizeof(T) + 15) & ~size_t(15)));
     if (LDSW) {
         constexpr int per16 = 16 / static_cast<int>(sizeof(T));
         const int vpr = C / per16;
-        for (int i = threadIdx.x; i < E * vpr; i += kBlock) {
+        for (int i = threadIdx.x; i < e_cnt * vpr; i += kBlock) {
             const int e = i / vpr, k = i % vpr;
             *reinterpret_cast<uint4 *>(w1s + e * cs + k * per16) =
-                *reinterpret_cast<const uint4 *>(w1 + static_cast<int64_t>(e) * C + k * per16);
+                *reinterpret_cast<const uint4 *>(w1 + static_cast<int64_t>(e_base + e) * C + k * per16);
         }
-        for (int e = threadIdx.x; e < E; e += kBlock) b1s[e] = b1[e];
+        for (int e = threadIdx.x; e < e_cnt; e += kBlock) b1s[e] = b1[e_base + e];
         __syncthreads();
     }
     const int64_t stride = nslot * kWavesPerBlock;  // in tiles of this XCD's range
@@ -492,11 +499,13 @@ k_expand(const T *__restrict__ x, int C, int E, const T *__restrict__ w1,
         const int64_t j = t * 16 + r;
         const bool valid = j < nrows;
         for (int mt = 0; mt < nmt; ++mt) {
-            const int e = mt * 16 + r;
-            const int e0 = mt * 16 + 4 * g;
+            const int el = mt * 16 + r;           // slab-local A row
+            const int e = e_base + el;
+            const int e0l = mt * 16 + 4 * g;      // slab-local output channel
+            const int e0 = e_base + e0l;
             floatx4 acc;  // bias first
             if (LDSW) {
-                acc = *reinterpret_cast<const floatx4 *>(b1s + e0);
+                acc = *reinterpret_cast<const floatx4 *>(b1s + e0l);
             } else {
                 acc = floatx4{b1[e0], b1[e0 + 1], b1[e0 + 2], b1[e0 + 3]};
             }
@@ -508,7 +517,7 @@ k_expand(const T *__restrict__ x, int C, int E, const T *__restrict__ w1,
                 const int c0 = ks * 32 + g * 8;
                 typename M::frag a;
                 if (LDSW)
-                    a = (ks < nks && c0 < C) ? M::load(w1s + e * cs + c0) : M::zero();
+                    a = (ks < nks && c0 < C) ? M::load(w1s + el * cs + c0) : M::zero();
                 else
                     a = (ks < nks && c0 < C) ? M::load(w1 + static_cast<int64_t>(e) * C + c0) : M::zero();
                 acc = M::run(a, b[ks], acc);
