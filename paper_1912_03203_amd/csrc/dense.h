@@ -129,17 +129,21 @@ k_dwconv3x3(const T *__restrict__ x, int N, int H, int W, int C, int stride, con
 
 // ------------------------------------------------------------ full 3x3
 // One lane per (output position, 8 output channels); weights [O][Ci][3][3]
-// and biases staged in LDS as fp32 (dynamic shared memory: 9*Ci*O + O
-// floats).  Ci is small (the stem's 3 input channels); input rows are read
-// element by element.
+// and biases staged in LDS as fp32, the weights reordered to [k][ci][o] so a
+// lane's 8 outputs of one tap and input channel are two 16-byte reads
+// (dynamic shared memory: 9*Ci*O + O floats).  Ci is small (the stem's 3
+// input channels); input rows are read element by element.
 template <typename T>
 __global__ void __launch_bounds__(kBlock)
 k_conv3x3(const T *__restrict__ x, int N, int H, int W, int Ci, int stride, const T *__restrict__ w,
           const float *__restrict__ b, int O, int act, T *__restrict__ y, int Ho, int Wo) {
     extern __shared__ __align__(16) unsigned char cv_smem[];
-    float *ws = reinterpret_cast<float *>(cv_smem);  // [O][Ci*9]
+    float *ws = reinterpret_cast<float *>(cv_smem);  // [9][Ci][O]
     float *bs = ws + 9 * Ci * O;
-    for (int i = threadIdx.x; i < 9 * Ci * O; i += kBlock) ws[i] = static_cast<float>(w[i]);
+    for (int i = threadIdx.x; i < 9 * Ci * O; i += kBlock) {
+        const int o = i / (9 * Ci), c = (i / 9) % Ci, k = i % 9;  // w[o][c][k]
+        ws[(k * Ci + c) * O + o] = static_cast<float>(w[i]);
+    }
     for (int o = threadIdx.x; o < O; o += kBlock) bs[o] = b[o];
     __syncthreads();
     const float lo = act_lo(act), hi = act_hi(act);
@@ -161,8 +165,11 @@ k_conv3x3(const T *__restrict__ x, int N, int H, int W, int Ci, int stride, cons
             const T *px = x + ((static_cast<int64_t>(n) * H + hh) * W + ww) * Ci;
             for (int c = 0; c < Ci; ++c) {
                 const float v = static_cast<float>(px[c]);
+                const float4 wa = *reinterpret_cast<const float4 *>(ws + (k * Ci + c) * O + o0);
+                const float4 wb = *reinterpret_cast<const float4 *>(ws + (k * Ci + c) * O + o0 + 4);
+                const float wk[8] = {wa.x, wa.y, wa.z, wa.w, wb.x, wb.y, wb.z, wb.w};
 #pragma unroll
-                for (int u = 0; u < 8; ++u) s[u] = __builtin_fmaf(ws[(o0 + u) * 9 * Ci + c * 9 + k], v, s[u]);
+                for (int u = 0; u < 8; ++u) s[u] = __builtin_fmaf(wk[u], v, s[u]);
             }
         }
         float o[8];
