@@ -887,7 +887,7 @@ def main():
     rows = wl.n * wl.h
     # patches of the one-launch block: column strips of at most 32, R rows,
     # at most `own` positions and `region` ring-included slots
-    own, region = (256, 340) if wl.c <= 32 else (128, 208)
+    own, region = (256, 340) if wl.c <= 32 else (128, 208) if wl.c <= 64 else (64, 108)
     strips = -(-wl.w // 32)
     wu = -(-wl.w // strips)
     pr = max(1, min(own // wu, region // (wu + 2) - 2, 50, wl.h))

@@ -266,7 +266,8 @@ PatchGeom fused_geom_t(dynconv_shape s) {
 
 PatchGeom fused_geom(dynconv_shape s, dynconv_dtype dt) {
     if (dt == DYNCONV_F32) return s.c <= 32 ? fused_geom_t<float, 32>(s) : fused_geom_t<float, 64>(s);
-    return s.c <= 32 ? fused_geom_t<half_t, 32>(s) : fused_geom_t<half_t, 64>(s);
+    if (s.c <= 32) return fused_geom_t<half_t, 32>(s);
+    return s.c <= 64 ? fused_geom_t<half_t, 64>(s) : fused_geom_t<half_t, 128>(s);
 }
 
 int fused_patch_count(dynconv_shape s, dynconv_dtype dt) {
@@ -314,8 +315,10 @@ void launch_fused(const void *src, void *dst, dynconv_shape s, const dynconv_blo
                   const dynconv_block *next, const FusedMasks &fm, hipStream_t st, Marks &mk) {
     if (s.c <= 32)
         launch_fused_k<T, DENSE, 1, 2, 32>(src, dst, s, b, next, fm, st, mk);
-    else
+    else if (s.c <= 64)
         launch_fused_k<T, DENSE, 2, 4, 64>(src, dst, s, b, next, fm, st, mk);
+    else if constexpr (sizeof(T) == 2)  // 16-bit only (use_fused keeps fp32 at 64)
+        launch_fused_k<T, DENSE, 4, 8, 128>(src, dst, s, b, next, fm, st, mk);
 }
 
 void dispatch_fused(dynconv_dtype dt, bool dense, const void *src, void *dst, dynconv_shape s,
@@ -347,10 +350,10 @@ constexpr int32_t kStackFlags = kStackDense | kStackUnfused | kStackGSoftmax;
 
 int mask_mode_of(int32_t flags) { return (flags & kStackGSoftmax) ? 1 : 0; }
 
-// The one-launch block kernel covers up to 64 channels; wider blocks run the
-// unfused kernel chain.
-bool use_fused(dynconv_shape s, dynconv_dtype, int32_t flags) {
-    return !(flags & kStackUnfused) && s.c <= kMaxFusedC;
+// The one-launch block kernel covers up to 64 channels in fp32 and 128 in
+// fp16/bf16; wider blocks run the unfused kernel chain.
+bool use_fused(dynconv_shape s, dynconv_dtype dt, int32_t flags) {
+    return !(flags & kStackUnfused) && s.c <= (dt == DYNCONV_F32 ? kMaxFusedC : kMaxFusedC16);
 }
 
 struct StackLayout {

@@ -46,7 +46,8 @@ namespace dynconv {
 
 constexpr int kChunk = 32;                  // hidden channels per slice
 constexpr int kChunkPad = kChunk + 8;       // padded LDS row of a slice
-constexpr int kMaxFusedC = 64;
+constexpr int kMaxFusedC = 64;    // fp32
+constexpr int kMaxFusedC16 = 128; // fp16 / bf16
 constexpr int kPatchMaxCols = 32;           // Wu
 constexpr int kPatchMaxRows = 50;           // R
 
@@ -63,12 +64,15 @@ struct PatchCfg {
 //   16-bit, C <= 64: 4 x 32 patches, 4 waves, two workgroups per CU
 //   fp32,   C <= 32: 8 x 32 patches, 8 waves, one workgroup per CU
 //   fp32,   C <= 64: 4 x 32 patches, 4 waves, one workgroup per CU
+//   16-bit, C <= 128: 64-position patches, 4 waves, two workgroups per CU
 template <typename T, int MAXC> struct PatchCfgOf;
 template <int MAXC> struct PatchCfgOf<float, MAXC> {
     typedef typename std::conditional<MAXC <= 32, PatchCfg<256, 340, 8, 2>, PatchCfg<128, 208, 4, 1>>::type type;
 };
 template <int MAXC> struct PatchCfgOf<half_t, MAXC> {
-    typedef typename std::conditional<MAXC <= 32, PatchCfg<256, 340, 8, 4>, PatchCfg<128, 208, 4, 2>>::type type;
+    typedef typename std::conditional<
+        MAXC <= 32, PatchCfg<256, 340, 8, 4>,
+        typename std::conditional<MAXC <= 64, PatchCfg<128, 208, 4, 2>, PatchCfg<64, 108, 4, 2>>::type>::type type;
 };
 template <int MAXC> struct PatchCfgOf<bf16_t, MAXC> : PatchCfgOf<half_t, MAXC> {};
 

@@ -141,11 +141,17 @@ def test_stack_validation(lib):
     need = lib.dynconv_stack_workspace_bytes(s, blocks, 3, 1, 2)
     assert need == (npos + 4 * npos + 4 * npos + 36 * npos + up(8 * 3) + up(8 * rows)
                     + up(8 * (rows + 1)) + up(8 * rows) + up((npos + 1) * 192 * 2))
-    # more than 64 channels always take the kernel chain
-    wide_c = dc.Shape(1, 4, 100, 72)
-    blocks72 = (dc.Block * 1)(fake_block(C=72))
-    assert lib.dynconv_stack_workspace_bytes(wide_c, blocks72, 1, 1, 0) == \
-        lib.dynconv_stack_workspace_bytes(wide_c, blocks72, 1, 1, 2)
+    # more than 64 channels in fp32, more than 128 in 16-bit, take the kernel chain
+    for dt, c in ((0, 72), (1, 136)):
+        wide_c = dc.Shape(1, 4, 100, c)
+        blk = (dc.Block * 1)(fake_block(C=c))
+        assert lib.dynconv_stack_workspace_bytes(wide_c, blk, 1, dt, 0) == \
+            lib.dynconv_stack_workspace_bytes(wide_c, blk, 1, dt, 2)
+    # 16-bit up to 128 channels stays on the one-launch path (64-position patches)
+    c96 = dc.Shape(2, 14, 14, 96)
+    blk96 = (dc.Block * 1)(fake_block(C=96, E=576))
+    assert lib.dynconv_stack_workspace_bytes(c96, blk96, 1, 1, 0) != \
+        lib.dynconv_stack_workspace_bytes(c96, blk96, 1, 1, 2)
     # wide images stay on the one-launch path: patches of 4 rows x 25 columns
     wide = dc.Shape(1, 4, 100, 32)
     assert lib.dynconv_stack_workspace_bytes(wide, blocks, 3, 1, 0) == \
@@ -187,10 +193,10 @@ def test_stack_launch_plans(lib):
                            "k_dw_project"] * 8
     assert names(3, 0) == ["k_copy16"] + ["k_expand", "k_dw_project"] * 8
     assert names(0, 1, shape=dc.Shape(2, 8, 300, 32), n=2) == ["k_block_fused"] * 2 + ["k_band_counts"]
-    arr72 = (dc.Block * 2)(*([fake_block(C=72)] * 2))
-    total = lib.dynconv_stack_launch_names(dc.Shape(2, 8, 8, 72), arr72, 2, 1, 0, 1, None, 0)
+    arr136 = (dc.Block * 2)(*([fake_block(C=136)] * 2))
+    total = lib.dynconv_stack_launch_names(dc.Shape(2, 8, 8, 136), arr136, 2, 1, 0, 1, None, 0)
     out = (ctypes.c_char_p * total)()
-    lib.dynconv_stack_launch_names(dc.Shape(2, 8, 8, 72), arr72, 2, 1, 0, 1, out, total)
+    lib.dynconv_stack_launch_names(dc.Shape(2, 8, 8, 136), arr136, 2, 1, 0, 1, out, total)
     assert [x.decode() for x in out][:7] == [
         "k_mask", "k_rowcount", "k_rowscan", "k_compact", "k_expand", "k_dw_project", "k_mask"]
     assert lib.dynconv_stack_launch_names(s, arr, 0, 1, 0, 0, None, 0) == -1
@@ -246,8 +252,12 @@ def test_shuffle_stack_validation_and_plans(lib):
         "k_band_counts"]
     assert names(2, n=1) == ["k_shuffle_split", "k_mask", "k_rowcount", "k_rowscan", "k_compact",
                              "k_expand", "k_dw_project", "k_shuffle_merge"]
+    # 116-channel halves run as 120-channel branches on the one-launch path (16-bit)
     wide = (dc.Block * 2)(*([fake_block(C=120, E=128, acts=(1, 0, 1))] * 2))
-    assert names(1, n=2, shape=dc.Shape(2, 14, 14, 232), arr=wide) == [
+    assert names(1, n=2, shape=dc.Shape(2, 14, 14, 232), arr=wide) == ["k_block_fused"] * 2
+    # 140-channel halves (144-channel branches) take compact rows and the kernel chain
+    wider = (dc.Block * 2)(*([fake_block(C=144, E=144, acts=(1, 0, 1))] * 2))
+    assert names(1, n=2, shape=dc.Shape(2, 14, 14, 280), arr=wider) == [
         "k_shuffle_split", "k_expand", "k_dw_project", "k_shuffle_merge", "k_expand", "k_dw_project",
         "k_shuffle_merge"]
     assert lib.dynconv_shuffle_stack_launch_names(s, br, 0, 2, 0, None, 0) == -1

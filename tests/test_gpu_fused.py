@@ -56,6 +56,10 @@ FUSED_CASES = [
     ("wide_w130_bf16", "bf16", (1, 7, 130, 24, 48), 0.5, 10),
     ("fp32_c48", "f32", (2, 10, 20, 48, 96), 0.4, 11),
     ("fp32_c64_w33", "f32", (1, 6, 33, 64, 64), 0.6, 12),
+    ("c96_e576_f16", "f16", (4, 14, 14, 96, 576), 0.4, 13),   # 16-bit, 65-128 channels
+    ("c128_bf16_w40", "bf16", (2, 10, 40, 128, 256), 0.3, 14),
+    ("c72_f16_h1", "f16", (3, 1, 30, 72, 144), 0.5, 15),
+    ("c120_bf16_w1", "bf16", (2, 70, 1, 120, 128), 0.4, 16),
 ]
 
 
@@ -95,7 +99,9 @@ def test_fused_empty_and_full_masks(bias):
                                             ("bf16", (4, 20, 28, 48, 96), 3),
                                             ("f32", (2, 16, 16, 16, 96), 2),
                                             ("f16", (2, 12, 90, 64, 128), 2),
-                                            ("f32", (1, 9, 40, 40, 80), 3)])
+                                            ("f32", (1, 9, 40, 40, 80), 3),
+                                            ("f16", (4, 14, 14, 96, 576), 2),
+                                            ("bf16", (2, 9, 33, 120, 128), 2)])
 def test_fused_stack_matches_kernel_chain(dtype, shape, nb):
     """One-launch blocks (out of place and in place, which takes the extra copy
     for an odd block count) and the multi-kernel chain give the same masks,

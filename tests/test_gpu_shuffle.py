@@ -122,7 +122,9 @@ def test_shuffle_dense_flag_and_degenerate_masks(shape):
 
 @pytest.mark.parametrize("dtype,shape,nu", [("bf16", (8, 28, 28, 116, 58), 3),
                                             ("bf16", (4, 14, 14, 232, 116), 3),
-                                            ("f16", (2, 12, 20, 48, 32), 2)])
+                                            ("f16", (2, 12, 20, 48, 32), 2),
+                                            ("bf16", (2, 9, 14, 280, 64), 2),
+                                            ("f32", (2, 7, 9, 116, 58), 2)])
 def test_shuffle_stack_matches_unit_calls(dtype, shape, nu):
     """A stack of units equals the same units called one at a time (each fed
     the previous call's output), and the one-launch branch equals the kernel
@@ -135,7 +137,12 @@ def test_shuffle_stack_matches_unit_calls(dtype, shape, nu):
     b0 = float(inputs.percentile_bias(s, 0.3))
     biases = [b0] * nu
     stack = run_units(x, ws, biases, dtype)
-    if C // 2 <= 64:  # one launch per unit, reading and writing the unit's rows
+    # one launch per unit, reading and writing the unit's rows, when the
+    # branch (its width rounded up to 8) fits the one-launch block and a half
+    # row is a whole number of 4-byte words
+    limit = 64 if dtype == "f32" else 128
+    elt = 4 if dtype == "f32" else 2
+    if -(-(C // 2) // 8) * 8 <= limit and (C // 2) * elt % 4 == 0:
         assert stack["names"][:nu] == ["k_block_fused"] * nu
     else:             # compact branch rows and the kernel chain
         assert stack["names"][0] == "k_shuffle_split" and stack["names"].count("k_shuffle_merge") == nu
