@@ -205,27 +205,43 @@ void launch_expand(const void *x, dynconv_shape s, const dynconv_block *b, const
 template <typename T, bool DENSE, int MAXMT>
 void launch_dw_project_k(const void *h1, const void *x, void *y, dynconv_shape s,
                          const dynconv_block *b, const int32_t *act, const int32_t *nbr,
-                         const int32_t *counts, hipStream_t st, Marks &mk) {
+                         const int32_t *counts, int nos, hipStream_t st, Marks &mk) {
     int64_t rows = positions(s);
     const int64_t groups = (rows + 16 * kDwGroup - 1) / (16 * kDwGroup);
     const int64_t g = groups < kMaxDwGrid ? (groups < 1 ? 1 : groups) : kMaxDwGrid;
-    const int grid = static_cast<int>((g + 7) / 8 * 8);  // whole groups of 8 (one per XCD)
+    // whole groups of 8 (one per XCD), each slot with all its output slabs
+    const int grid = static_cast<int>((g + 7) / 8 * 8 * nos);
     launch(mk, k_dw_project<T, DENSE, MAXMT>, dim3(grid), dim3(kBlock), dw_lds_bytes<T>(),
                        st, static_cast<const T *>(h1), static_cast<const T *>(x), static_cast<T *>(y),
                        s.n, s.h, s.w, s.c, b->c_hidden, static_cast<const T *>(b->w_dw), b->b_dw,
                        b->act_dw, static_cast<const T *>(b->w_project), b->b_project, b->act_project,
-                       act, nbr, counts);
+                       act, nbr, counts, nos);
 }
+
+// Output slabs of the depthwise-projection: when the capacity has fewer than
+// kDwTargetItems groups, the output tiles are cut into slabs of 2, 4 or 8
+// tiles so that groups x slabs reaches that many work items (or one slab per
+// tile pair).
+constexpr int64_t kDwTargetItems = 512;
 
 template <typename T, bool DENSE>
 void launch_dw_project(const void *h1, const void *x, void *y, dynconv_shape s,
                        const dynconv_block *b, const int32_t *act, const int32_t *nbr,
                        const int32_t *counts, hipStream_t st, Marks &mk) {
-    int mt = (b->c_out + 15) / 16;
-    if (mt <= 2) launch_dw_project_k<T, DENSE, 2>(h1, x, y, s, b, act, nbr, counts, st, mk);
-    else if (mt <= 4) launch_dw_project_k<T, DENSE, 4>(h1, x, y, s, b, act, nbr, counts, st, mk);
-    else if (mt <= 8) launch_dw_project_k<T, DENSE, 8>(h1, x, y, s, b, act, nbr, counts, st, mk);
-    else launch_dw_project_k<T, DENSE, 16>(h1, x, y, s, b, act, nbr, counts, st, mk);
+    const int nmt = (b->c_out + 15) / 16;
+    const int64_t groups = (positions(s) + 16 * kDwGroup - 1) / (16 * kDwGroup);
+    int want = 1;
+    if (groups < kDwTargetItems) {
+        const int64_t w = (kDwTargetItems + groups - 1) / (groups < 1 ? 1 : groups);
+        want = static_cast<int>(w < nmt ? w : nmt);
+    }
+    const int per = (nmt + want - 1) / want;  // tiles per slab before rounding to an instantiation
+    const int tiles = per <= 2 ? 2 : per <= 4 ? 4 : per <= 8 ? 8 : 16;
+    const int nos = (nmt + tiles - 1) / tiles;
+    if (tiles == 2) launch_dw_project_k<T, DENSE, 2>(h1, x, y, s, b, act, nbr, counts, nos, st, mk);
+    else if (tiles == 4) launch_dw_project_k<T, DENSE, 4>(h1, x, y, s, b, act, nbr, counts, nos, st, mk);
+    else if (tiles == 8) launch_dw_project_k<T, DENSE, 8>(h1, x, y, s, b, act, nbr, counts, nos, st, mk);
+    else launch_dw_project_k<T, DENSE, 16>(h1, x, y, s, b, act, nbr, counts, nos, st, mk);
 }
 
 template <typename T>

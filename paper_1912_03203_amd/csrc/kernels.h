@@ -548,6 +548,11 @@ k_expand(const T *__restrict__ x, int C, int E, const T *__restrict__ w1,
 // starting from the projection bias, and the epilogue adds the identity path
 // and writes y at the active position (in place when y == x).  Hidden slices
 // pass through LDS in chunks of kDwChunk.
+// The output channels are cut into nos slabs of MAXMT 16-row tiles; a work
+// item is (group, slab).  Every slab of a group recomputes the group's
+// depthwise (identical values) and projects onto its own output rows, so
+// small images with many channels (7x7x160, 960 hidden) still spread over
+// the chip; each output keeps one accumulator chain, in the same order.
 constexpr int kDwGroup = 2;
 constexpr int kDwChunk = 8;
 
@@ -567,7 +572,7 @@ k_dw_project(const T *__restrict__ h1, const T *x, T *y, int N, int H, int W, in
              const T *__restrict__ w2, const float *__restrict__ b2, int act2,
              const T *__restrict__ w3, const float *__restrict__ b3, int act3,
              const int32_t *__restrict__ act_list, const int32_t *__restrict__ nbr,
-             const int32_t *__restrict__ counts) {
+             const int32_t *__restrict__ counts, int nos) {
     typedef mma<T> M;
     typedef typename M::frag Frag;
     extern __shared__ __align__(16) unsigned char dw_lds[];
@@ -577,7 +582,10 @@ k_dw_project(const T *__restrict__ h1, const T *x, T *y, int N, int H, int W, in
     const int64_t nrows = DENSE ? npos : min(max(static_cast<int64_t>(counts[0]), int64_t{0}), npos);
     constexpr int GR = kDwGroup * 16;  // rows per group
     const int64_t ngroups = (nrows + GR - 1) / GR;
-    if ((blockIdx.x / 8) >= (ngroups + 7) / 8) return;  // no group on this slot (uniform)
+    // workgroup b: XCD b % 8, output slab (b / 8) % nos, group slot (b / 8) / nos
+    const int os = static_cast<int>((blockIdx.x / 8) % nos);
+    const int mt0 = os * MAXMT;  // first output tile of the slab
+    if ((blockIdx.x / 8) / nos >= (ngroups + 7) / 8) return;  // no group on this slot (uniform)
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int r = lane % 16, g = lane / 16;
     const int nsl = (E + 31) / 32;
@@ -608,9 +616,10 @@ k_dw_project(const T *__restrict__ h1, const T *x, T *y, int N, int H, int W, in
     // XCD-aware order: workgroup i runs on XCD i % 8; each XCD walks its own
     // contiguous range of groups, so the rows a group's taps read (the
     // previous and next image rows) were just expanded or read on that XCD
-    // and sit in its L2.  gridDim.x is a multiple of 8.
+    // and sit in its L2; the slabs of a group run on the same XCD.
+    // gridDim.x is a multiple of 8 * nos.
     const int64_t per_xcd = (ngroups + 7) / 8;
-    const int64_t xcd = blockIdx.x % 8, slot = blockIdx.x / 8, nslot = gridDim.x / 8;
+    const int64_t xcd = blockIdx.x % 8, slot = (blockIdx.x / 8) / nos, nslot = gridDim.x / 8 / nos;
     for (int64_t k = slot; k < per_xcd; k += nslot) {
         const int64_t grp = xcd * per_xcd + k;
         if (grp >= ngroups) break;  // uniform per workgroup
@@ -646,9 +655,9 @@ k_dw_project(const T *__restrict__ h1, const T *x, T *y, int N, int H, int W, in
         floatx4 acc[MAXMT];  // projection bias first
 #pragma unroll
         for (int mt = 0; mt < MAXMT; ++mt) {
-            const int c0 = mt * 16 + 4 * g;
+            const int c0 = (mt0 + mt) * 16 + 4 * g;
 #pragma unroll
-            for (int v = 0; v < 4; ++v) acc[mt][v] = (mt < nmt && c0 < C) ? b3[c0 + v] : 0.0f;
+            for (int v = 0; v < 4; ++v) acc[mt][v] = (mt0 + mt < nmt && c0 < C) ? b3[c0 + v] : 0.0f;
         }
         for (int s0 = 0; s0 < nsl; s0 += kDwChunk) {
             const int ns = min(kDwChunk, nsl - s0);
@@ -691,9 +700,10 @@ k_dw_project(const T *__restrict__ h1, const T *x, T *y, int N, int H, int W, in
                 const int e0 = (s0 + sl) * 32 + g * 8;
 #pragma unroll
                 for (int mt = 0; mt < MAXMT; ++mt) {  // unconditional MFMAs, as in k_expand
-                    const int c = mt * 16 + r;
-                    const Frag a = (mt < nmt && e0 < E && c < C) ? M::load(w3 + static_cast<int64_t>(c) * E + e0)
-                                                                  : M::zero();
+                    const int c = (mt0 + mt) * 16 + r;
+                    const Frag a = (mt0 + mt < nmt && e0 < E && c < C)
+                                       ? M::load(w3 + static_cast<int64_t>(c) * E + e0)
+                                       : M::zero();
                     acc[mt] = M::run(a, bf, acc[mt]);
                 }
             }
@@ -703,8 +713,8 @@ k_dw_project(const T *__restrict__ h1, const T *x, T *y, int N, int H, int W, in
         if (wave < gt && pix >= 0) {
 #pragma unroll
             for (int mt = 0; mt < MAXMT; ++mt) {
-                const int c0 = mt * 16 + 4 * g;
-                if (mt < nmt && c0 < C) {
+                const int c0 = (mt0 + mt) * 16 + 4 * g;
+                if (mt0 + mt < nmt && c0 < C) {
                     float xv[4], o[4];
                     io<T>::load4(x + pix * C + c0, xv);
 #pragma unroll

@@ -169,6 +169,9 @@ BLOCK_CASES = [
     ("ragged_f32", "f32", (2, 9, 5, 8, 16), 0.6, 6),
     ("max_channels_f16", "f16", (1, 6, 7, 256, 1536), 0.5, 7),
     ("wide_hidden_bf16", "bf16", (2, 14, 14, 160, 960), 0.3, 8),
+    # MobileNetV2's last gated blocks at batch 64: 98 groups, 5 output slabs
+    ("mbv2_7x7x160_b64_f16", "f16", (64, 7, 7, 160, 960), 0.4, 9),
+    ("slabs_f32_c96", "f32", (4, 9, 11, 96, 192), 0.5, 10),
 ]
 
 
