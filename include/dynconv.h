@@ -348,7 +348,8 @@ typedef enum {
  *            y[o][i][j] = act(sum w[o][c][kh][kw] x[c][s*i+kh-1][s*j+kw-1] + b[o]),
  *            output (H-1)/stride+1 x (W-1)/stride+1; 1 <= c_in <= 16,
  *            c_out a multiple of 8, 9*c_in*c_out + c_out <= 16384
- *   CONV1X1  w [c_out][c_in], b [c_out], act; c_in, c_out multiples of 8
+ *   CONV1X1  w [c_out][c_in], b [c_out], act; c_in, c_out multiples of 8,
+ *            c_out <= 4096
  *   BLOCK    blk: expansion 1x1 (w_expand NULL for an expansion factor of 1,
  *            then c_hidden = c_in), depthwise 3x3 with `stride`, projection
  *            1x1, each with its activation; the block adds its input when
@@ -356,7 +357,9 @@ typedef enum {
  *            gated = 1 (stride 1, c_in == c_out, w_expand present): the gated
  *            block of Eq. 3 with blk's mask unit, executed as
  *            dynconv_stack_forward executes one block (constraints of
- *            dynconv_block apply); gated = 0: every position.
+ *            dynconv_block apply); gated = 0: every position, channel
+ *            counts multiples of 8, c_hidden <= 1792 (the depthwise weights
+ *            are staged in 64 KB of LDS), c_out <= 4096.
  * c_in/c_out of BLOCK layers are blk.c_in/blk.c_out; the layer's own c_in,
  * c_out, w, b, act are for the convolutions.
  */

@@ -17,51 +17,87 @@
 namespace dynconv {
 
 // ------------------------------------------------------------ pointwise
-// Workgroup tile: 64 positions x 64 outputs, 4 waves; wave w owns positions
-// 16w .. 16w+15 of the tile and all 64 outputs (4 MFMA row tiles).  Outputs
-// run along M (rows of w), positions along N, so lane (r, g) loads 8
-// consecutive channels of one position (B) and of one output row (A) with a
-// 16-byte load; the contraction steps through c in 32s, zero past C.
-// Every MFMA is issued unconditionally (zero fragments out of range).
-constexpr int kPwTile = 64;
+// A work item is a tile of 64 positions (16 per wave) and a range of OT
+// 16-row output tiles.  Outputs run along M (rows of w), positions along N:
+// lane (r, g) supplies 8 consecutive channels of position r (B) and of output
+// row r (A).  The contraction runs in chunks of KB 32-channel steps: the
+// wave issues the chunk's KB x loads at once, the workgroup stages the
+// chunk's weights for its output range in LDS (rows padded by 8 elements),
+// then every wave runs KB x OT matrix-core steps from there.  With one chunk
+// (C <= 32 KB) the weights are staged once per workgroup: a workgroup keeps
+// its output range and walks position tiles, requesting the next tile's x
+// before it contracts the current one.  The accumulation starts from
+// the bias and takes c in ascending steps of 32, zero past C.  Every MFMA is
+// issued unconditionally (zero fragments out of range).
+// Workgroup b runs on XCD b % 8 and takes output range (b / 8) % nor; the
+// nor workgroups of one position tile run on the same XCD, so its x rows
+// are read from HBM once.
+constexpr int kPwPos = 64;
 
-template <typename T>
+template <typename T, int OT, int KB>
+__host__ __device__ constexpr size_t pw_lds_bytes() {
+    return static_cast<size_t>(OT) * 16 * (KB * 32 + 8) * sizeof(T);
+}
+
+template <typename T, int OT, int KB>
 __global__ void __launch_bounds__(kBlock)
 k_conv1x1(const T *__restrict__ x, int64_t P, int C, const T *__restrict__ w, const float *__restrict__ b,
-          int O, int act, const T *__restrict__ res, T *__restrict__ y) {
+          int O, int act, const T *__restrict__ res, T *__restrict__ y, int nor) {
     typedef mma<T> M;
+    typedef typename M::frag Frag;
+    constexpr int ROWS = OT * 16;
+    constexpr int LD = KB * 32 + 8;  // LDS row pitch in elements
+    constexpr int PIECES = KB * 4;   // 8-element pieces per staged row
+    extern __shared__ __align__(16) unsigned char pw_lds[];
+    T *ws = reinterpret_cast<T *>(pw_lds);  // [ROWS][LD]
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int r = lane % 16, g = lane / 16;
-    const int otiles = (O + kPwTile - 1) / kPwTile;
-    const int64_t ptiles = (P + kPwTile - 1) / kPwTile;
+    const int xcd = blockIdx.x % 8;
+    const int orng = static_cast<int>((blockIdx.x / 8) % nor);
+    const int64_t slot = (blockIdx.x / 8) / nor, nslot = gridDim.x / 8 / nor;
+    const int o_base = orng * ROWS;
+    const int64_t ptiles = (P + kPwPos - 1) / kPwPos;
+    const int nch = (C + KB * 32 - 1) / (KB * 32);
     const float lo = act_lo(act), hi = act_hi(act);
-    for (int64_t t = blockIdx.x; t < ptiles * otiles; t += gridDim.x) {
-        const int64_t pt = t / otiles;
-        const int ot = static_cast<int>(t % otiles);
-        const int64_t p = pt * kPwTile + wave * 16 + r;  // this lane's position (B column)
-        const bool pin = p < P;
-        floatx4 acc[4];
+    // weights of output rows o_base .. o_base+ROWS-1, channels c_base .. c_base+32KB-1
+    auto stage = [&](int c_base) {
+        for (int i = threadIdx.x; i < ROWS * PIECES; i += kBlock) {
+            const int row = i / PIECES, c = c_base + (i % PIECES) * 8;
+            const int o = o_base + row;
+            const Frag v = (o < O && c < C) ? M::load(w + static_cast<int64_t>(o) * C + c) : M::zero();
+            *reinterpret_cast<Frag *>(ws + row * LD + (c - c_base)) = v;
+        }
+    };
+    auto init = [&](floatx4 (&acc)[OT]) {
 #pragma unroll
-        for (int mt = 0; mt < 4; ++mt) {
-            const int o0 = ot * kPwTile + mt * 16 + 4 * g;
+        for (int mt = 0; mt < OT; ++mt) {
+            const int o0 = o_base + mt * 16 + 4 * g;
 #pragma unroll
             for (int v = 0; v < 4; ++v) acc[mt][v] = (o0 + v < O) ? b[o0 + v] : 0.0f;
         }
-        for (int c0 = 0; c0 < C; c0 += 32) {
-            const int c = c0 + 8 * g;
-            const typename M::frag bx = (pin && c < C) ? M::load(x + p * C + c) : M::zero();
+    };
+    auto load_x = [&](Frag (&bx)[KB], int64_t p, int c_base) {
 #pragma unroll
-            for (int mt = 0; mt < 4; ++mt) {
-                const int o = ot * kPwTile + mt * 16 + r;
-                const typename M::frag a =
-                    (o < O && c < C) ? M::load(w + static_cast<int64_t>(o) * C + c) : M::zero();
-                acc[mt] = M::run(a, bx, acc[mt]);
+        for (int kb = 0; kb < KB; ++kb) {
+            const int c = c_base + kb * 32 + 8 * g;
+            bx[kb] = (p < P && c < C) ? M::load(x + p * C + c) : M::zero();
+        }
+    };
+    auto contract = [&](floatx4 (&acc)[OT], const Frag (&bx)[KB]) {
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) {
+#pragma unroll
+            for (int mt = 0; mt < OT; ++mt) {
+                const Frag a = *reinterpret_cast<const Frag *>(ws + (mt * 16 + r) * LD + kb * 32 + 8 * g);
+                acc[mt] = M::run(a, bx[kb], acc[mt]);
             }
         }
+    };
+    auto finish = [&](const floatx4 (&acc)[OT], int64_t p) {
 #pragma unroll
-        for (int mt = 0; mt < 4; ++mt) {
-            const int o0 = ot * kPwTile + mt * 16 + 4 * g;
-            if (pin && o0 < O) {  // O is a multiple of 8: all four outputs exist
+        for (int mt = 0; mt < OT; ++mt) {
+            const int o0 = o_base + mt * 16 + 4 * g;
+            if (p < P && o0 < O) {  // O is a multiple of 8: all four outputs exist
                 float out[4];
 #pragma unroll
                 for (int v = 0; v < 4; ++v) out[v] = clamp_act(acc[mt][v], lo, hi);
@@ -74,65 +110,142 @@ k_conv1x1(const T *__restrict__ x, int64_t P, int C, const T *__restrict__ w, co
                 io<T>::store4(y + p * O + o0, out);
             }
         }
+    };
+    const int64_t step = nslot * 8;
+    const int64_t lane_p = wave * 16 + r;  // this lane's position within a tile (B column)
+    if (nch == 1) {
+        // weights staged once; the next tile's x is requested before the
+        // current tile is contracted
+        stage(0);
+        __syncthreads();
+        int64_t pt = slot * 8 + xcd;
+        Frag bn[KB];
+        load_x(bn, pt * kPwPos + lane_p, 0);
+        for (; pt < ptiles; pt += step) {
+            // small weight ranges stay in registers across tiles; larger ones
+            // are re-read from LDS per tile (a compiler barrier keeps them
+            // from being hoisted out of the loop)
+            if constexpr (OT * KB * sizeof(Frag) > 128) __asm__ volatile("" ::: "memory");
+            Frag bx[KB];
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb) bx[kb] = bn[kb];
+            if (pt + step < ptiles) load_x(bn, (pt + step) * kPwPos + lane_p, 0);
+            floatx4 acc[OT];
+            init(acc);
+            contract(acc, bx);
+            finish(acc, pt * kPwPos + lane_p);
+        }
+        return;
+    }
+    for (int64_t pt = slot * 8 + xcd; pt < ptiles; pt += step) {
+        const int64_t p = pt * kPwPos + lane_p;
+        floatx4 acc[OT];
+        init(acc);
+        for (int ch = 0; ch < nch; ++ch) {
+            const int c_base = ch * KB * 32;
+            Frag bx[KB];
+            load_x(bx, p, c_base);
+            __syncthreads();  // every wave is done with the previous chunk
+            stage(c_base);
+            __syncthreads();
+            contract(acc, bx);
+        }
+        finish(acc, p);
     }
 }
 
 // ------------------------------------------------------------ depthwise
-// One lane per (output position, 8 channels); the workgroup stages the
-// weights transposed, w_t[k][c], and the biases in LDS (dynamic shared
-// memory: 9*C elements + C floats).
-template <typename T>
+// A work item is (image, block of R output rows, 256 consecutive (column,
+// 8-channel group) tasks, groups fastest).  A lane's task walks the input
+// rows of its R output rows once: each input row's three taps (16-byte
+// loads, zeros past the left and right edges) feed every output row that
+// uses it, so a lane issues (S (R - 1) + 3) x 3 tap loads for R outputs
+// instead of 9 R.  The 9 weight vectors are loaded once per task.  Each
+// output accumulates in fp32 from the bias, taps in (kh, kw) order; rows
+// outside the image are skipped.
+template <typename T, int S, int R>
 __global__ void __launch_bounds__(kBlock)
-k_dwconv3x3(const T *__restrict__ x, int N, int H, int W, int C, int stride, const T *__restrict__ w,
+k_dwconv3x3(const T *__restrict__ x, int N, int H, int W, int C, const T *__restrict__ w,
             const float *__restrict__ b, int act, T *__restrict__ y, int Ho, int Wo) {
+    typedef typename io<T>::vec8 V;
+    constexpr int ROWS = S * (R - 1) + 3;  // input rows of R output rows
     extern __shared__ __align__(16) unsigned char dw_smem[];
-    T *wt = reinterpret_cast<T *>(dw_smem);
-    float *bs = reinterpret_cast<float *>(dw_smem + ((9 * C * static_cast<int>(sizeof(T)) + 15) / 16) * 16);
+    T *wt = reinterpret_cast<T *>(dw_smem);  // [9][C]: the taps, transposed
     for (int i = threadIdx.x; i < 9 * C; i += kBlock) {
-        const int c = i / 9, k = i % 9;
-        wt[k * C + c] = w[i];
+        const int ch = i / 9, k = i % 9;
+        wt[k * C + ch] = w[i];
     }
-    for (int c = threadIdx.x; c < C; c += kBlock) bs[c] = b[c];
     __syncthreads();
     const float lo = act_lo(act), hi = act_hi(act);
-    const int groups = C / 8;
-    const int64_t total = static_cast<int64_t>(N) * Ho * Wo * groups;
-    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < total;
-         i += static_cast<int64_t>(gridDim.x) * kBlock) {
-        const int c = static_cast<int>(i % groups) * 8;
-        const int64_t q = i / groups;  // output position
-        const int j = static_cast<int>(q % Wo);
-        const int ii = static_cast<int>((q / Wo) % Ho);
-        const int n = static_cast<int>(q / (static_cast<int64_t>(Wo) * Ho));
-        float s[8];
+    const int cgs = C / 8;
+    const int tasks = Wo * cgs;
+    const int chunks = (tasks + kBlock - 1) / kBlock;
+    const int rbs = (Ho + R - 1) / R;
+    const int64_t items = static_cast<int64_t>(N) * rbs * chunks;
+    for (int64_t it = blockIdx.x; it < items; it += gridDim.x) {
+        const int chunk = static_cast<int>(it % chunks);
+        const int64_t nr = it / chunks;
+        const int rb = static_cast<int>(nr % rbs), n = static_cast<int>(nr / rbs);
+        const int task = chunk * kBlock + static_cast<int>(threadIdx.x);
+        if (task >= tasks) continue;
+        const int cg = task % cgs, j = task / cgs, c = cg * 8;
+        const int i0 = rb * R;  // first output row
+        V wk[9];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) s[u] = bs[c + u];
+        for (int k = 0; k < 9; ++k) wk[k] = io<T>::raw8(wt + k * C + c);
+        float acc[R][8];
 #pragma unroll
-        for (int k = 0; k < 9; ++k) {
-            const int hh = stride * ii + k / 3 - 1, ww = stride * j + k % 3 - 1;
-            if (hh >= 0 && hh < H && ww >= 0 && ww < W) {
-                float v[8], wk[8];
-                io<T>::load8(x + ((static_cast<int64_t>(n) * H + hh) * W + ww) * C + c, v);
-                io<T>::load8(wt + k * C + c, wk);
+        for (int q = 0; q < R; ++q)
 #pragma unroll
-                for (int u = 0; u < 8; ++u) s[u] = __builtin_fmaf(wk[u], v[u], s[u]);
+            for (int u = 0; u < 8; ++u) acc[q][u] = b[c + u];
+        const T *img = x + static_cast<int64_t>(n) * H * W * C;
+#pragma unroll
+        for (int t = 0; t < ROWS; ++t) {
+            const int hh = S * i0 - 1 + t;
+            if (hh < 0 || hh >= H) continue;
+            V v[3];
+#pragma unroll
+            for (int dw = 0; dw < 3; ++dw) {
+                const int ww = S * j - 1 + dw;
+                if (ww >= 0 && ww < W) {
+                    v[dw] = io<T>::raw8(img + (static_cast<int64_t>(hh) * W + ww) * C + c);
+                } else {
+                    v[dw] = V{};
+                }
+            }
+#pragma unroll
+            for (int q = 0; q < R; ++q) {
+                const int dh = t - S * q;  // compile-time after unrolling
+                if (dh < 0 || dh > 2) continue;
+#pragma unroll
+                for (int dw = 0; dw < 3; ++dw)
+#pragma unroll
+                    for (int u = 0; u < 8; ++u)
+                        acc[q][u] = __builtin_fmaf(static_cast<float>(wk[dh * 3 + dw][u]),
+                                                   static_cast<float>(v[dw][u]), acc[q][u]);
             }
         }
-        float o[8];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) o[u] = clamp_act(s[u], lo, hi);
-        T *dst = y + q * C + c;
-        io<T>::store4(dst, o);
-        io<T>::store4(dst + 4, o + 4);
+        for (int q = 0; q < R; ++q) {
+            if (i0 + q >= Ho) break;
+            float o[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) o[u] = clamp_act(acc[q][u], lo, hi);
+            T *dst = y + ((static_cast<int64_t>(n) * Ho + i0 + q) * Wo + j) * C + c;
+            io<T>::store4(dst, o);
+            io<T>::store4(dst + 4, o + 4);
+        }
     }
 }
 
 // ------------------------------------------------------------ full 3x3
-// One lane per (output position, 8 output channels); weights [O][Ci][3][3]
-// and biases staged in LDS as fp32, the weights reordered to [k][ci][o] so a
-// lane's 8 outputs of one tap and input channel are two 16-byte reads
-// (dynamic shared memory: 9*Ci*O + O floats).  Ci is small (the stem's 3
-// input channels); input rows are read element by element.
+// One lane per output position computing 32 outputs at a time; weights
+// [O][Ci][3][3] and biases staged in LDS as fp32, reordered to [k][ci][o] so
+// that the 32 weights of one tap and input channel are 8 broadcast 16-byte
+// reads.  Ci is small (the stem's 3 input channels): a lane reads each of its
+// 9 Ci input values once per 32 outputs.  Accumulation in fp32 from the
+// bias, taps in (kh, kw) order, input channels ascending (dynamic shared
+// memory: 9*Ci*O + O floats).
 template <typename T>
 __global__ void __launch_bounds__(kBlock)
 k_conv3x3(const T *__restrict__ x, int N, int H, int W, int Ci, int stride, const T *__restrict__ w,
@@ -147,37 +260,48 @@ k_conv3x3(const T *__restrict__ x, int N, int H, int W, int Ci, int stride, cons
     for (int o = threadIdx.x; o < O; o += kBlock) bs[o] = b[o];
     __syncthreads();
     const float lo = act_lo(act), hi = act_hi(act);
-    const int groups = O / 8;
-    const int64_t total = static_cast<int64_t>(N) * Ho * Wo * groups;
-    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < total;
-         i += static_cast<int64_t>(gridDim.x) * kBlock) {
-        const int o0 = static_cast<int>(i % groups) * 8;
-        const int64_t q = i / groups;
-        const int j = static_cast<int>(q % Wo);
-        const int ii = static_cast<int>((q / Wo) % Ho);
-        const int n = static_cast<int>(q / (static_cast<int64_t>(Wo) * Ho));
-        float s[8];
+    const int64_t total = static_cast<int64_t>(N) * Ho * Wo;
+    for (int64_t q = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; q < total;
+         q += static_cast<int64_t>(gridDim.x) * kBlock) {
+        const int64_t ni = q / Wo;
+        const int j = static_cast<int>(q - ni * Wo);
+        const int n = static_cast<int>(ni / Ho), i = static_cast<int>(ni - static_cast<int64_t>(n) * Ho);
+        const T *img = x + static_cast<int64_t>(n) * H * W * Ci;
+        for (int o0 = 0; o0 < O; o0 += 32) {
+            const int ng = min(4, (O - o0) / 8);  // 8-output groups in this pass
+            float s[32];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) s[u] = bs[o0 + u];
-        for (int k = 0; k < 9; ++k) {
-            const int hh = stride * ii + k / 3 - 1, ww = stride * j + k % 3 - 1;
-            if (hh < 0 || hh >= H || ww < 0 || ww >= W) continue;
-            const T *px = x + ((static_cast<int64_t>(n) * H + hh) * W + ww) * Ci;
-            for (int c = 0; c < Ci; ++c) {
-                const float v = static_cast<float>(px[c]);
-                const float4 wa = *reinterpret_cast<const float4 *>(ws + (k * Ci + c) * O + o0);
-                const float4 wb = *reinterpret_cast<const float4 *>(ws + (k * Ci + c) * O + o0 + 4);
-                const float wk[8] = {wa.x, wa.y, wa.z, wa.w, wb.x, wb.y, wb.z, wb.w};
+            for (int u = 0; u < 32; ++u) s[u] = (u / 8 < ng) ? bs[o0 + u] : 0.0f;
 #pragma unroll
-                for (int u = 0; u < 8; ++u) s[u] = __builtin_fmaf(wk[u], v, s[u]);
+            for (int k = 0; k < 9; ++k) {
+                const int hh = stride * i + k / 3 - 1, ww = stride * j + k % 3 - 1;
+                if (hh < 0 || hh >= H || ww < 0 || ww >= W) continue;
+                const T *px = img + (static_cast<int64_t>(hh) * W + ww) * Ci;
+                for (int c = 0; c < Ci; ++c) {
+                    const float v = static_cast<float>(px[c]);
+                    const float *wr = ws + (k * Ci + c) * O + o0;
+#pragma unroll
+                    for (int gq = 0; gq < 4; ++gq) {
+                        if (gq >= ng) break;
+                        const float4 wa = *reinterpret_cast<const float4 *>(wr + 8 * gq);
+                        const float4 wb = *reinterpret_cast<const float4 *>(wr + 8 * gq + 4);
+                        const float wk[8] = {wa.x, wa.y, wa.z, wa.w, wb.x, wb.y, wb.z, wb.w};
+#pragma unroll
+                        for (int u = 0; u < 8; ++u) s[8 * gq + u] = __builtin_fmaf(wk[u], v, s[8 * gq + u]);
+                    }
+                }
+            }
+            T *dst = y + q * O + o0;
+#pragma unroll
+            for (int gq = 0; gq < 4; ++gq) {
+                if (gq >= ng) break;
+                float o[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) o[u] = clamp_act(s[8 * gq + u], lo, hi);
+                io<T>::store4(dst + 8 * gq, o);
+                io<T>::store4(dst + 8 * gq + 4, o + 4);
             }
         }
-        float o[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) o[u] = clamp_act(s[u], lo, hi);
-        T *dst = y + q * O + o0;
-        io<T>::store4(dst, o);
-        io<T>::store4(dst + 4, o + 4);
     }
 }
 

@@ -7,6 +7,7 @@
 
 #include <stdint.h>
 #include <algorithm>
+#include <atomic>
 #include <string.h>
 
 #include "dynconv.h"
@@ -744,7 +745,7 @@ dynconv_status layer_shape(const dynconv_layer &L, dynconv_shape in, LayerShapes
     if (b.w_expand && !b.b_expand) return DYNCONV_ERR_NULL;
     const int E = b.w_expand ? b.c_hidden : b.c_in;
     if (!b.w_expand && b.c_hidden != b.c_in) return DYNCONV_ERR_SHAPE;
-    if (b.c_in % 8 || b.c_out % 8 || E % 8 || b.c_in < 8 || b.c_out < 8 || E > 4096 || b.c_out > 4096)
+    if (b.c_in % 8 || b.c_out % 8 || E % 8 || b.c_in < 8 || b.c_out < 8 || E > 1792 || b.c_out > 4096)
         return DYNCONV_ERR_UNSUPPORTED;
     for (int a : {b.act_expand, b.act_dw, b.act_project})
         if (a < DYNCONV_ACT_NONE || a > DYNCONV_ACT_RELU6) return DYNCONV_ERR_ARG;
@@ -812,29 +813,103 @@ int elem_grid(int64_t lanes) {
     return static_cast<int>(g);
 }
 
+// Workgroups of a kernel that the whole device holds at once (occupancy x
+// compute units); 0 when the runtime cannot say.
+template <typename K>
+int64_t resident_groups(K kern, size_t lds) {
+    int dev = 0, cus = 0, per_cu = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, kBlock, lds) != hipSuccess)
+        return 0;
+    return static_cast<int64_t>(cus) * per_cu;
+}
+
+template <typename T, int OT, int KB>
+void launch_conv1x1_k(const void *x, int64_t P, int C, const void *w, const float *b, int O, int act,
+                      const void *res, void *y, hipStream_t st, Marks &mk) {
+    const int nor = ((O + 15) / 16 + OT - 1) / OT;
+    const int64_t ptiles = (P + kPwPos - 1) / kPwPos;
+    int64_t slots = (ptiles + 7) / 8;  // position-tile slots per XCD
+    // one contraction chunk: as many workgroups as the device holds at once
+    // (queried once), each staging the weights once and walking several
+    // tiles; else one tile per workgroup
+    const bool one_chunk = C <= KB * 32;
+    static std::atomic<int64_t> resident{0};
+    if (one_chunk && resident.load() == 0)
+        resident.store(resident_groups(k_conv1x1<T, OT, KB>, pw_lds_bytes<T, OT, KB>()));
+    const int64_t full = resident.load() > 0 ? resident.load() : 1024;
+    const int64_t cap = one_chunk ? (full / 8 + nor - 1) / nor : 2048 / nor + 1;
+    if (slots > cap) slots = cap;
+    if (slots < 1) slots = 1;
+    launch(mk, k_conv1x1<T, OT, KB>, dim3(static_cast<unsigned>(slots * 8 * nor)), dim3(kBlock),
+           pw_lds_bytes<T, OT, KB>(), st, static_cast<const T *>(x), P, C, static_cast<const T *>(w), b, O, act,
+           static_cast<const T *>(res), static_cast<T *>(y), nor);
+}
+
+// Output tiles per workgroup (2, 4, 6, 8 or 12) and contraction steps per
+// chunk (1, 2, 4 or 8): one output range when the outputs fit 12 tiles;
+// fewer tiles per range while position tiles x ranges stay under 1024 work
+// items; the largest chunk the contraction needs whose staged weights fit
+// 64 KB of LDS.
+template <typename T, int OT>
+void launch_conv1x1_ot(const void *x, int64_t P, int C, const void *w, const float *b, int O, int act,
+                       const void *res, void *y, hipStream_t st, Marks &mk) {
+    constexpr bool kFits8 = pw_lds_bytes<T, OT, 8>() <= kMaxDynLds;
+    const int ks = (C + 31) / 32;
+    int kb = ks <= 1 ? 1 : ks <= 2 ? 2 : ks <= 4 ? 4 : 8;
+    if (kb == 8 && !kFits8) kb = 4;
+    while (kb > 1 && static_cast<size_t>(OT) * 16 * (kb * 32 + 8) * sizeof(T) > kMaxDynLds) kb /= 2;
+    if (kb == 1) launch_conv1x1_k<T, OT, 1>(x, P, C, w, b, O, act, res, y, st, mk);
+    else if (kb == 2) launch_conv1x1_k<T, OT, 2>(x, P, C, w, b, O, act, res, y, st, mk);
+    else if (kb == 4) launch_conv1x1_k<T, OT, 4>(x, P, C, w, b, O, act, res, y, st, mk);
+    else if constexpr (kFits8) launch_conv1x1_k<T, OT, 8>(x, P, C, w, b, O, act, res, y, st, mk);
+}
+
 template <typename T>
 void launch_conv1x1(const void *x, int64_t P, int C, const void *w, const float *b, int O, int act,
                     const void *res, void *y, hipStream_t st, Marks &mk) {
-    const int64_t tiles = ((P + kPwTile - 1) / kPwTile) * ((O + kPwTile - 1) / kPwTile);
-    const int grid = static_cast<int>(tiles < 16384 ? tiles : 16384);
-    launch(mk, k_conv1x1<T>, dim3(grid), dim3(kBlock), 0, st, static_cast<const T *>(x), P, C,
-           static_cast<const T *>(w), b, O, act, static_cast<const T *>(res), static_cast<T *>(y));
+    static const int kOt[] = {12, 8, 6, 4, 2};
+    const int nmt = (O + 15) / 16;
+    const int64_t ptiles = (P + kPwPos - 1) / kPwPos;
+    int i = nmt <= 2 ? 4 : nmt <= 4 ? 3 : nmt <= 6 ? 2 : nmt <= 8 ? 1 : 0;
+    while (i < 4 && ptiles * ((nmt + kOt[i] - 1) / kOt[i]) < 1024) ++i;
+    switch (kOt[i]) {
+    case 12: launch_conv1x1_ot<T, 12>(x, P, C, w, b, O, act, res, y, st, mk); break;
+    case 8: launch_conv1x1_ot<T, 8>(x, P, C, w, b, O, act, res, y, st, mk); break;
+    case 6: launch_conv1x1_ot<T, 6>(x, P, C, w, b, O, act, res, y, st, mk); break;
+    case 4: launch_conv1x1_ot<T, 4>(x, P, C, w, b, O, act, res, y, st, mk); break;
+    default: launch_conv1x1_ot<T, 2>(x, P, C, w, b, O, act, res, y, st, mk); break;
+    }
+}
+
+// Output rows per depthwise task: 4 for 16-bit storage, 2 for fp32.
+template <typename T, int S>
+void launch_dwconv_s(const void *x, dynconv_shape in, dynconv_shape out, int C, const void *w, const float *b,
+                     int act, void *y, hipStream_t st, Marks &mk) {
+    constexpr int R = sizeof(T) == 4 ? 2 : 4;
+    const size_t lds = static_cast<size_t>(9) * C * sizeof(T);
+    const int64_t chunks = (static_cast<int64_t>(out.w) * (C / 8) + kBlock - 1) / kBlock;
+    int64_t items = static_cast<int64_t>(out.n) * ((out.h + R - 1) / R) * chunks;
+    if (items > 4096) items = 4096;
+    if (items < 1) items = 1;
+    launch(mk, k_dwconv3x3<T, S, R>, dim3(static_cast<unsigned>(items)), dim3(kBlock), lds, st,
+           static_cast<const T *>(x), in.n, in.h, in.w, C, static_cast<const T *>(w), b, act, static_cast<T *>(y),
+           out.h, out.w);
 }
 
 template <typename T>
 void launch_dwconv(const void *x, dynconv_shape in, dynconv_shape out, int C, int stride, const void *w,
                    const float *b, int act, void *y, hipStream_t st, Marks &mk) {
-    const size_t lds = (9 * C * sizeof(T) + 15) / 16 * 16 + 4 * C;
-    launch(mk, k_dwconv3x3<T>, dim3(elem_grid(positions(out) * (C / 8))), dim3(kBlock), lds, st,
-           static_cast<const T *>(x), in.n, in.h, in.w, C, stride, static_cast<const T *>(w), b, act,
-           static_cast<T *>(y), out.h, out.w);
+    if (stride == 1) launch_dwconv_s<T, 1>(x, in, out, C, w, b, act, y, st, mk);
+    else launch_dwconv_s<T, 2>(x, in, out, C, w, b, act, y, st, mk);
 }
 
 template <typename T>
 void launch_conv3x3(const void *x, dynconv_shape in, dynconv_shape out, const dynconv_layer &L, void *y,
                     hipStream_t st, Marks &mk) {
     const size_t lds = 4 * (9 * L.c_in * L.c_out + L.c_out);
-    launch(mk, k_conv3x3<T>, dim3(elem_grid(positions(out) * (L.c_out / 8))), dim3(kBlock), lds, st,
+    launch(mk, k_conv3x3<T>, dim3(elem_grid(positions(out))), dim3(kBlock), lds, st,
            static_cast<const T *>(x), in.n, in.h, in.w, L.c_in, L.stride, static_cast<const T *>(L.w), L.b,
            L.c_out, L.act, static_cast<T *>(y), out.h, out.w);
 }

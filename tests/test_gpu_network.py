@@ -176,3 +176,101 @@ def test_gated_network_end_to_end(net_f16):
     err = util.normwise(y, util.nhwc(cur))
     log("  gated network vs forced-mask oracle: err %.2e" % err)
     assert err <= util.TOL["f16"]
+
+
+POINTWISE_CASES = [
+    # dtype, (N, H, W), C, O: every output-range width (2..12 tiles of 16),
+    # contraction chunks of 1..8 steps of 32 and several chunks, one partial
+    # 64-position tile, and large position counts
+    ("f16", (16, 112, 112), 16, 96),
+    ("f16", (4, 56, 56), 24, 144),
+    ("bf16", (64, 7, 7), 960, 320),
+    ("f16", (64, 7, 7), 320, 1280),
+    ("f16", (2, 3, 5), 576, 160),
+    ("f32", (3, 9, 11), 40, 200),
+    ("f32", (64, 7, 7), 960, 320),
+    ("bf16", (1, 1, 1), 8, 8),
+    ("f16", (8, 14, 14), 136, 72),
+]
+
+
+@pytest.mark.parametrize("dtype,nhw,C,O", POINTWISE_CASES)
+def test_pointwise_layer(dtype, nhw, C, O):
+    """A network of one 1x1 convolution against the oracle's conv1x1."""
+    import oracle.network as onet
+    N, H, W = nhw
+    rng = inputs.rng_for(4000 + C + O)
+    x = inputs.round_to_storage(rng.normal(0.0, 1.0, size=(N, H, W, C)), dtype)
+    L = {"kind": "conv1x1", "w": inputs.round_to_storage(rng.normal(0.0, 0.05, size=(O, C)), dtype),
+         "b": rng.normal(0.0, 0.05, size=O).astype(np.float32), "act": 2}
+    y, _, _ = run_net(x, [L], dtype)
+    want = util.nhwc(onet.conv1x1(util.nchw(x), L["w"], L["b"], L["act"]))
+    err = util.normwise(y, want)
+    log("  pointwise %s %s C=%d O=%d err %.2e" % (dtype, nhw, C, O, err))
+    assert err <= util.TOL[dtype]
+
+
+@pytest.mark.parametrize("dtype,nhw,stride,c,co,e", [
+    ("f16", (2, 9, 7), 2, 16, 24, 96), ("bf16", (3, 1, 13), 2, 24, 32, 48), ("f32", (2, 11, 5), 1, 8, 16, 40),
+    ("f16", (1, 2, 2), 2, 32, 64, 1792), ("bf16", (4, 17, 30), 1, 40, 16, 40)])
+def test_strided_and_widening_blocks(dtype, nhw, stride, c, co, e):
+    """Ungated blocks of odd sizes, both strides, widening outputs (no
+    residual), a 1792-channel hidden layer and expansion factor 1."""
+    import oracle.network as onet
+    N, H, W = nhw
+    rng = inputs.rng_for(4200 + c + e)
+    x = inputs.round_to_storage(inputs.blob_features(rng, N, H, W, c), dtype)
+
+    def wgt(*shape):
+        return inputs.round_to_storage(rng.normal(0.0, 0.1, size=shape), dtype)
+
+    t1 = e != c
+    L = {"kind": "block", "stride": stride, "acts": (2, 2, 0),
+         "w1": wgt(e, c) if t1 else None, "b1": rng.normal(0, 0.1, e).astype(np.float32) if t1 else None,
+         "w2": wgt(e, 9), "b2": rng.normal(0, 0.1, e).astype(np.float32),
+         "w3": wgt(co, e), "b3": rng.normal(0, 0.1, co).astype(np.float32)}
+    y, _, _ = run_net(x, [L], dtype)
+    want = util.nhwc(onet.dense_block(util.nchw(x), L))
+    assert y.shape == want.shape
+    err = util.normwise(y, want)
+    log("  block %s %s s%d %d->%d (E %d) err %.2e" % (dtype, nhw, stride, c, co, e, err))
+    assert err <= util.TOL[dtype]
+
+
+@pytest.mark.parametrize("dtype", ["f16", "f32"])
+def test_ungated_residual_block(dtype):
+    """A stride-1 block of equal widths without a mask unit runs dense and
+    adds its input (the projection's residual operand)."""
+    import oracle.network as onet
+    rng = inputs.rng_for(4100)
+    C, E = 24, 144
+    x = inputs.round_to_storage(inputs.blob_features(rng, 3, 20, 17, C), dtype)
+    w = inputs.block_weights(rng, C, E, dtype=dtype)
+    L = {"kind": "block", "stride": 1, "acts": (2, 2, 0), "w1": w["w1"], "b1": w["b1"], "w2": w["w2"],
+         "b2": w["b2"], "w3": w["w3"], "b3": w["b3"]}
+    y, _, _ = run_net(x, [L], dtype)
+    want = util.nhwc(onet.dense_block(util.nchw(x), L))
+    err = util.normwise(y, want)
+    log("  ungated residual block %s err %.2e" % (dtype, err))
+    assert err <= util.TOL[dtype]
+
+
+@pytest.mark.parametrize("dtype,nhw,ci,co,stride", [
+    ("f16", (2, 17, 23), 3, 32, 2), ("bf16", (1, 9, 8), 16, 40, 1), ("f32", (3, 5, 7), 1, 8, 2),
+    ("f16", (1, 1, 1), 4, 72, 1), ("f16", (2, 30, 3), 8, 200, 2)])
+def test_full_conv3x3_layer(dtype, nhw, ci, co, stride):
+    """A network of one full 3x3 convolution (the stem's kind) against the
+    oracle's conv3x3: odd sizes, both strides, output counts that are not
+    multiples of 32."""
+    import oracle.network as onet
+    N, H, W = nhw
+    rng = inputs.rng_for(4300 + ci + co)
+    x = inputs.round_to_storage(rng.normal(0.0, 1.0, size=(N, H, W, ci)), dtype)
+    L = {"kind": "conv3x3", "w": inputs.round_to_storage(rng.normal(0.0, 0.1, size=(co, ci, 3, 3)), dtype),
+         "b": rng.normal(0.0, 0.1, size=co).astype(np.float32), "stride": stride, "act": 2}
+    y, _, _ = run_net(x, [L], dtype)
+    want = util.nhwc(onet.conv3x3(util.nchw(x), L["w"], L["b"], stride, L["act"]))
+    assert y.shape == want.shape
+    err = util.normwise(y, want)
+    log("  conv3x3 %s %s %d->%d s%d err %.2e" % (dtype, nhw, ci, co, stride, err))
+    assert err <= util.TOL[dtype]
