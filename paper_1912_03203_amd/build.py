@@ -25,14 +25,29 @@ def hipcc() -> str:
 
 
 def build(verbose: bool = False) -> str:
+    """Compile the library and, in parallel, its device assembly, which the
+    MFMA check (mfma_lint) scans; raises on a compile error or a finding."""
+    from . import mfma_lint
+
     tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [hipcc()] + HIPCC_FLAGS + ["-I", os.path.join(ROOT, "include"),
-                                     "-I", os.path.join(PKG, "csrc"), "-o", tmp, SRC]
-    res = subprocess.run(cmd, capture_output=True, text=True)
-    if res.returncode != 0:
-        raise RuntimeError("hipcc failed:\n" + res.stdout + res.stderr)
+    asm = os.path.join(PKG, "_build", "dynconv_gfx950.s")
+    os.makedirs(os.path.dirname(asm), exist_ok=True)
+    inc = ["-I", os.path.join(ROOT, "include"), "-I", os.path.join(PKG, "csrc")]
+    lib_cmd = [hipcc()] + HIPCC_FLAGS + inc + ["-o", tmp, SRC]
+    asm_flags = [f for f in HIPCC_FLAGS if f not in ("-fPIC", "-shared")]
+    asm_cmd = [hipcc()] + asm_flags + ["-S", "--offload-device-only"] + inc + ["-o", asm, SRC]
+    procs = [subprocess.Popen(c, stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True)
+             for c in (lib_cmd, asm_cmd)]
+    outs = [p.communicate() for p in procs]
+    for p, (out, err) in zip(procs, outs):
+        if p.returncode != 0:
+            raise RuntimeError("hipcc failed:\n" + out + err)
     if verbose:
-        print(res.stdout + res.stderr)
+        print(outs[0][0] + outs[0][1])
+    with open(asm) as f:
+        findings = mfma_lint.check(f.read())
+    if findings:
+        raise RuntimeError("MFMA result read too early in the generated code:\n" + "\n".join(findings[:20]))
     os.replace(tmp, LIB)
     return LIB
 

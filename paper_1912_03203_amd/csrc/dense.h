@@ -238,6 +238,208 @@ k_dwconv3x3(const T *__restrict__ x, int N, int H, int W, int C, const T *__rest
     }
 }
 
+// ------------------------------------------------------ expansion + depthwise
+// An ungated block's 1x1 expansion and depthwise 3x3 in one launch, so that
+// the expanded tensor never goes to HBM.  A work item is a tile of 8 x 8
+// depthwise outputs of one image; its input region, (S*7+3)^2 positions, is
+// staged in LDS (rows of C + 8 elements, zeros outside the image).  The
+// workgroups are persistent: each stages all weights in LDS once (expansion
+// rows of C + 8, depthwise taps transposed to [9][E]) and walks items,
+// loading the next item's region into registers while it computes the
+// current one.  Per 32-channel slice of the hidden layer: each wave expands
+// 16-position tiles of the region on the matrix cores (operands as in
+// k_conv1x1: bias first, 32-channel steps ascending), applies the activation
+// and stores the slice into a region array (zeros at positions outside the
+// image: the depthwise's zero padding); then lane (o, cg) computes the
+// depthwise of output o for 8 hidden channels from 9 fixed slots of that
+// array, fp32 from the bias, taps in (kh, kw) order, and writes it to
+// h2 [Ho*Wo][E].
+constexpr int kEdTile = 8;  // depthwise outputs per tile side
+
+template <int S>
+__host__ __device__ constexpr int ed_region_side() { return S * (kEdTile - 1) + 3; }
+template <int S>
+__host__ __device__ constexpr int ed_region_tiles() {
+    return (ed_region_side<S>() * ed_region_side<S>() + 15) / 16;
+}
+template <typename T, int S>
+__host__ __device__ constexpr size_t ed_lds_bytes(int C, int E) {
+    return static_cast<size_t>(ed_region_tiles<S>()) * 16 * ((C + 8) + 40) * sizeof(T)  // xs + h1
+           + static_cast<size_t>(E) * (C + 8) * sizeof(T) + 9 * static_cast<size_t>(E) * sizeof(T)  // w1, w2t
+           + 8 * static_cast<size_t>(E);                                                            // b1, b2
+}
+
+template <typename T, int S, int KS>
+__global__ void __launch_bounds__(kBlock)
+k_expand_dw(const T *__restrict__ x, int N, int H, int W, int C, const T *__restrict__ w1,
+            const float *__restrict__ b1, int act1, int E, const T *__restrict__ w2, const float *__restrict__ b2,
+            int act2, T *__restrict__ h2, int Ho, int Wo) {
+    typedef mma<T> M;
+    typedef typename M::frag Frag;
+    typedef typename io<T>::vec8 V;
+    constexpr int RS = ed_region_side<S>();
+    constexpr int RP = RS * RS;
+    constexpr int NT = ed_region_tiles<S>();
+    constexpr int TPW = (NT + kWavesPerBlock - 1) / kWavesPerBlock;  // tiles per wave
+    constexpr int HP = 40;                                          // h1 row pitch (32 + 8)
+    constexpr int XP = (NT * 16 * KS * 4 + kBlock - 1) / kBlock;     // x pieces per thread (<= 32)
+    static_assert(XP <= 32, "x pieces per thread exceed the validity mask");
+    extern __shared__ __align__(16) unsigned char ed_smem[];
+    const int PX = C + 8;  // row pitch of x and of the expansion weights
+    T *xs = reinterpret_cast<T *>(ed_smem);  // [NT*16][PX]
+    T *h1 = xs + NT * 16 * PX;               // [NT*16][HP]
+    T *w1s = h1 + NT * 16 * HP;              // [E][PX]
+    T *w2t = w1s + E * PX;                   // [9][E]
+    float *b1s = reinterpret_cast<float *>(w2t + 9 * E);  // [E]
+    float *b2s = b1s + E;                                 // [E]
+    const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+    const int r = lane % 16, g = lane / 16;
+    const float lo1 = act_lo(act1), hi1 = act_hi(act1), lo2 = act_lo(act2), hi2 = act_hi(act2);
+    const int tr = (Ho + kEdTile - 1) / kEdTile, tc = (Wo + kEdTile - 1) / kEdTile;
+    const int64_t items = static_cast<int64_t>(N) * tr * tc;
+    const int nsl = (E + 31) / 32;
+    const int pieces = C / 8;  // 16-byte pieces of an x row
+    if (static_cast<int64_t>(blockIdx.x) >= items) return;
+    // all weights, once
+    for (int i = tid; i < E * pieces; i += kBlock) {
+        const int e = i / pieces, pc = (i % pieces) * 8;
+        *reinterpret_cast<V *>(w1s + e * PX + pc) = io<T>::raw8(w1 + static_cast<int64_t>(e) * C + pc);
+    }
+    for (int i = tid; i < 9 * E; i += kBlock) {
+        const int e = i / 9, k = i % 9;
+        w2t[k * E + e] = w2[i];
+    }
+    for (int e = tid; e < E; e += kBlock) {
+        b1s[e] = b1[e];
+        b2s[e] = b2[e];
+    }
+    // the item's region origin; one thread's x pieces of it, into registers
+    auto origin = [&](int64_t it, int &n, int &i0, int &j0) {
+        n = static_cast<int>(it / (tr * tc));
+        const int rem = static_cast<int>(it % (tr * tc));
+        i0 = (rem / tc) * kEdTile;
+        j0 = (rem % tc) * kEdTile;
+    };
+    // Loads are issued unconditionally (pieces outside the image read the
+    // tensor's first piece) and replaced by zeros only when stored, so no
+    // wait for them is needed before the current item's slices.
+    auto load_x = [&](int64_t it, V (&xr)[XP], uint32_t &ok) {
+        int n, i0, j0;
+        origin(it, n, i0, j0);
+        const int hb = S * i0 - 1, wb = S * j0 - 1;
+        const T *img = x + static_cast<int64_t>(n) * H * W * C;
+        ok = 0;
+#pragma unroll
+        for (int q = 0; q < XP; ++q) {
+            const int i = tid + q * kBlock;
+            const int slot = i / pieces, pc = (i % pieces) * 8;
+            const int hh = hb + slot / RS, ww = wb + slot % RS;
+            const bool in = i < NT * 16 * pieces && slot < RP && hh >= 0 && hh < H && ww >= 0 && ww < W;
+            xr[q] = io<T>::raw8(in ? img + (static_cast<int64_t>(hh) * W + ww) * C + pc : x);
+            ok |= static_cast<uint32_t>(in) << q;
+        }
+    };
+    auto store_x = [&](const V (&xr)[XP], uint32_t ok) {
+#pragma unroll
+        for (int q = 0; q < XP; ++q) {
+            const int i = tid + q * kBlock;
+            if (i < NT * 16 * pieces)
+                *reinterpret_cast<V *>(xs + (i / pieces) * PX + (i % pieces) * 8) = ((ok >> q) & 1u) ? xr[q] : V{};
+        }
+    };
+    V xr[XP];
+    uint32_t xok;
+    int64_t it = blockIdx.x;
+    load_x(it, xr, xok);
+    store_x(xr, xok);
+    __syncthreads();
+    for (;;) {
+        const int64_t next = it + gridDim.x;
+        if (next < items) load_x(next, xr, xok);
+        int n, i0, j0;
+        origin(it, n, i0, j0);
+        const int hb = S * i0 - 1, wb = S * j0 - 1;
+        for (int sl = 0; sl < nsl; ++sl) {
+            const int e0 = sl * 32;
+            // expansion of the region tiles; waves past the last tile repeat
+            // it (same values), so every wave issues the same MFMAs
+#pragma unroll
+            for (int jt = 0; jt < TPW; ++jt) {
+                const int t = wave + kWavesPerBlock * jt;
+                const int tt = t < NT ? t : NT - 1;
+                const int slot = tt * 16 + r;
+                Frag bx[KS];
+#pragma unroll
+                for (int ks = 0; ks < KS; ++ks) {
+                    const int c = ks * 32 + 8 * g;
+                    bx[ks] = (c < C) ? *reinterpret_cast<const Frag *>(xs + slot * PX + c) : M::zero();
+                }
+                // D[e][slot]: rows are hidden channels, columns region slots
+                const int hh = hb + slot / RS, ww = wb + slot % RS;
+                const bool inside = slot < RP && hh >= 0 && hh < H && ww >= 0 && ww < W;
+#pragma unroll
+                for (int m = 0; m < 2; ++m) {
+                    const int er = e0 + m * 16 + r;  // A row: hidden channel
+                    floatx4 d;
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        const int e = e0 + m * 16 + 4 * g + v;
+                        d[v] = (e < E) ? b1s[e] : 0.0f;
+                    }
+#pragma unroll
+                    for (int ks = 0; ks < KS; ++ks) {
+                        const int c = ks * 32 + 8 * g;
+                        const Frag a = (er < E && c < C) ? *reinterpret_cast<const Frag *>(w1s + er * PX + c)
+                                                         : M::zero();
+                        d = M::run(a, bx[ks], d);
+                    }
+                    if (t < NT) {
+                        float o[4];
+#pragma unroll
+                        for (int v = 0; v < 4; ++v) o[v] = inside ? clamp_act(d[v], lo1, hi1) : 0.0f;
+                        io<T>::store4(h1 + slot * HP + m * 16 + 4 * g, o);
+                    }
+                }
+            }
+            __syncthreads();
+            // depthwise: lane (o, cg), output o of the tile, channels 8cg..8cg+7
+            {
+                const int o = tid / 4, cg = tid % 4;
+                const int oi = o / kEdTile, oj = o % kEdTile;
+                const int e8 = e0 + 8 * cg;
+                const int i = i0 + oi, j = j0 + oj;
+                if (e8 < E) {
+                    float acc[8];
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) acc[u] = b2s[e8 + u];
+#pragma unroll
+                    for (int k = 0; k < 9; ++k) {
+                        const int slot = (S * oi + k / 3) * RS + S * oj + k % 3;
+                        const V v = io<T>::raw8(h1 + slot * HP + 8 * cg);
+                        const V wk = io<T>::raw8(w2t + k * E + e8);
+#pragma unroll
+                        for (int u = 0; u < 8; ++u)
+                            acc[u] = __builtin_fmaf(static_cast<float>(wk[u]), static_cast<float>(v[u]), acc[u]);
+                    }
+                    if (i < Ho && j < Wo) {
+                        float out[8];
+#pragma unroll
+                        for (int u = 0; u < 8; ++u) out[u] = clamp_act(acc[u], lo2, hi2);
+                        T *dst = h2 + ((static_cast<int64_t>(n) * Ho + i) * Wo + j) * E + e8;
+                        io<T>::store4(dst, out);
+                        io<T>::store4(dst + 4, out + 4);
+                    }
+                }
+            }
+            __syncthreads();  // h1 is rewritten by the next slice, xs by the next item
+        }
+        if (next >= items) break;
+        store_x(xr, xok);
+        __syncthreads();
+        it = next;
+    }
+}
+
 // ------------------------------------------------------------ full 3x3
 // One lane per output position computing 32 outputs at a time; weights
 // [O][Ci][3][3] and biases staged in LDS as fp32, reordered to [k][ci][o] so

@@ -278,7 +278,7 @@ void dispatch_mask(dynconv_dtype dt, const void *x, dynconv_shape s, const float
 template <typename T, int MAXC>
 PatchGeom fused_geom_t(dynconv_shape s) {
     typedef typename PatchCfgOf<T, MAXC>::type CFG;
-    return patch_geom(s.h, s.w, CFG::kOwn, CFG::kRegion);
+    return patch_geom(s.n, s.h, s.w, CFG::kOwn, CFG::kRegion);
 }
 
 PatchGeom fused_geom(dynconv_shape s, dynconv_dtype dt) {
@@ -914,6 +914,53 @@ void launch_conv3x3(const void *x, dynconv_shape in, dynconv_shape out, const dy
            L.c_out, L.act, static_cast<T *>(y), out.h, out.w);
 }
 
+// Expansion + depthwise in one launch (ungated blocks): 16-bit storage, at
+// most 64 input channels, LDS within 64 KB, and at least kEdMinItems 8x8
+// output tiles.  Its VALU overhead per tile (region bookkeeping, the
+// activation and packing of every expanded slice) makes it pay only where
+// the expanded tensor is large (MobileNetV2's 112x112x96 at batch 64 saves
+// about 26 us; 56x56x144 breaks even), so smaller layers keep the
+// two-kernel path.
+constexpr int64_t kEdMinItems = 2048;
+
+int64_t ed_items(dynconv_shape out) {
+    return static_cast<int64_t>(out.n) * ((out.h + kEdTile - 1) / kEdTile) * ((out.w + kEdTile - 1) / kEdTile);
+}
+
+bool use_expand_dw(dynconv_dtype dt, int C, int E, int stride, dynconv_shape out) {
+    if (dt == DYNCONV_F32 || C > 64 || ed_items(out) < kEdMinItems) return false;
+    const size_t lds = stride == 1 ? ed_lds_bytes<half_t, 1>(C, E) : ed_lds_bytes<half_t, 2>(C, E);
+    return lds <= kMaxDynLds;
+}
+
+// Persistent workgroups: as many as the device holds at once.
+template <typename T, int S, int KS>
+void launch_expand_dw_k(const void *x, dynconv_shape in, dynconv_shape out, const dynconv_block &b, int E,
+                        void *h2, hipStream_t st, Marks &mk) {
+    const size_t lds = ed_lds_bytes<T, S>(b.c_in, E);
+    int64_t grid = ed_items(out);
+    const int64_t full = resident_groups(k_expand_dw<T, S, KS>, lds);
+    if (full > 0 && grid > full) grid = full;
+    launch(mk, k_expand_dw<T, S, KS>, dim3(static_cast<unsigned>(grid)), dim3(kBlock), lds,
+           st, static_cast<const T *>(x), in.n, in.h, in.w, b.c_in, static_cast<const T *>(b.w_expand), b.b_expand,
+           b.act_expand, E, static_cast<const T *>(b.w_dw), b.b_dw, b.act_dw, static_cast<T *>(h2), out.h, out.w);
+}
+
+template <typename T>
+void launch_expand_dw(const void *x, dynconv_shape in, dynconv_shape out, const dynconv_block &b, int E, int stride,
+                      void *h2, hipStream_t st, Marks &mk) {
+    if constexpr (sizeof(T) == 2) {
+        const bool k1 = b.c_in <= 32;
+        if (stride == 1) {
+            if (k1) launch_expand_dw_k<T, 1, 1>(x, in, out, b, E, h2, st, mk);
+            else launch_expand_dw_k<T, 1, 2>(x, in, out, b, E, h2, st, mk);
+        } else {
+            if (k1) launch_expand_dw_k<T, 2, 1>(x, in, out, b, E, h2, st, mk);
+            else launch_expand_dw_k<T, 2, 2>(x, in, out, b, E, h2, st, mk);
+        }
+    }
+}
+
 #define DC_TYPED(dt, call)                                  \
     do {                                                    \
         if ((dt) == DYNCONV_F32) { typedef float T; call; }  \
@@ -952,6 +999,17 @@ void net_walk(const void *x, void *y, dynconv_shape in, dynconv_dtype dt, const 
         } else {
             const dynconv_block &b = L.blk;
             const void *hin = src;
+            if (b.w_expand && use_expand_dw(dt, b.c_in, ls.hidden, L.stride, ls.out)) {
+                if (plan.note("k_expand_dw"))
+                    DC_TYPED(dt, launch_expand_dw<T>(src, ls.in, ls.out, b, ls.hidden, L.stride, h2, st, mk));
+                const bool resid = L.stride == 1 && b.c_in == b.c_out;
+                if (plan.note("k_conv1x1"))
+                    DC_TYPED(dt, launch_conv1x1<T>(h2, positions(ls.out), ls.hidden, b.w_project, b.b_project,
+                                                   b.c_out, b.act_project, resid ? src : nullptr, dst, st, mk));
+                src = dst;
+                cur = ls.out;
+                continue;
+            }
             if (b.w_expand) {
                 if (plan.note("k_conv1x1"))
                     DC_TYPED(dt, launch_conv1x1<T>(src, positions(ls.in), b.c_in, b.w_expand, b.b_expand,

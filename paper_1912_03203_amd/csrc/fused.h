@@ -78,22 +78,26 @@ template <int MAXC> struct PatchCfgOf<bf16_t, MAXC> : PatchCfgOf<half_t, MAXC> {
 
 // Patch geometry: the image width is cut into equal column strips of at most
 // 32, the height into strips of R rows, with R * Wu <= own and the region
-// (R+2) x (Wu+2) <= region.
+// (R+2) x (Wu+2) <= region.  Small images get shorter row strips until the
+// batch has at least kMinPatches patches, so that the launch still covers
+// the chip.
+constexpr int kMinPatches = 256;
 struct PatchGeom {
     int R, Wu, nph, npw;
 };
-__host__ __device__ inline PatchGeom patch_geom(int H, int W, int own, int region) {
+__host__ __device__ inline PatchGeom patch_geom(int N, int H, int W, int own, int region) {
     PatchGeom p;
     const int strips = (W + kPatchMaxCols - 1) / kPatchMaxCols;
     p.Wu = (W + strips - 1) / strips;
+    p.npw = (W + p.Wu - 1) / p.Wu;
     int r = own / p.Wu;
     const int rr = region / (p.Wu + 2) - 2;
     if (r > rr) r = rr;
     if (r > kPatchMaxRows) r = kPatchMaxRows;
     if (r > H) r = H;
+    while (r > 1 && static_cast<int64_t>(N) * ((H + r - 1) / r) * p.npw < kMinPatches) --r;
     p.R = r < 1 ? 1 : r;
     p.nph = (H + p.R - 1) / p.R;
-    p.npw = (W + p.Wu - 1) / p.Wu;
     return p;
 }
 

@@ -134,9 +134,10 @@ def test_stack_validation(lib):
         return (v + 255) // 256 * 256
 
     # one-launch blocks: ping-pong copy of x, two masks, counts, per-patch
-    # counts (fp16 at 32 channels: patches of 16 x 16, one per image)
+    # counts (fp16 at 32 channels: 16 x 16 images give one patch per image at
+    # full height; a batch this small gets patches of one row, 64 in all)
     fused = lib.dynconv_stack_workspace_bytes(s, blocks, 3, 1, 0)
-    assert fused == up(npos * 32 * 2) + 2 * up(npos) + up(8 * 3) + up(8 * 3 * 4)
+    assert fused == up(npos * 32 * 2) + 2 * up(npos) + up(8 * 3) + up(8 * 3 * 64)
     # kernel chain: mask, lists, counts, row scratch, hidden tensor of the widest block
     need = lib.dynconv_stack_workspace_bytes(s, blocks, 3, 1, 2)
     assert need == (npos + 4 * npos + 4 * npos + 36 * npos + up(8 * 3) + up(8 * rows)
@@ -152,10 +153,11 @@ def test_stack_validation(lib):
     blk96 = (dc.Block * 1)(fake_block(C=96, E=576))
     assert lib.dynconv_stack_workspace_bytes(c96, blk96, 1, 1, 0) != \
         lib.dynconv_stack_workspace_bytes(c96, blk96, 1, 1, 2)
-    # wide images stay on the one-launch path: patches of 4 rows x 25 columns
+    # wide images stay on the one-launch path: column strips of 25, and for
+    # a batch this small row strips of 1 (16 patches)
     wide = dc.Shape(1, 4, 100, 32)
     assert lib.dynconv_stack_workspace_bytes(wide, blocks, 3, 1, 0) == \
-        up(400 * 32 * 2) + 2 * up(400) + up(8 * 3) + up(8 * 3 * 4)
+        up(400 * 32 * 2) + 2 * up(400) + up(8 * 3) + up(8 * 3 * 16)
     f = lib.dynconv_stack_forward
     assert f(None, FAKE, s, 1, blocks, 3, 0, None, None, FAKE, need, None) == ERR_NULL
     assert f(FAKE, None, s, 1, blocks, 3, 0, None, None, FAKE, need, None) == ERR_NULL

@@ -237,6 +237,38 @@ def test_strided_and_widening_blocks(dtype, nhw, stride, c, co, e):
     assert err <= util.TOL[dtype]
 
 
+@pytest.mark.parametrize("dtype,nhw,stride,c,co,e", [
+    ("bf16", (520, 19, 19), 2, 24, 32, 40),   # 4 output tiles per image (ragged), 2 slices (last partial)
+    ("f16", (108, 30, 33), 1, 64, 64, 144),   # two contraction steps, 4.5 slices, residual
+    ("f16", (128, 56, 56), 2, 16, 24, 96)])   # MobileNetV2's second block at batch 128
+def test_expand_depthwise_one_launch(dtype, nhw, stride, c, co, e):
+    """Ungated blocks with enough 8x8 output tiles run the expansion and the
+    depthwise in one launch (k_expand_dw); against the oracle's dense block."""
+    import oracle.network as onet
+    N, H, W = nhw
+    rng = inputs.rng_for(4400 + c + e)
+    x = inputs.round_to_storage(inputs.blob_features(rng, N, H, W, c), dtype)
+
+    def wgt(*shape):
+        return inputs.round_to_storage(rng.normal(0.0, 0.1, size=shape), dtype)
+
+    L = {"kind": "block", "stride": stride, "acts": (2, 2, 0),
+         "w1": wgt(e, c), "b1": rng.normal(0, 0.1, e).astype(np.float32),
+         "w2": wgt(e, 9), "b2": rng.normal(0, 0.1, e).astype(np.float32),
+         "w3": wgt(co, e), "b3": rng.normal(0, 0.1, co).astype(np.float32)}
+    net = dc.NetworkWeights([L], dc.NAME_TO_DTYPE[dtype])
+    xd = to_dev(x, dtype)
+    out = dc.network_output_shape(dc.shape_of(xd), net)
+    y = torch.empty((out.n, out.h, out.w, out.c), dtype=xd.dtype, device=DEV)
+    names = dc.Network(xd, y, net).launch_names()
+    assert names == ["k_expand_dw", "k_conv1x1"], names
+    yg, _, _ = run_net(x, [L], dtype)
+    want = util.nhwc(onet.dense_block(util.nchw(x), L))
+    err = util.normwise(yg, want)
+    log("  expand+dw %s %s s%d %d->%d (E %d) err %.2e" % (dtype, nhw, stride, c, co, e, err))
+    assert err <= util.TOL[dtype]
+
+
 @pytest.mark.parametrize("dtype", ["f16", "f32"])
 def test_ungated_residual_block(dtype):
     """A stride-1 block of equal widths without a mask unit runs dense and

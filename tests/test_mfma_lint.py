@@ -1,0 +1,47 @@
+"""The build-time MFMA check on small hand-written assembly fragments."""
+from paper_1912_03203_amd import mfma_lint
+
+HEAD = "_ZN7dynconv1kEv:\n"
+
+
+def test_early_read_is_reported():
+    asm = HEAD + """
+	v_mfma_f32_16x16x32_f16 v[0:3], v[4:7], v[8:11], v[0:3]
+	v_add_f32_e32 v12, v1, v13
+"""
+    found = mfma_lint.check(asm)
+    assert len(found) == 1 and "after 0 states" in found[0]
+
+
+def test_enough_states_are_clean():
+    asm = HEAD + """
+	v_mfma_f32_16x16x32_f16 v[0:3], v[4:7], v[8:11], v[0:3]
+	s_nop 7
+	v_add_f32_e32 v12, v1, v13
+"""
+    assert mfma_lint.check(asm) == []
+
+
+def test_accumulator_chaining_is_clean_and_ab_read_is_reported():
+    chain = HEAD + """
+	v_mfma_f32_16x16x32_f16 v[0:3], v[4:7], v[8:11], v[0:3]
+	v_mfma_f32_16x16x32_f16 v[0:3], v[14:17], v[18:21], v[0:3]
+	s_nop 7
+	global_store_dwordx4 v[30:31], v[0:3], off
+"""
+    assert mfma_lint.check(chain) == []
+    ab = HEAD + """
+	v_mfma_f32_16x16x32_f16 v[0:3], v[4:7], v[8:11], v[0:3]
+	v_mfma_f32_16x16x32_f16 v[20:23], v[0:3], v[8:11], v[20:23]
+"""
+    assert any("A/B operand" in f for f in mfma_lint.check(ab))
+
+
+def test_store_of_result_counts_as_a_read():
+    asm = HEAD + """
+	v_mfma_f32_16x16x32_f16 v[0:3], v[4:7], v[8:11], v[0:3]
+	v_mov_b32_e32 v40, 0
+	global_store_dwordx4 v[30:31], v[0:3], off
+"""
+    found = mfma_lint.check(asm)
+    assert len(found) == 1 and "after 1 states" in found[0]
