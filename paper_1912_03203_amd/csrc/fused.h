@@ -510,13 +510,12 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
                         floatx4 d = binit[m];
 #pragma unroll
                         for (int ks = 0; ks < MAXKS; ++ks) d = M::run(a1[m][ks], bx[j][ks], d);
-                        const int e0 = ec * kChunk + m * 16 + 4 * g;
                         float o[4];
 #pragma unroll
                         for (int v = 0; v < 4; ++v) o[v] = clamp_act(d[v], lo1, hi1);
-                        // channels past E go to the spare row
-                        const int q = (e0 < E) ? nq[j] : kRegion;
-                        io<T>::store4(&L.h1r[q][m * 16 + 4 * g], o);
+                        // channels past E have zero weights and bias: they
+                        // store zeros, which the depthwise reads with zero taps
+                        io<T>::store4(&L.h1r[nq[j]][m * 16 + 4 * g], o);
                     }
                 }
             }
@@ -541,11 +540,13 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
             for (int j = 0; j < kActTiles; ++j) {
                 const int t = wave + NW * j;
                 if (t * 16 < n_act) {
+                    // every lane computes: a lane past the active list reads
+                    // around an own slot and its column of the projection is
+                    // never stored (MFMA output columns depend only on their
+                    // own B column); channels past E come out as exact zeros
                     float hv[8];
-#pragma unroll
-                    for (int u = 0; u < 8; ++u) hv[u] = 0.0f;
-                    if (aq[j] >= 0 && ein) {
-                        const char *own = h1base + aq[j] * col_bytes;
+                    {
+                        const char *own = h1base + (aq[j] >= 0 ? aq[j] : WP + 1) * col_bytes;
                         // all nine taps in flight before the first FMA
                         typename io<T>::vec8 tv[9];
 #pragma unroll

@@ -6,7 +6,8 @@ compiled without the wait states that the read needs, which gave wrong and
 non-deterministic results.  The kernels therefore issue every MFMA
 unconditionally, and this check scans the device assembly of each build:
 after every v_mfma it walks the following instructions (counting one state
-per instruction, N + 1 per s_nop N) and reports the first instruction that
+per instruction, N + 1 per s_nop N, up to an unconditional branch) and
+reports the first instruction that
 reads one of the MFMA's destination registers with fewer than MIN_STATES
 states in between, or another MFMA that takes them as its A or B operand
 (its C operand may chain: the hardware forwards it).  It is a heuristic
@@ -57,6 +58,8 @@ def check(asm: str) -> list:
                 continue
             parts = t.split(None, 1)
             op = parts[0]
+            if op in ("s_branch", "s_endpgm", "s_setpc_b64"):
+                break  # the text that follows is not this path's next instruction
             if op.startswith("s_nop"):
                 states += int(parts[1].split()[0], 0) + 1
                 continue

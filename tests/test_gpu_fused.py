@@ -60,6 +60,7 @@ FUSED_CASES = [
     ("c128_bf16_w40", "bf16", (2, 10, 40, 128, 256), 0.3, 14),
     ("c72_f16_h1", "f16", (3, 1, 30, 72, 144), 0.5, 15),
     ("c120_bf16_w1", "bf16", (2, 70, 1, 120, 128), 0.4, 16),
+    ("c128_f16_w23", "f16", (2, 9, 23, 128, 272), 0.3, 18),
 ]
 
 

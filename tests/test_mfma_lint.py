@@ -45,3 +45,20 @@ def test_store_of_result_counts_as_a_read():
 """
     found = mfma_lint.check(asm)
     assert len(found) == 1 and "after 1 states" in found[0]
+
+
+def test_scan_stops_at_an_unconditional_branch():
+    asm = HEAD + """
+	v_mfma_f32_16x16x4_f32 a[0:3], v1, v2, a[0:3]
+	s_branch .LBB0_2
+.LBB0_1:
+	v_accvgpr_read_b32 v51, a3
+"""
+    assert mfma_lint.check(asm) == []
+    fall = HEAD + """
+	v_mfma_f32_16x16x4_f32 a[0:3], v1, v2, a[0:3]
+	s_cbranch_scc1 .LBB0_2
+.LBB0_1:
+	v_accvgpr_read_b32 v51, a3
+"""
+    assert len(mfma_lint.check(fall)) == 1
