@@ -219,7 +219,8 @@ size_t dynconv_stack_workspace_bytes(dynconv_shape s, const dynconv_block *blks,
  * With DYNCONV_STACK_DENSE the mask units are skipped and every block runs on
  * all positions (the baseline of Eq. 1).
  *
- * Execution: when s.c <= 64 and DYNCONV_STACK_UNFUSED is not set, each
+ * Execution: when s.c <= 64 (fp32) or s.c <= 128 (fp16, bf16) and
+ * DYNCONV_STACK_UNFUSED is not set, each
  * block is ONE kernel over small patches of the image (at most 256
  * positions, at most 32 columns wide), each of which builds the active and
  * halo lists of its patch on chip (ballot ranks in raster order), gathers,
@@ -292,10 +293,15 @@ dynconv_status dynconv_stack_forward_profiled(const void *x, void *y, dynconv_sh
  * channels (the caller zero-pads PyTorch's cb-channel weights; since the
  * padded input channels are zero, their weight columns do not matter, and
  * outputs cb .. cp-1 are discarded).  c_hidden is a multiple of 16 (pad
- * with zero weights).  Execution: the branch input is copied into compact
- * cp-channel rows, the branch runs as one gated block (the one-launch kernel
- * when cp <= 64, else the kernel chain), and one kernel writes the shuffled
- * unit output together with the next unit's branch rows.
+ * with zero weights).  Execution: when cp fits the one-launch block kernel
+ * (cp <= 64 in fp32, cp <= 128 in fp16/bf16), cb * sizeof(dtype) is a
+ * multiple of 4 and DYNCONV_STACK_UNFUSED is not set, each unit is ONE
+ * launch on the unit's own rows: it stages the branch half (zero-extended
+ * to cp channels) and the pass-through half, runs the gated block and
+ * writes the shuffled rows.  Otherwise the branch input is copied into
+ * compact cp-channel rows, the branch runs as one gated block (the
+ * one-launch kernel or the kernel chain), and one kernel writes the
+ * shuffled unit output together with the next unit's branch rows.
  *   x, y   (device) NHWC, shape s (s.c even), dtype dt; must not overlap
  *   branches (host array of n_units, device weights), 1 <= n_units <= 1024
  *   flags  0 or DYNCONV_STACK_DENSE (every branch on all positions, no mask
