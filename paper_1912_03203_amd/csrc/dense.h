@@ -359,44 +359,57 @@ k_expand_dw(const T *__restrict__ x, int N, int H, int W, int C, const T *__rest
         int n, i0, j0;
         origin(it, n, i0, j0);
         const int hb = S * i0 - 1, wb = S * j0 - 1;
+        // the item's B fragments (region x) and in-image flags, kept for
+        // every slice; waves past the last tile repeat it (same values), so
+        // every wave issues the same MFMAs
+        Frag bx[TPW][KS];
+        uint32_t inside = 0;
+#pragma unroll
+        for (int jt = 0; jt < TPW; ++jt) {
+            const int t = wave + kWavesPerBlock * jt;
+            const int slot = (t < NT ? t : NT - 1) * 16 + r;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                const int c = ks * 32 + 8 * g;
+                bx[jt][ks] = (c < C) ? *reinterpret_cast<const Frag *>(xs + slot * PX + c) : M::zero();
+            }
+            const int hh = hb + slot / RS, ww = wb + slot % RS;
+            inside |= static_cast<uint32_t>(slot < RP && hh >= 0 && hh < H && ww >= 0 && ww < W) << jt;
+        }
         for (int sl = 0; sl < nsl; ++sl) {
             const int e0 = sl * 32;
-            // expansion of the region tiles; waves past the last tile repeat
-            // it (same values), so every wave issues the same MFMAs
+            // the slice's expansion rows (A) and biases, once per slice
+            Frag a1[2][KS];
+            floatx4 binit[2];
 #pragma unroll
-            for (int jt = 0; jt < TPW; ++jt) {
-                const int t = wave + kWavesPerBlock * jt;
-                const int tt = t < NT ? t : NT - 1;
-                const int slot = tt * 16 + r;
-                Frag bx[KS];
+            for (int m = 0; m < 2; ++m) {
+                const int er = e0 + m * 16 + r;  // A row: hidden channel
 #pragma unroll
                 for (int ks = 0; ks < KS; ++ks) {
                     const int c = ks * 32 + 8 * g;
-                    bx[ks] = (c < C) ? *reinterpret_cast<const Frag *>(xs + slot * PX + c) : M::zero();
+                    a1[m][ks] = (er < E && c < C) ? *reinterpret_cast<const Frag *>(w1s + er * PX + c) : M::zero();
                 }
-                // D[e][slot]: rows are hidden channels, columns region slots
-                const int hh = hb + slot / RS, ww = wb + slot % RS;
-                const bool inside = slot < RP && hh >= 0 && hh < H && ww >= 0 && ww < W;
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const int e = e0 + m * 16 + 4 * g + v;
+                    binit[m][v] = (e < E) ? b1s[e] : 0.0f;
+                }
+            }
+            // D[e][slot]: rows are hidden channels, columns region slots
+#pragma unroll
+            for (int jt = 0; jt < TPW; ++jt) {
+                const int t = wave + kWavesPerBlock * jt;
+                const int slot = (t < NT ? t : NT - 1) * 16 + r;
+                const bool in = (inside >> jt) & 1u;
 #pragma unroll
                 for (int m = 0; m < 2; ++m) {
-                    const int er = e0 + m * 16 + r;  // A row: hidden channel
-                    floatx4 d;
+                    floatx4 d = binit[m];
 #pragma unroll
-                    for (int v = 0; v < 4; ++v) {
-                        const int e = e0 + m * 16 + 4 * g + v;
-                        d[v] = (e < E) ? b1s[e] : 0.0f;
-                    }
-#pragma unroll
-                    for (int ks = 0; ks < KS; ++ks) {
-                        const int c = ks * 32 + 8 * g;
-                        const Frag a = (er < E && c < C) ? *reinterpret_cast<const Frag *>(w1s + er * PX + c)
-                                                         : M::zero();
-                        d = M::run(a, bx[ks], d);
-                    }
+                    for (int ks = 0; ks < KS; ++ks) d = M::run(a1[m][ks], bx[jt][ks], d);
                     if (t < NT) {
                         float o[4];
 #pragma unroll
-                        for (int v = 0; v < 4; ++v) o[v] = inside ? clamp_act(d[v], lo1, hi1) : 0.0f;
+                        for (int v = 0; v < 4; ++v) o[v] = in ? clamp_act(d[v], lo1, hi1) : 0.0f;
                         io<T>::store4(h1 + slot * HP + m * 16 + 4 * g, o);
                     }
                 }

@@ -916,12 +916,10 @@ void launch_conv3x3(const void *x, dynconv_shape in, dynconv_shape out, const dy
 
 // Expansion + depthwise in one launch (ungated blocks): 16-bit storage, at
 // most 64 input channels, LDS within 64 KB, and at least kEdMinItems 8x8
-// output tiles.  Its VALU overhead per tile (region bookkeeping, the
-// activation and packing of every expanded slice) makes it pay only where
-// the expanded tensor is large (MobileNetV2's 112x112x96 at batch 64 saves
-// about 26 us; 56x56x144 breaks even), so smaller layers keep the
-// two-kernel path.
-constexpr int64_t kEdMinItems = 2048;
+// output tiles (below that too few workgroups share the work; MobileNetV2
+// at batch 64: 112x112x16 -> 96 and 56x56x24 -> 144 qualify, 62 against 100
+// us and 38 against 41 us with the projection).
+constexpr int64_t kEdMinItems = 1024;
 
 int64_t ed_items(dynconv_shape out) {
     return static_cast<int64_t>(out.n) * ((out.h + kEdTile - 1) / kEdTile) * ((out.w + kEdTile - 1) / kEdTile);
