@@ -520,4 +520,96 @@ k_conv3x3(const T *__restrict__ x, int N, int H, int W, int Ci, int stride, cons
     }
 }
 
+// ------------------------------------------------ full 3x3 on the matrix cores
+// The same convolution as an implicit-im2col contraction for 16-bit
+// storage: the contraction index runs over (tap, input channel) pairs,
+// kk = k * Ci + c with tap k = 3 kh + kw, zero-padded to KS steps of 32.
+// Outputs run along M, output positions along N: lane (r, g) gathers the 8
+// input values kk = 32 ks + 8 g .. +7 of its position r (zeros outside the
+// image and past 9 Ci) straight into its B fragment, the weights sit in LDS
+// as [O][32 KS + 8] rows in kk order, and the wave walks the outputs in
+// ranges of OT tiles of 16.  Accumulation from the bias in kk order (32 at a
+// time on the matrix core); the taps' (dh, dw, c) per kk come from a small
+// LDS table.  Dynamic shared memory: O (32 KS + 8) elements + 32 KS ints.
+template <typename T, int KS, int OT>
+__global__ void __launch_bounds__(kBlock)
+k_conv3x3_mfma(const T *__restrict__ x, int N, int H, int W, int Ci, int stride, const T *__restrict__ w,
+               const float *__restrict__ b, int O, int act, T *__restrict__ y, int Ho, int Wo) {
+    typedef mma<T> M;
+    typedef typename M::frag Frag;
+    constexpr int KP = KS * 32 + 8;  // LDS row pitch of the weights
+    extern __shared__ __align__(16) unsigned char c3_smem[];
+    T *ws = reinterpret_cast<T *>(c3_smem);         // [O][KP]
+    int *tap = reinterpret_cast<int *>(ws + O * KP);  // [32 KS]: (dh+1) | (dw+1) << 2 | c << 4, -1 past 9 Ci
+    const int K = 9 * Ci;
+    for (int i = threadIdx.x; i < O * KP; i += kBlock) {
+        const int o = i / KP, kk = i % KP;
+        ws[i] = (kk < K) ? w[(o * Ci + kk % Ci) * 9 + kk / Ci] : static_cast<T>(0.0f);
+    }
+    for (int kk = threadIdx.x; kk < 32 * KS; kk += kBlock) {
+        const int k = kk / Ci, c = kk % Ci;
+        tap[kk] = (kk < K) ? ((k / 3) | ((k % 3) << 2) | (c << 4)) : -1;
+    }
+    __syncthreads();
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int r = lane % 16, g = lane / 16;
+    const float lo = act_lo(act), hi = act_hi(act);
+    const int64_t total = static_cast<int64_t>(N) * Ho * Wo;
+    const int64_t tiles = (total + 63) / 64;
+    const int nmt = (O + 15) / 16;
+    for (int64_t t = blockIdx.x; t < tiles; t += gridDim.x) {
+        const int64_t q = t * 64 + wave * 16 + r;  // this lane's output position (B column)
+        const bool qin = q < total;
+        const int64_t qq = qin ? q : 0;
+        const int64_t ni = qq / Wo;
+        const int j = static_cast<int>(qq - ni * Wo);
+        const int n = static_cast<int>(ni / Ho), i = static_cast<int>(ni - static_cast<int64_t>(n) * Ho);
+        const int h0 = stride * i - 1, w0 = stride * j - 1;
+        const T *img = x + static_cast<int64_t>(n) * H * W * Ci;
+        Frag bx[KS];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            float v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const int e = tap[ks * 32 + 8 * g + u];
+                const int hh = h0 + (e & 3), ww = w0 + ((e >> 2) & 3), c = e >> 4;
+                v[u] = (qin && e >= 0 && hh >= 0 && hh < H && ww >= 0 && ww < W)
+                           ? static_cast<float>(img[(static_cast<int64_t>(hh) * W + ww) * Ci + c])
+                           : 0.0f;
+            }
+            bx[ks] = M::pack(v);
+        }
+        for (int ob = 0; ob < nmt; ob += OT) {
+            floatx4 acc[OT];
+#pragma unroll
+            for (int mt = 0; mt < OT; ++mt) {
+                const int o0 = (ob + mt) * 16 + 4 * g;
+#pragma unroll
+                for (int v = 0; v < 4; ++v) acc[mt][v] = (o0 + v < O) ? b[o0 + v] : 0.0f;
+            }
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+                for (int mt = 0; mt < OT; ++mt) {
+                    const int o = (ob + mt) * 16 + r;
+                    const Frag a = (o < O) ? *reinterpret_cast<const Frag *>(ws + o * KP + ks * 32 + 8 * g)
+                                           : M::zero();
+                    acc[mt] = M::run(a, bx[ks], acc[mt]);
+                }
+            }
+#pragma unroll
+            for (int mt = 0; mt < OT; ++mt) {
+                const int o0 = (ob + mt) * 16 + 4 * g;
+                if (qin && o0 < O) {  // O is a multiple of 8: all four outputs exist
+                    float out[4];
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) out[v] = clamp_act(acc[mt][v], lo, hi);
+                    io<T>::store4(y + q * O + o0, out);
+                }
+            }
+        }
+    }
+}
+
 }  // namespace dynconv

@@ -905,9 +905,42 @@ void launch_dwconv(const void *x, dynconv_shape in, dynconv_shape out, int C, in
     else launch_dwconv_s<T, 2>(x, in, out, C, w, b, act, y, st, mk);
 }
 
+template <typename T, int KS, int OT>
+void launch_conv3x3_mfma(const void *x, dynconv_shape in, dynconv_shape out, const dynconv_layer &L, void *y,
+                         hipStream_t st, Marks &mk) {
+    const size_t lds = static_cast<size_t>(L.c_out) * (KS * 32 + 8) * sizeof(T) + 4 * 32 * KS;
+    int64_t grid = (positions(out) + 63) / 64;
+    if (grid > 8192) grid = 8192;
+    if (grid < 1) grid = 1;
+    launch(mk, k_conv3x3_mfma<T, KS, OT>, dim3(static_cast<unsigned>(grid)), dim3(kBlock), lds, st,
+           static_cast<const T *>(x), in.n, in.h, in.w, L.c_in, L.stride, static_cast<const T *>(L.w), L.b,
+           L.c_out, L.act, static_cast<T *>(y), out.h, out.w);
+}
+
+// 16-bit storage: the matrix-core form when its weights fit 64 KB of LDS;
+// fp32 (and wider layers): one lane per position on the VALU.
 template <typename T>
 void launch_conv3x3(const void *x, dynconv_shape in, dynconv_shape out, const dynconv_layer &L, void *y,
                     hipStream_t st, Marks &mk) {
+    const int ks = (9 * L.c_in + 31) / 32;
+    if constexpr (sizeof(T) == 2) {
+        const size_t lds = static_cast<size_t>(L.c_out) * (ks * 32 + 8) * sizeof(T) + 4 * 32 * ks;
+        if (lds <= kMaxDynLds) {
+            const bool wide = L.c_out > 32;
+#define DC_C3(KS)                                                                         \
+    (wide ? launch_conv3x3_mfma<T, KS, 4>(x, in, out, L, y, st, mk)                      \
+          : launch_conv3x3_mfma<T, KS, 2>(x, in, out, L, y, st, mk))
+            switch (ks) {
+            case 1: DC_C3(1); return;
+            case 2: DC_C3(2); return;
+            case 3: DC_C3(3); return;
+            case 4: DC_C3(4); return;
+            case 5: DC_C3(5); return;
+            default: break;
+            }
+#undef DC_C3
+        }
+    }
     const size_t lds = 4 * (9 * L.c_in * L.c_out + L.c_out);
     launch(mk, k_conv3x3<T>, dim3(elem_grid(positions(out))), dim3(kBlock), lds, st,
            static_cast<const T *>(x), in.n, in.h, in.w, L.c_in, L.stride, static_cast<const T *>(L.w), L.b,

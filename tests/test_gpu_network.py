@@ -289,11 +289,13 @@ def test_ungated_residual_block(dtype):
 
 @pytest.mark.parametrize("dtype,nhw,ci,co,stride", [
     ("f16", (2, 17, 23), 3, 32, 2), ("bf16", (1, 9, 8), 16, 40, 1), ("f32", (3, 5, 7), 1, 8, 2),
-    ("f16", (1, 1, 1), 4, 72, 1), ("f16", (2, 30, 3), 8, 200, 2)])
+    ("f16", (1, 1, 1), 4, 72, 1), ("f16", (2, 30, 3), 8, 200, 2), ("bf16", (3, 31, 29), 7, 8, 2),
+    ("f16", (2, 40, 37), 11, 24, 1)])
 def test_full_conv3x3_layer(dtype, nhw, ci, co, stride):
     """A network of one full 3x3 convolution (the stem's kind) against the
     oracle's conv3x3: odd sizes, both strides, output counts that are not
-    multiples of 32."""
+    multiples of 32, 1-16 input channels (1-5 contraction steps of 32 on the
+    matrix cores in 16-bit storage; fp32 on the VALU)."""
     import oracle.network as onet
     N, H, W = nhw
     rng = inputs.rng_for(4300 + ci + co)
