@@ -212,7 +212,8 @@ void launch_dw_project_k(const void *h1, const void *x, void *y, dynconv_shape s
     const int64_t g = groups < kMaxDwGrid ? (groups < 1 ? 1 : groups) : kMaxDwGrid;
     // whole groups of 8 (one per XCD), each slot with all its output slabs
     const int grid = static_cast<int>((g + 7) / 8 * 8 * nos);
-    launch(mk, k_dw_project<T, DENSE, MAXMT>, dim3(grid), dim3(kBlock), dw_lds_bytes<T>(),
+    auto kern = nos > 1 ? k_dw_project<T, DENSE, MAXMT, true> : k_dw_project<T, DENSE, MAXMT, false>;
+    launch(mk, kern, dim3(grid), dim3(kBlock), dw_lds_bytes<T>(),
                        st, static_cast<const T *>(h1), static_cast<const T *>(x), static_cast<T *>(y),
                        s.n, s.h, s.w, s.c, b->c_hidden, static_cast<const T *>(b->w_dw), b->b_dw,
                        b->act_dw, static_cast<const T *>(b->w_project), b->b_project, b->act_project,

@@ -548,7 +548,7 @@ k_expand(const T *__restrict__ x, int C, int E, const T *__restrict__ w1,
 // starting from the projection bias, and the epilogue adds the identity path
 // and writes y at the active position (in place when y == x).  Hidden slices
 // pass through LDS in chunks of kDwChunk.
-// The output channels are cut into nos slabs of MAXMT 16-row tiles; a work
+// With SLABS the output channels are cut into nos slabs of MAXMT 16-row tiles; a work
 // item is (group, slab).  Every slab of a group recomputes the group's
 // depthwise (identical values) and projects onto its own output rows, so
 // small images with many channels (7x7x160, 960 hidden) still spread over
@@ -566,13 +566,13 @@ __host__ __device__ constexpr size_t dw_lds_bytes() {
            + static_cast<size_t>(kDwGroup) * 16 * 10 * 4;                 // positions + neighbour rows
 }
 
-template <typename T, bool DENSE, int MAXMT>
+template <typename T, bool DENSE, int MAXMT, bool SLABS>
 __global__ void __launch_bounds__(kBlock)
 k_dw_project(const T *__restrict__ h1, const T *x, T *y, int N, int H, int W, int C, int E,
              const T *__restrict__ w2, const float *__restrict__ b2, int act2,
              const T *__restrict__ w3, const float *__restrict__ b3, int act3,
              const int32_t *__restrict__ act_list, const int32_t *__restrict__ nbr,
-             const int32_t *__restrict__ counts, int nos) {
+             const int32_t *__restrict__ counts, int nos_arg) {
     typedef mma<T> M;
     typedef typename M::frag Frag;
     extern __shared__ __align__(16) unsigned char dw_lds[];
@@ -583,7 +583,10 @@ k_dw_project(const T *__restrict__ h1, const T *x, T *y, int N, int H, int W, in
     constexpr int GR = kDwGroup * 16;  // rows per group
     const int64_t ngroups = (nrows + GR - 1) / GR;
     // workgroup b: XCD b % 8, output slab (b / 8) % nos, group slot (b / 8) / nos
-    const int os = static_cast<int>((blockIdx.x / 8) % nos);
+    // (without SLABS one slab: the register budget of the common case stays
+    // that of a kernel without slab arithmetic)
+    const int nos = SLABS ? nos_arg : 1;
+    const int os = SLABS ? static_cast<int>((blockIdx.x / 8) % nos) : 0;
     const int mt0 = os * MAXMT;  // first output tile of the slab
     if ((blockIdx.x / 8) / nos >= (ngroups + 7) / 8) return;  // no group on this slot (uniform)
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
