@@ -178,6 +178,41 @@ def test_gated_network_end_to_end(net_f16):
     assert err <= util.TOL["f16"]
 
 
+def test_gated_network_full_batch_sampled_images():
+    """The benchmark's launch configuration: the gated network on the 64-image
+    batch (224x224x3, fp16), with mask biases set by the oracle on images 0
+    and 63.  Images are independent, so those two images are checked as in
+    test_gated_network_end_to_end against the oracle run on them alone."""
+    import oracle
+    x, layers, dens = inputs.make_network_inputs(0, 64, 224, 224, dtype="f16")
+    pick = [0, 63]
+    xs = np.ascontiguousarray(x[pick])
+    biases = oracle_biases(xs, layers, dens, "f16")
+    y, m, _ = run_net(x, layers, "f16", biases=biases, masks=True)
+    rnd = rounder("f16")
+    cur = util.nchw(xs).astype(np.float64)
+    off, gi, flips = 0, 0, []
+    for L in layers:
+        if L.get("gated"):
+            _, _, H, W = cur.shape
+            hw = H * W
+            G = np.concatenate([m[off + i * hw: off + (i + 1) * hw] for i in pick])
+            off += 64 * hw
+            Go, mo = oracle.mask(cur.astype(np.float32), L["w_m"], biases[gi])
+            d = G != Go
+            envelope = np.abs(L["w_m"]).sum() * util.TOL["f16"] * np.abs(cur).max()
+            assert (np.abs(mo[d]) <= envelope).all(), "gated block %d" % gi
+            flips.append(int(d.sum()))
+            cur = rnd(oracle.block_dense(cur, L, G)[0])
+            gi += 1
+        else:
+            cur, _ = oracle.network_forward(cur, [L], None, round_to=rnd)
+    log("  decisions differing from the oracle's own, per gated block: %s" % flips)
+    err = util.normwise(y[pick], util.nhwc(cur))
+    log("  images 0 and 63 of the gated 64-image batch vs forced-mask oracle: err %.2e" % err)
+    assert err <= util.TOL["f16"]
+
+
 POINTWISE_CASES = [
     # dtype, (N, H, W), C, O: every output-range width (2..12 tiles of 16),
     # contraction chunks of 1..8 steps of 32 and several chunks, one partial
