@@ -14,8 +14,10 @@
  * * Pointers marked (device) must be device memory of the current HIP device;
  *   (host) pointers are read during the call only.  The library allocates and
  *   frees nothing: every buffer, including the workspace, belongs to the
- *   caller.  It keeps no global state, so calls on different streams may run
- *   concurrently as long as their buffers are disjoint.
+ *   caller.  Its only global state is a cache of device occupancy figures
+ *   (workgroups the device holds at once, per kernel; written once, read
+ *   atomically), so calls on different streams may run concurrently as long
+ *   as their buffers are disjoint.
  * * Every call validates all of its arguments on the host first.  On any
  *   error it returns a nonzero status and enqueues nothing.  Otherwise the
  *   work is enqueued asynchronously on `stream` (a hipStream_t; NULL is the
