@@ -227,7 +227,7 @@ struct DwProjStager {
             if (j < kTaps && e_base + j / 9 < E) t[sl] = w2[static_cast<int64_t>(e_base) * 9 + j];
         }
     }
-    __device__ __forceinline__ void store(DwProjWeights<T, MAXC> &dst, int C, int E, int ec, int tid) const {
+    __device__ __forceinline__ void store(DwProjWeights<T, MAXC> &dst, int C, int tid) const {
         const int n3 = C * kChunk / kPer16;
 #pragma unroll
         for (int sl = 0; sl < kSlots; ++sl) {
@@ -487,7 +487,7 @@ k_block_fused(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
             // ---- 3a. expansion of this slice into the region array; meanwhile
             // this slice's depthwise/projection weights go to LDS and the next
             // slice's are requested
-            stB.store(L.wd, C, E, ec, tid);
+            stB.store(L.wd, C, tid);
             if (ec + 1 < nchunks) stB.load(w2, w3, b2, C, E, ec + 1, tid);
             typename M::frag a1[2][MAXKS];
             floatx4 binit[2];
@@ -656,7 +656,7 @@ k_band_counts(const int32_t *__restrict__ band_counts, int nbands, int32_t *__re
     part[threadIdx.x] = acc;
     __syncthreads();
     for (int off = kBlock / 2; off > 0; off >>= 1) {
-        if (threadIdx.x < off) {
+        if (static_cast<int>(threadIdx.x) < off) {
             part[threadIdx.x].x += part[threadIdx.x + off].x;
             part[threadIdx.x].y += part[threadIdx.x + off].y;
         }
