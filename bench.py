@@ -773,13 +773,15 @@ def summarize_traffic(args):
         "%d bytes each way, the sparse stack, the dense stack, 3 times each). Each counter is scaled "
         "by the ratio of the copy's known size to what the counter reads for it." % copy_bytes,
         "",
+        "Commands ($REPO: the repository root; $OUT: any output directory):",
+        "",
         "```",
         "cd /tmp && export TMPDIR=/tmp && timeout -s KILL 120 rocprofv3 --pmc FETCH_SIZE --output-format csv "
-        "-d $REPO/gpurun_out/traffic_fetch -o run -- python3 $REPO/bench.py --traffic-pass",
+        "-d $OUT/traffic_fetch -o run -- python3 $REPO/bench.py --traffic-pass",
         "cd /tmp && export TMPDIR=/tmp && timeout -s KILL 120 rocprofv3 --pmc WRITE_SIZE --output-format csv "
-        "-d $REPO/gpurun_out/traffic_write -o run -- python3 $REPO/bench.py --traffic-pass",
-        "python3 bench.py --summarize-traffic gpurun_out/traffic_fetch/run_counter_collection.csv "
-        "gpurun_out/traffic_write/run_counter_collection.csv",
+        "-d $OUT/traffic_write -o run -- python3 $REPO/bench.py --traffic-pass",
+        "python3 $REPO/bench.py --summarize-traffic $OUT/traffic_fetch/run_counter_collection.csv "
+        "$OUT/traffic_write/run_counter_collection.csv",
         "```",
         "",
         "| dispatches | n | FETCH_SIZE KiB | WRITE_SIZE KiB | scaled bytes |",
