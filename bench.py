@@ -23,6 +23,12 @@ Also reported on the same JSON line:
                 bounded sample of the same workload
   sweep         per-block latency of the 32 x 56x56x24 (hidden 144) fp16 block
                 at densities 0.1 .. 0.9, sparse and dense
+  sweep_pose_stack
+                the 8-block pose stack at densities 0.1 .. 0.9 and at per-block
+                densities ~ U[0.2, 0.4] (seed 1)
+  sweep_parity_block_fp32
+                the 1 x 32x32x32 (hidden 192) fp32 block at density 0.5
+                (launch-bound)
   chain         the same stack through the kernel chain (the per-block calls'
                 kernels), sparse and dense, with per-kernel HBM fractions
   shufflenet    ShuffleNetV2 stride-1 units (gated branch) at 64 x 28x28x116 and
@@ -123,8 +129,9 @@ class HipEvents:
 
 # ------------------------------------------------------------------ setup
 def calibrate(dc, inputs, torch, x0_dev, blocks_np, dt, density):
-    """Per-block mask bias for the target density, from the library's own
-    bias-free logits of each block's input (offline, before timing)."""
+    """Per-block mask bias for the target density (one value, or one per
+    block), from the library's own bias-free logits of each block's input
+    (offline, before timing)."""
     n, h, w, c = x0_dev.shape
     npos = n * h * w
     shape = dc.shape_of(x0_dev)
@@ -137,7 +144,8 @@ def calibrate(dc, inputs, torch, x0_dev, blocks_np, dt, density):
         blk = dc.BlockWeights.from_arrays(wts, dt, device=x.device)
         dc.mask(x, blk.w_mask, 0.0, logits=logits)
         torch.cuda.synchronize()
-        blk.b_mask = float(inputs.percentile_bias(logits.cpu().numpy(), density))
+        d = density[len(out)] if isinstance(density, (list, tuple)) else density
+        blk.b_mask = float(inputs.percentile_bias(logits.cpu().numpy(), d))
         m = dc.mask(x, blk.w_mask, blk.b_mask)
         dc.build_indices(m, shape, 1, idx, ws_i)
         ws = torch.empty(dc.block_workspace_bytes(shape, blk, dt), dtype=torch.uint8, device=x.device)
@@ -448,23 +456,28 @@ def mask_variants(dc, torch, wl, x0, sparse_blocks, t_gbinary, use_graph, steps,
     return out
 
 
-def density_sweep(dc, inputs, torch, steps, warmup, use_graph, flags):
-    wl = inputs.WORKLOADS["mbv2_stage2_block_56x56x24_f16"]
+def density_sweep(dc, inputs, torch, steps, warmup, use_graph, flags,
+                  workload="mbv2_stage2_block_56x56x24_f16", densities=None):
+    """Step time of a stack at each density (one value for every block, or a
+    tuple with one value per block), against the same stack dense."""
+    wl = inputs.WORKLOADS[workload]
     x_np, blocks_np, _ = inputs.make_block_inputs(wl, 0)
     dt = dc.NAME_TO_DTYPE[wl.dtype]
     x0 = torch.from_numpy(x_np).cuda().to(dt)
-    dense_blk = [dc.BlockWeights.from_arrays(blocks_np[0], dt)]
-    dense_t = Runner(dc, torch, x0, dense_blk, flags | dc.STACK_DENSE, use_graph, 1).timed(steps, warmup)
+    dense_blk = [dc.BlockWeights.from_arrays(b, dt) for b in blocks_np]
+    dense_t = Runner(dc, torch, x0, dense_blk, flags | dc.STACK_DENSE, use_graph, wl.blocks).timed(steps, warmup)
     rows = []
-    for d in wl.densities:
+    for d in (wl.densities if densities is None else densities):
         blks = calibrate(dc, inputs, torch, x0, blocks_np, dt, d)
-        r = Runner(dc, torch, x0, blks, flags, use_graph, 1)
+        r = Runner(dc, torch, x0, blks, flags, use_graph, wl.blocks)
         t = r.timed(steps, warmup)
-        P, Pd = (int(v) for v in r.read_counts()[0].cpu())
-        rows.append({"density": d, "active_frac": P / wl.nhw, "dilated_frac": Pd / wl.nhw,
+        counts = r.read_counts().cpu().numpy()
+        rows.append({"density": list(d) if isinstance(d, tuple) else d,
+                     "active_frac": [float(c[0]) / wl.nhw for c in counts],
+                     "dilated_frac": [float(c[1]) / wl.nhw for c in counts],
                      "sparse_us": 1e6 * t, "dense_us": 1e6 * dense_t, "speedup": dense_t / t,
-                     "sparse_images_per_s": wl.n / t})
-    return {"workload": wl.name, "rows": rows}
+                     "sparse_images_per_s": wl.n / t, "dense_images_per_s": wl.n / dense_t})
+    return {"workload": wl.name, "blocks": wl.blocks, "rows": rows}
 
 
 def calibrate_shuffle(dc, inputs, torch, x0_dev, branches_np, dt, density):
@@ -966,8 +979,14 @@ def main():
                                                  use_graph, args.profile_steps)
     if not args.no_sweep:
         log("density sweep")
-        result["sweep"] = density_sweep(dc, inputs, torch, min(args.steps, 100), min(args.warmup, 10),
-                                        use_graph, base_flags)
+        sw_steps, sw_warm = min(args.steps, 100), min(args.warmup, 10)
+        result["sweep"] = density_sweep(dc, inputs, torch, sw_steps, sw_warm, use_graph, base_flags)
+        pose_d = (0.1, 0.25, 0.5, 0.75, 0.9)
+        mixed = tuple(float(v) for v in np.random.default_rng(1).uniform(0.2, 0.4, size=wl.blocks))
+        result["sweep_pose_stack"] = density_sweep(dc, inputs, torch, sw_steps, sw_warm, use_graph, base_flags,
+                                                   "pose_stack8_64x64x32_f16", pose_d + (mixed,))
+        result["sweep_parity_block_fp32"] = density_sweep(dc, inputs, torch, sw_steps, sw_warm, use_graph,
+                                                          base_flags, "mbv2_block_32x32x32_f32")
     if not args.no_cpu:
         log("cpu baseline (oracle)")
         result["cpu_baseline"] = cpu_baseline(inputs, wl, x_np, blocks_np, args.density)
