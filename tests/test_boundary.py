@@ -263,3 +263,57 @@ def test_shuffle_stack_validation_and_plans(lib):
         "k_shuffle_split", "k_expand", "k_dw_project", "k_shuffle_merge", "k_expand", "k_dw_project",
         "k_shuffle_merge"]
     assert lib.dynconv_shuffle_stack_launch_names(s, br, 0, 2, 0, None, 0) == -1
+
+
+def net_layers(over=None):
+    """stem 3x3 s2 (3 -> 32), an ungated block s2 (32 -> 24, hidden 96), a
+    1x1 (24 -> 64); overrides as {(layer index, field): value}."""
+    stem = dc.Layer(dc.LAYER_CONV3X3, 2, 0, 3, 32, FAKE, FAKE, 2)
+    blk = dc.Layer(dc.LAYER_BLOCK, 2, 0, 0, 0, 0, 0, 0, fake_block(C=32, E=96, Co=24, w_mask=None))
+    last = dc.Layer(dc.LAYER_CONV1X1, 1, 0, 24, 64, FAKE, FAKE, 2)
+    arr = (dc.Layer * 3)(stem, blk, last)
+    for (i, field), v in (over or {}).items():
+        if field.startswith("blk."):
+            setattr(arr[i].blk, field[4:], v)
+        else:
+            setattr(arr[i], field, v)
+    return arr
+
+
+def test_network_validation(lib):
+    s = dc.Shape(2, 9, 11, 3)
+    out = dc.Shape()
+
+    def shape(arr, n=3, sh=s):
+        return lib.dynconv_network_output_shape(sh, arr, n, ctypes.byref(out))
+
+    assert shape(net_layers()) == OK
+    assert (out.n, out.h, out.w, out.c) == (2, 3, 3, 64)  # (9-1)//2+1 = 5 -> 3; 11 -> 6 -> 3
+    assert lib.dynconv_network_workspace_bytes(s, net_layers(), 3, 1, 0) > 0
+    cap = 16
+    names = (ctypes.c_char_p * cap)()
+    n = lib.dynconv_network_launch_names(s, net_layers(), 3, 1, 0, 0, names, cap)
+    assert [names[i].decode() for i in range(n)] == ["k_conv3x3", "k_conv1x1", "k_dwconv3x3", "k_conv1x1",
+                                                     "k_conv1x1"]
+    # widths, strides, kinds, activations and pointers are checked layer by layer
+    assert shape(net_layers({(0, "c_in"): 17}), sh=dc.Shape(2, 9, 11, 17)) == ERR_SHAPE
+    assert shape(net_layers({(0, "c_out"): 36})) == ERR_UNSUPPORTED
+    assert shape(net_layers({(0, "stride"): 3})) == ERR_ARG
+    assert shape(net_layers({(0, "act"): 3})) == ERR_ARG
+    assert shape(net_layers({(0, "w"): None})) == ERR_NULL
+    assert shape(net_layers({(1, "blk.c_in"): 24})) == ERR_SHAPE
+    assert shape(net_layers({(1, "blk.c_hidden"): 1800})) == ERR_UNSUPPORTED
+    assert shape(net_layers({(1, "gated"): 1})) == ERR_UNSUPPORTED   # gated needs stride 1, equal widths
+    assert shape(net_layers({(1, "kind"): 7})) == ERR_ARG
+    assert shape(net_layers({(2, "c_in"): 32})) == ERR_SHAPE
+    assert shape(net_layers({(2, "c_out"): 4104})) == ERR_UNSUPPORTED
+    assert shape(net_layers({(2, "w"): FAKE + 8})) == ERR_ALIGN
+    assert shape(net_layers(), n=0) == ERR_ARG
+    assert lib.dynconv_network_workspace_bytes(s, net_layers({(0, "stride"): 3}), 3, 1, 0) == 0
+    assert lib.dynconv_network_launch_names(s, net_layers(), 3, 1, 8, 0, None, 0) == -1
+    f = lib.dynconv_network_forward
+    need = lib.dynconv_network_workspace_bytes(s, net_layers(), 3, 1, 0)
+    assert f(FAKE, FAKE + (1 << 30), s, 1, net_layers(), 3, 0, None, None, FAKE, need - 1, None) == ERR_WORKSPACE
+    assert f(FAKE, FAKE, s, 1, net_layers(), 3, 0, None, None, FAKE, need, None) == ERR_SHAPE  # y overlaps x
+    assert f(None, FAKE, s, 1, net_layers(), 3, 0, None, None, FAKE, need, None) == ERR_NULL
+    assert f(FAKE, FAKE + (1 << 30), s, 5, net_layers(), 3, 0, None, None, FAKE, need, None) == ERR_DTYPE
