@@ -838,6 +838,8 @@ def main():
                          "then the sparse and the dense stack")
     ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write the traffic summary from the counter CSVs of two --traffic-pass runs")
+    ap.add_argument("--section", choices=("network", "shufflenet"),
+                    help="run only this report (for a kernel trace of it) and print its JSON object")
     args = ap.parse_args()
     if args.summarize_traffic:
         summarize_traffic(args)
@@ -858,6 +860,11 @@ def main():
         print("no GPU visible", file=sys.stderr)
         sys.exit(1)
     dc.load()
+    if args.section:
+        report = network_report if args.section == "network" else shufflenet_report
+        print(json.dumps({args.section: report(dc, inputs, torch, args.steps, args.warmup, not args.no_graph,
+                                               args.profile_steps)}))
+        return
     wl = inputs.WORKLOADS[args.workload]
     dt = dc.NAME_TO_DTYPE[wl.dtype]
     use_graph = not args.no_graph
