@@ -41,6 +41,9 @@ Also reported on the same JSON line:
   mask_variants the stack with G-Softmax mask units against G-Binary ones
   network       a whole MobileNetV2 (64 x 224x224x3 -> 7x7x1280, fp16) with its 10
                 stride-1 residual blocks gated, densities ~ U[0.2, 0.6], and dense
+  pose_network  the pose network end to end (32 x 256x256x3 ellipse images: a
+                MobileNetV2 backbone to 64x64x32, then the 8 stacked blocks; 9
+                gated blocks, densities ~ U[0.2, 0.4]), and dense
   bandwidth_probes
                 the chain's mask / gather+expand / depthwise+scatter kernels and
                 the one-launch block at batches moving >= 512 MB per kernel,
@@ -568,14 +571,23 @@ def shufflenet_report(dc, inputs, torch, steps, warmup, use_graph, profile_steps
     return rows
 
 
-def calibrate_network(dc, inputs, torch, x0, layers, dens, dt):
+def calibrate_network(dc, inputs, torch, x0, layers, dens, dt, labels=None):
     """Mask bias of every gated block of a whole network for its target
     density, from the library's bias-free logits of the block's input, the
-    layers run one after another (offline, before timing)."""
+    layers run one after another (offline, before timing).  With person
+    labels (the pose network), each gated block's mask weights are first set
+    to point from the background to the people in its own input features
+    (ellipse_mask_weights on the labels subsampled to its resolution)."""
     cur = x0
     biases = []
     gi = 0
+    rng = np.random.default_rng(11)
     for L in layers:
+        if L.get("gated") and labels is not None:
+            n, h, w, c = cur.shape
+            step = labels.shape[1] // h
+            lab = np.ascontiguousarray(labels[:, ::step, ::step][:, :h, :w])
+            L["w_m"] = inputs.ellipse_mask_weights(rng, cur.float().cpu().numpy(), lab, 1)[0]
         one = dc.NetworkWeights([L], dt, biases=[0.0] if L.get("gated") else None)
         if L.get("gated"):
             n, h, w, c = cur.shape
@@ -595,15 +607,26 @@ def calibrate_network(dc, inputs, torch, x0, layers, dens, dt):
     return biases
 
 
-def network_report(dc, inputs, torch, steps, warmup, use_graph, profile_steps):
-    """Whole MobileNetV2 feature extractor (batch 64, 224x224x3 -> 7x7x1280,
-    fp16): 17 blocks, the 10 stride-1 residual blocks gated with densities
-    ~ U[0.2, 0.6], against the same network run dense."""
-    n, h, w = 64, 224, 224
-    x_np, layers, dens = inputs.make_network_inputs(0, n, h, w, dtype="f16")
+def network_report(dc, inputs, torch, steps, warmup, use_graph, profile_steps, kind="mobilenetv2"):
+    """A whole network against the same network run dense.  "mobilenetv2":
+    the MobileNetV2 feature extractor (batch 64, 224x224x3 -> 7x7x1280, fp16),
+    17 blocks, the 10 stride-1 residual blocks gated with densities
+    ~ U[0.2, 0.6].  "pose": the pose network (batch 32, 256x256x3 ellipse
+    images -> 64x64x32, fp16): a MobileNetV2 backbone, then 8 stacked
+    stride-1 blocks; 9 gated blocks with densities ~ U[0.2, 0.4], their mask
+    units pointed at the people (set during calibration)."""
+    labels = None
+    if kind == "pose":
+        n, h, w = 32, 256, 256
+        x_np, layers, dens, labels = inputs.make_pose_network_inputs(0, n, dtype="f16")
+        name = "pose_network_256_b32_f16"
+    else:
+        n, h, w = 64, 224, 224
+        x_np, layers, dens = inputs.make_network_inputs(0, n, h, w, dtype="f16")
+        name = "mobilenetv2_224_b64_f16"
     dt = torch.float16
     x0 = torch.from_numpy(x_np).cuda().to(dt)
-    biases = calibrate_network(dc, inputs, torch, x0, layers, dens, dt)
+    biases = calibrate_network(dc, inputs, torch, x0, layers, dens, dt, labels)
     sp_net = dc.NetworkWeights(layers, dt, biases=biases)
     dn_net = dc.NetworkWeights(layers, dt, biases=None)
     ng = sp_net.ngated
@@ -625,7 +648,7 @@ def network_report(dc, inputs, torch, steps, warmup, use_graph, profile_steps):
     def top(prof):
         return {k: {"avg_us": v["avg_us"], "launches": v["launches"], "total_us": v["total_us"]}
                 for k, v in sorted(prof.items(), key=lambda kv: -kv[1]["total_us"])}
-    return {"workload": "mobilenetv2_224_b64_f16", "batch": n, "input": [h, w, 3], "output": [sh.h, sh.w, sh.c],
+    return {"workload": name, "batch": n, "input": [h, w, 3], "output": [sh.h, sh.w, sh.c],
             "gated_blocks": ng, "target_density": dens.tolist(),
             "active_frac": [float(c[0]) / p for c, p in zip(counts, npos)],
             "dilated_frac": [float(c[1]) / p for c, p in zip(counts, npos)],
@@ -838,7 +861,7 @@ def main():
                          "then the sparse and the dense stack")
     ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write the traffic summary from the counter CSVs of two --traffic-pass runs")
-    ap.add_argument("--section", choices=("network", "shufflenet"),
+    ap.add_argument("--section", choices=("network", "pose_network", "shufflenet"),
                     help="run only this report (for a kernel trace of it) and print its JSON object")
     args = ap.parse_args()
     if args.summarize_traffic:
@@ -861,9 +884,13 @@ def main():
         sys.exit(1)
     dc.load()
     if args.section:
-        report = network_report if args.section == "network" else shufflenet_report
-        print(json.dumps({args.section: report(dc, inputs, torch, args.steps, args.warmup, not args.no_graph,
-                                               args.profile_steps)}))
+        g = not args.no_graph
+        if args.section == "shufflenet":
+            out = shufflenet_report(dc, inputs, torch, args.steps, args.warmup, g, args.profile_steps)
+        else:
+            kind = "pose" if args.section == "pose_network" else "mobilenetv2"
+            out = network_report(dc, inputs, torch, args.steps, args.warmup, g, args.profile_steps, kind)
+        print(json.dumps({args.section: out}))
         return
     wl = inputs.WORKLOADS[args.workload]
     dt = dc.NAME_TO_DTYPE[wl.dtype]
@@ -977,6 +1004,9 @@ def main():
         log("whole network")
         result["network"] = network_report(dc, inputs, torch, min(args.steps, 30), min(args.warmup, 5), use_graph,
                                            min(args.profile_steps, 5))
+        log("pose network")
+        result["pose_network"] = network_report(dc, inputs, torch, min(args.steps, 30), min(args.warmup, 5),
+                                                use_graph, min(args.profile_steps, 5), "pose")
     if not args.no_probes:
         log("bandwidth probes")
         result["bandwidth_probes"] = bandwidth_probes(dc, inputs, torch)

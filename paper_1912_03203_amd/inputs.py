@@ -263,11 +263,12 @@ MBV2_STAGES = ((1, 16, 1, 1), (6, 24, 2, 2), (6, 32, 3, 2), (6, 64, 4, 2), (6, 9
 MBV2_LAST = 1280
 
 
-def mbv2_layers(rng, dtype="f16", std=0.05, mask_std=0.1, in_c=3):
+def mbv2_layers(rng, dtype="f16", std=0.05, mask_std=0.1, in_c=3, stages=MBV2_STAGES, last=MBV2_LAST):
     """Folded-BN weights of a MobileNetV2 feature extractor as a layer list
-    (dicts; PyTorch layouts, storage-rounded weights, fp32 biases).  Every
-    block with stride 1 and equal input and output widths is gated: it carries
-    a mask unit w_m and "gated": True."""
+    (dicts; PyTorch layouts, storage-rounded weights, fp32 biases): the stem,
+    the (t, c, n, s) stages, and a final 1x1 to `last` channels (none when
+    last is None).  Every block with stride 1 and equal input and output
+    widths is gated: it carries a mask unit w_m and "gated": True."""
     def wgt(*shape):
         return round_to_storage(rng.normal(0.0, std, size=shape), dtype)
 
@@ -276,7 +277,7 @@ def mbv2_layers(rng, dtype="f16", std=0.05, mask_std=0.1, in_c=3):
 
     layers = [{"kind": "conv3x3", "w": wgt(MBV2_STEM, in_c, 3, 3), "b": bias(MBV2_STEM), "stride": 2, "act": 2}]
     c_in = MBV2_STEM
-    for t, c, n, s in MBV2_STAGES:
+    for t, c, n, s in stages:
         for i in range(n):
             stride = s if i == 0 else 1
             e = c_in * t
@@ -288,7 +289,8 @@ def mbv2_layers(rng, dtype="f16", std=0.05, mask_std=0.1, in_c=3):
                 layer["w_m"] = rng.normal(0.0, mask_std, size=c_in).astype(np.float32)
             layers.append(layer)
             c_in = c
-    layers.append({"kind": "conv1x1", "w": wgt(MBV2_LAST, c_in), "b": bias(MBV2_LAST), "act": 2})
+    if last is not None:
+        layers.append({"kind": "conv1x1", "w": wgt(last, c_in), "b": bias(last), "act": 2})
     return layers
 
 
@@ -301,3 +303,24 @@ def make_network_inputs(seed, n, h, w, dtype="f16", density_range=(0.2, 0.6)):
     ngated = sum(1 for l in layers if l.get("gated"))
     dens = rng.uniform(density_range[0], density_range[1], size=ngated)
     return x, layers, dens
+
+
+# Pose-estimation network: a MobileNetV2 backbone from 256x256x3 to 64x64x32
+# (stem, the t=1 block, the 24-channel stage, one 32-channel block), then 8
+# stacked stride-1 blocks at 64x64x32 with hidden width 192.  Gated: the
+# second 24-channel block and the 8 stacked blocks.
+POSE_STAGES = ((1, 16, 1, 1), (6, 24, 2, 2), (6, 32, 1, 1), (6, 32, 8, 1))
+
+
+def make_pose_network_inputs(seed, n, dtype="f16", density_range=(0.2, 0.4)):
+    """Ellipse "person" images (256x256x3: flat background, 1-2 textured
+    ellipses), the pose layer list, a target density per gated block
+    ~ U[density_range] and the [n, 256, 256] person labels (for mask units
+    pointed at the people, see ellipse_mask_weights)."""
+    rng = rng_for(seed)
+    x, labels = ellipse_features(rng, n, 256, 256, 3)
+    x = round_to_storage(x, dtype)
+    layers = mbv2_layers(rng, dtype, stages=POSE_STAGES, last=None)
+    ngated = sum(1 for l in layers if l.get("gated"))
+    dens = rng.uniform(density_range[0], density_range[1], size=ngated)
+    return x, layers, dens, labels

@@ -213,6 +213,39 @@ def test_gated_network_full_batch_sampled_images():
     assert err <= util.TOL["f16"]
 
 
+def test_pose_network_end_to_end():
+    """The pose network (256x256x3 ellipse images -> MobileNetV2 backbone ->
+    8 stacked gated blocks at 64x64x32) on 2 images, with the oracle's biases,
+    checked as in test_gated_network_end_to_end."""
+    import oracle
+    x, layers, dens, _ = inputs.make_pose_network_inputs(7, 2, dtype="f16")
+    biases = oracle_biases(x, layers, dens, "f16")
+    y, m, c = run_net(x, layers, "f16", biases=biases, masks=True)
+    assert y.shape == (2, 64, 64, 32)
+    rnd = rounder("f16")
+    cur = util.nchw(x).astype(np.float64)
+    off, gi, flips = 0, 0, []
+    for L in layers:
+        if L.get("gated"):
+            N, C, H, W = cur.shape
+            G = m[off:off + N * H * W]
+            off += N * H * W
+            Go, mo = oracle.mask(cur.astype(np.float32), L["w_m"], biases[gi])
+            d = G != Go
+            envelope = np.abs(L["w_m"]).sum() * util.TOL["f16"] * np.abs(cur).max()
+            assert (np.abs(mo[d]) <= envelope).all(), "gated block %d" % gi
+            flips.append(int(d.sum()))
+            assert int(c[gi][0]) == int(G.sum())
+            cur = rnd(oracle.block_dense(cur, L, G)[0])
+            gi += 1
+        else:
+            cur, _ = oracle.network_forward(cur, [L], None, round_to=rnd)
+    log("  pose network: decisions differing from the oracle's own, per gated block: %s" % flips)
+    err = util.normwise(y, util.nhwc(cur))
+    log("  pose network vs forced-mask oracle: err %.2e" % err)
+    assert err <= util.TOL["f16"]
+
+
 POINTWISE_CASES = [
     # dtype, (N, H, W), C, O: every output-range width (2..12 tiles of 16),
     # contraction chunks of 1..8 steps of 32 and several chunks, one partial
