@@ -65,6 +65,15 @@ if ROOT not in sys.path:
 
 METRIC = "images/sec of sparse MobileNetV2 block stack at mask density 0.25; speedup vs dense"
 HBM_PEAK_GBS = 8000.0
+# what the stack's input feature maps are (the benchmark draws them directly;
+# the pose_network report runs the backbone from 256x256x3 images instead)
+INPUT_RECIPES = {
+    "ellipses": "64x64x32 features drawn directly: 1-2 person ellipses (15-35% of the image each, "
+                "own mean + 3 texture blobs) on a flat N(0,0.3) background + N(0,0.05) noise; mask "
+                "weights point from background to person mean; standing in for a MobileNetV2 backbone "
+                "on 256x256x3 person crops",
+    "blobs": "4 random Gaussian blobs per image + N(0,0.05) noise",
+}
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_block_fused_pose_stack8_traffic.md")
@@ -266,8 +275,13 @@ def algorithmic_bytes(name, dense, s, C, E, npos, rows, P, Pd, last=False, bands
     separate buffer), reads this block's mask and writes the next one's."""
     weights = 2 * E * C * s + 9 * E * s + 4 * (2 * E + C)
     if name == "k_block_fused":
-        masks = 0 if dense else npos + (0 if last else npos)
-        return 2 * npos * C * s + masks + weights
+        if dense:  # x read and y written at every position
+            return 2 * npos * C * s + weights
+        # the fused-block ideal: the mask unit reads x everywhere, the
+        # expansion gathers the dilated rows, the residual reads x and writes
+        # y at the active rows; this block's mask in, the next one's out
+        masks = npos + (0 if last else npos)
+        return npos * C * s + Pd * C * s + 2 * P * C * s + masks + weights
     if name == "k_copy16":
         return 2 * npos * C * s
     if name == "k_band_counts":  # per-band (P, P_d) pairs in, the block's sums out
@@ -288,10 +302,65 @@ def algorithmic_bytes(name, dense, s, C, E, npos, rows, P, Pd, last=False, bands
     return table[name]
 
 
-def cpu_baseline(inputs, wl, x0_np, blocks_np, density, budget_s=12.0):
+def work_counts(wl, counts, t_sp, t_dn):
+    """Multiply-accumulates of one step from the device's per-block counts
+    (Sec. 3.3): dense F_b = NHW (9E + 2CE) (Eq. 9) and sparse
+    F_b,sp = P_d C E + P (9E + EC) (Eq. 10, N_b = P by Eq. 11), summed over
+    the blocks; flop rates count two per multiply-accumulate."""
+    C, E, nhw = wl.c, wl.e, wl.nhw
+    dense = wl.blocks * nhw * (9 * E + 2 * C * E)
+    sparse = sum(int(Pd) * C * E + int(P) * (9 * E + E * C) for P, Pd in counts)
+    return {"eq9_dense_macs_per_step": int(dense), "eq10_sparse_macs_per_step": int(sparse),
+            "mac_ratio_dense_over_sparse": dense / sparse if sparse else None,
+            "sparse_tflops": 2.0 * sparse / t_sp / 1e12, "dense_tflops": 2.0 * dense / t_dn / 1e12,
+            "P_per_block": [int(P) for P, _ in counts], "Pd_per_block": [int(Pd) for _, Pd in counts]}
+
+
+def compact_record(result):
+    """The benchmark's one-line result: the headline, the roofline of the
+    dominant kernel, the work counts, the CPU baseline and one summary number
+    per extra report (the full report goes to a file)."""
+    r3 = lambda v: None if v is None else float("%.4g" % v)
+    keep = ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step", "higher_is_better",
+            "scaling", "vs_baseline", "dtype", "data", "config", "speedup_vs_dense", "dense", "roofline",
+            "work", "cpu_baseline")
+    out = {k: result[k] for k in keep if k in result}
+    out["per_block_us"] = {k: r3(v) for k, v in result["per_block_us"].items()}
+    if "cpu_baseline_parallel" in result:
+        c = result["cpu_baseline_parallel"]
+        out["cpu_baseline_parallel"] = {"value": r3(c["value"]), "cores": c["cores"], "kind": c["kind"]}
+    if "cpu_baseline_dense" in result:
+        c = result["cpu_baseline_dense"]
+        out["cpu_baseline_dense"] = {"value": r3(c["value"]), "cores": c["cores"], "kind": c["kind"]}
+    if "timing_protocol" in result:
+        tp = result["timing_protocol"]
+        out["timing_protocol"] = {"sparse_median_us": r3(tp["sparse"]["median_us"]),
+                                  "dense_median_us": r3(tp["dense"]["median_us"]),
+                                  "speedup_median": r3(tp["speedup_median"])}
+    extra = {}
+    for key in ("sweep_pose_stack", "sweep"):
+        if key in result:
+            extra[key] = [[r["density"] if not isinstance(r["density"], list) else "U[0.2,0.4]",
+                           r3(r["sparse_us"]), r3(r["dense_us"]), r3(r["speedup"])] for r in result[key]["rows"]]
+    for key in ("network", "pose_network"):
+        if key in result:
+            extra[key] = {"images_per_s": r3(result[key]["sparse_images_per_s"]),
+                          "speedup_vs_dense": r3(result[key]["speedup_vs_dense"])}
+    if "shufflenet" in result:
+        extra["shufflenet_speedup"] = {r["workload"]: r3(r["speedup_vs_dense"]) for r in result["shufflenet"]}
+    if "chain" in result and "speedup_vs_dense" in result["chain"]:
+        extra["chain_speedup_vs_dense"] = r3(result["chain"]["speedup_vs_dense"])
+    if extra:
+        out["other_reports"] = extra
+    return out
+
+
+def cpu_baseline(inputs, wl, x0_np, blocks_np, density, budget_s=12.0, form="sparse"):
     """The oracle (mask, dilation, index maps, gather/scatter block; fp64; one
     thread) on the first S images of the batch, biases calibrated on that
-    sample.  S is sized so the timed run takes about budget_s seconds."""
+    sample.  S is sized so the timed run takes about budget_s seconds.
+    form="dense": the oracle's dense block with masked output (the plain
+    definition, Eq. 1 with the mask of Eq. 3) after the same mask unit."""
     import oracle
 
     def run(x_nhwc, biases=None, timed=False):
@@ -308,9 +377,12 @@ def cpu_baseline(inputs, wl, x0_np, blocks_np, density, budget_s=12.0):
             cal.append(bias)
             t0 = time.perf_counter()
             G, _ = oracle.mask(x.astype(np.float32), wts["w_m"], bias)
-            Gd = oracle.dilate(G, N, H, W, 1)
-            A, D, nbr = oracle.indices(G, Gd, N, H, W)
-            y, _, _ = oracle.block_sparse(x, wts, A, D, nbr)
+            if form == "dense":
+                y, _, _ = oracle.block_dense(x, wts, G)
+            else:
+                Gd = oracle.dilate(G, N, H, W, 1)
+                A, D, nbr = oracle.indices(G, Gd, N, H, W)
+                y, _, _ = oracle.block_sparse(x, wts, A, D, nbr)
             t += time.perf_counter() - t0
             y_nhwc = inputs.round_to_storage(y.transpose(0, 2, 3, 1), wl.dtype)
             x = np.ascontiguousarray(y_nhwc.transpose(0, 3, 1, 2)).astype(np.float64)
@@ -322,9 +394,11 @@ def cpu_baseline(inputs, wl, x0_np, blocks_np, density, budget_s=12.0):
     sample = x0_np[:S]
     cal, _ = run(sample)
     _, t = run(sample, cal)
+    what = ("mask, dense block with masked output" if form == "dense"
+            else "mask, dilation, index maps, gather/scatter block")
     return {"value": S / t, "unit": "images/s", "cores": 1, "kind": "oracle",
-            "sample": "%d of %d images through all %d blocks (mask, dilation, index maps, "
-                      "gather/scatter block; fp64 C loops, one thread); %.1f s" % (S, wl.n, len(blocks_np), t)}
+            "sample": "%d of %d images through all %d blocks (%s; fp64 C loops, one thread); %.1f s"
+                      % (S, wl.n, len(blocks_np), what, t)}
 
 
 def cpu_baseline_parallel(inputs, wl, x0_np, blocks_np, density, budget_s=8.0):
@@ -337,7 +411,10 @@ def cpu_baseline_parallel(inputs, wl, x0_np, blocks_np, density, budget_s=8.0):
     from concurrent.futures import ThreadPoolExecutor
 
     import oracle
-    threads = max(1, min(16, len(os.sched_getaffinity(0))))
+    # one thread per core this process may use, at most the 16 host cores that
+    # a one-GPU machine gives a job
+    affinity = len(os.sched_getaffinity(0))
+    threads = max(1, min(16, affinity))
     x = np.ascontiguousarray(x0_np.transpose(0, 3, 1, 2)).astype(np.float64)
     biases = []
     cur = x
@@ -380,7 +457,7 @@ def cpu_baseline_parallel(inputs, wl, x0_np, blocks_np, density, budget_s=8.0):
     except OSError:
         pass
     return {"value": reps * x.shape[0] / t, "unit": "images/s", "cores": threads, "kind": "oracle",
-            "cpu": model,
+            "cpu": model, "affinity_cores": affinity,
             "sample": "all %d images x %d repeats through all %d blocks, one image per task on %d threads; %.1f s"
                       % (x.shape[0], reps, len(blocks_np), threads, t)}
 
@@ -856,6 +933,8 @@ def main():
     ap.add_argument("--no-probes", action="store_true", help="skip the HBM-scale bandwidth probes")
     ap.add_argument("--no-network", action="store_true", help="skip the whole-MobileNetV2 report")
     ap.add_argument("--profile-steps", type=int, default=20)
+    ap.add_argument("--report", help="where the full JSON report goes "
+                                     "(default gpurun_out/bench_report.json); stdout gets the compact line")
     ap.add_argument("--traffic-pass", action="store_true",
                     help="untimed launches for an HBM-counter run: a plain copy of known size, "
                          "then the sparse and the dense stack")
@@ -972,7 +1051,8 @@ def main():
         "vs_baseline": None,
         "dtype": wl.dtype,
         "data": "synthetic",
-        "config": {"workload": wl.name, "batch": wl.n, "h": wl.h, "w": wl.w, "c": wl.c,
+        "config": {"workload": wl.name, "input_recipe": INPUT_RECIPES[wl.features],
+                   "batch": wl.n, "h": wl.h, "w": wl.w, "c": wl.c,
                    "hidden": wl.e, "blocks": wl.blocks, "density": args.density,
                    "graph": use_graph, "seed": args.seed,
                    "execution": "kernel chain" if args.unfused else "one launch per block"},
@@ -984,7 +1064,9 @@ def main():
         "kernels": {"sparse": prof_sp, "dense": prof_dn, "sparse_kernel_sum_us": kernel_sum_us},
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
-                     "algorithmic_bytes_per_launch": bytes_per_launch},
+                     "algorithmic_bytes_per_launch": bytes_per_launch,
+                     "avg_us_per_launch": prof_sp[dom]["avg_us"]},
+        "work": work_counts(wl, counts, t_sp, t_dn),
     }
     rec = measured_traffic(wl.name, args.density) if dom == "k_block_fused" else None
     if rec is not None:
@@ -1029,7 +1111,15 @@ def main():
         result["cpu_baseline"] = cpu_baseline(inputs, wl, x_np, blocks_np, args.density)
         log("cpu baseline (oracle, all host cores)")
         result["cpu_baseline_parallel"] = cpu_baseline_parallel(inputs, wl, x_np, blocks_np, args.density)
-    print(json.dumps(result), flush=True)
+        log("cpu baseline (dense oracle)")
+        result["cpu_baseline_dense"] = cpu_baseline(inputs, wl, x_np, blocks_np, args.density, budget_s=8.0,
+                                                    form="dense")
+    report = args.report or os.path.join(ROOT, "gpurun_out", "bench_report.json")
+    os.makedirs(os.path.dirname(os.path.abspath(report)), exist_ok=True)
+    with open(report, "w") as f:
+        json.dump(result, f, indent=1)
+    log("full report: %s" % report)
+    print(json.dumps(compact_record(result)), flush=True)
 
 
 if __name__ == "__main__":

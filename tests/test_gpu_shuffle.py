@@ -1,8 +1,8 @@
 """Parity of the ShuffleNetV2 unit stack (dynconv_shuffle_stack_forward) with
 the CPU oracle: masks and counts bit-exact, the pass-through half and the
-inactive branch positions bit for bit, the unit output within 1e-5 (fp32) /
-2e-2 (fp16, bf16) normwise (the branch increment alone: the same, 4e-2 in
-bf16)."""
+inactive branch positions bit for bit, the unit output and the branch output
+on its own within 1e-5 (fp32) / 2e-2 (fp16, bf16) normwise (the branch
+increment alone: the same, 4e-2 in bf16)."""
 import numpy as np
 import pytest
 import torch
@@ -58,6 +58,8 @@ def check_unit_output(y_gpu, x_f32, y_oracle, G, dtype):
     assert np.ascontiguousarray(yg[~G][:, 1::2]).tobytes() == np.ascontiguousarray(xo[~G][:, cb:]).tobytes()
     yo = y_oracle.reshape(-1, C)
     e_y = util.normwise(yg, yo)
+    # the branch output b = x2 + G o F(x2) (odd output channels) on its own
+    e_br = util.normwise(yg[:, 1::2], yo[:, 1::2])
     e_b = util.normwise(yg[G][:, 1::2].astype(np.float64) - xo[G][:, cb:],
                         yo[G][:, 1::2] - xo[G][:, cb:]) if G.any() else 0.0
     # The bound is on the unit output y.  The branch increment F alone is
@@ -65,8 +67,10 @@ def check_unit_output(y_gpu, x_f32, y_oracle, G, dtype):
     # significands (relative rounding 2^-9 each) and both contractions
     # cancel, so F's own normwise error gets twice the output bound there.
     tol_b = 2 * util.TOL[dtype] if dtype == "bf16" else util.TOL[dtype]
-    log("  normwise err: y %.3e  branch F %.3e  (tol %.0e, F %.0e)" % (e_y, e_b, util.TOL[dtype], tol_b))
+    log("  normwise err: y %.3e  branch output %.3e  branch F %.3e  (tol %.0e, F %.0e)"
+        % (e_y, e_br, e_b, util.TOL[dtype], tol_b))
     assert e_y <= util.TOL[dtype]
+    assert e_br <= util.TOL[dtype]
     assert e_b <= tol_b
 
 

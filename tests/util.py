@@ -39,6 +39,17 @@ def normwise(got, want):
     return 0.0 if err == 0 else err / (scale if scale > 0 else 1.0)
 
 
+def elementwise(got, want):
+    """Diagnostic: max over elements of |got - want| / max(|want|, 1e-3 max|want|)."""
+    got = np.asarray(got, np.float64)
+    want = np.asarray(want, np.float64)
+    if not want.size:
+        return 0.0
+    floor = 1e-3 * np.max(np.abs(want))
+    den = np.maximum(np.abs(want), floor if floor > 0 else 1.0)
+    return float(np.max(np.abs(got - want) / den))
+
+
 def oracle_block_dense_chunked(x_nchw, wts, G=None):
     """oracle.block_dense over chunks of images in a thread pool."""
     x = np.asarray(x_nchw, np.float64)
