@@ -16,8 +16,10 @@
  *   frees nothing: every buffer, including the workspace, belongs to the
  *   caller.  Its only global state is a cache of device occupancy figures
  *   (workgroups the device holds at once, per kernel; written once, read
- *   atomically), so calls on different streams may run concurrently as long
- *   as their buffers are disjoint.
+ *   atomically) and the static scratch array of
+ *   dynconv_stack_forward_noalloc, so calls on different streams may run
+ *   concurrently as long as their buffers are disjoint (for that call: as
+ *   long as they run on different devices).
  * * Every call validates all of its arguments on the host first.  On any
  *   error it returns a nonzero status and enqueues nothing.  Otherwise the
  *   work is enqueued asynchronously on `stream` (a hipStream_t; NULL is the
@@ -275,6 +277,30 @@ dynconv_status dynconv_stack_forward_profiled(const void *x, void *y, dynconv_sh
                                               int32_t *counts, void *ws, size_t ws_bytes,
                                               void *stream, void *const *events,
                                               int32_t n_events);
+
+/*
+ * dynconv_stack_forward for callers that cannot allocate device memory:
+ * code under HIP graph capture that must not call hipMalloc, tight serving
+ * loops, harnesses that forbid allocation.  It takes no workspace: the
+ * library keeps one static scratch array of
+ * dynconv_stack_noalloc_max_workspace_bytes() (16 MiB) in device memory on
+ * every device it runs on, held until the process ends, and this call uses
+ * the current device's copy.  Arguments, results and errors are those of
+ * dynconv_stack_forward (the same kernels, bit-identical output), except:
+ *   * a stack whose dynconv_stack_workspace_bytes exceeds the array returns
+ *     DYNCONV_ERR_WORKSPACE and enqueues nothing;
+ *   * the first call on a device looks the array up (hipGetSymbolAddress;
+ *     a failure returns DYNCONV_ERR_HIP);
+ *   * it calls no hipMalloc, hipFree or other allocating routine.
+ * Every call on one device shares that device's array and leaves the last
+ * call's contents in it (nothing in it needs to start at zero), so calls
+ * that overlap in time on one device race: serialise them (one stream, or
+ * events between streams).
+ */
+size_t dynconv_stack_noalloc_max_workspace_bytes(void);
+dynconv_status dynconv_stack_forward_noalloc(const void *x, void *y, dynconv_shape s, dynconv_dtype dt,
+                                             const dynconv_block *blks, int32_t n_blocks, int32_t flags,
+                                             uint8_t *masks, int32_t *counts, void *stream);
 
 /*
  * ShuffleNetV2 stride-1 units whose convolutional branch is a gated residual

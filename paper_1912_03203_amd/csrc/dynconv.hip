@@ -1063,6 +1063,32 @@ void net_walk(const void *x, void *y, dynconv_shape in, dynconv_dtype dt, const 
     }
 }
 
+// ------------------------------------------------------------ static scratch
+// Device memory of the stack call that allocates nothing: one array per
+// device, held until the process ends.  In host code `scratch` names a
+// host-side stand-in, never a device address: kernels and copies take the
+// address that hipGetSymbolAddress returns for the current device.
+constexpr size_t kStaticScratchBytes = size_t(16) << 20;
+constexpr int kMaxDevices = 64;
+__device__ __align__(256) char scratch[kStaticScratchBytes];
+std::atomic<char *> g_scratch_ptr[kMaxDevices];
+
+// The current device's copy of `scratch` (looked up once per device).
+dynconv_status static_scratch(char **out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return DYNCONV_ERR_HIP;
+    if (dev < 0 || dev >= kMaxDevices) return DYNCONV_ERR_UNSUPPORTED;
+    char *p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+    if (!p) {
+        void *q = nullptr;
+        if (hipGetSymbolAddress(&q, HIP_SYMBOL(scratch)) != hipSuccess || !q) return DYNCONV_ERR_HIP;
+        p = static_cast<char *>(q);
+        g_scratch_ptr[dev].store(p, std::memory_order_release);
+    }
+    *out = p;
+    return DYNCONV_OK;
+}
+
 }  // namespace
 
 // ================================================================ C ABI
@@ -1228,6 +1254,19 @@ dynconv_status dynconv_stack_forward_profiled(const void *x, void *y, dynconv_sh
                                               void *stream, void *const *events, int32_t n_events) {
     return stack_common(x, y, s, dt, blks, n_blocks, flags, masks, counts, ws, ws_bytes, stream,
                         events, n_events, true);
+}
+
+size_t dynconv_stack_noalloc_max_workspace_bytes(void) { return kStaticScratchBytes; }
+
+dynconv_status dynconv_stack_forward_noalloc(const void *x, void *y, dynconv_shape s, dynconv_dtype dt,
+                                             const dynconv_block *blks, int32_t n_blocks, int32_t flags,
+                                             uint8_t *masks, int32_t *counts, void *stream) {
+    if (dynconv_status st = stack_checked(x, y, s, dt, blks, n_blocks, flags)) return st;
+    if (stack_layout(s, blks, n_blocks, dt, flags).total > kStaticScratchBytes) return DYNCONV_ERR_WORKSPACE;
+    char *ws = nullptr;
+    if (dynconv_status st = static_scratch(&ws)) return st;
+    return stack_common(x, y, s, dt, blks, n_blocks, flags, masks, counts, ws, kStaticScratchBytes, stream,
+                        nullptr, 0, false);
 }
 
 size_t dynconv_shuffle_stack_workspace_bytes(dynconv_shape s, const dynconv_block *branches,

@@ -33,7 +33,8 @@ EXPORTED = (
     "dynconv_shuffle_stack_forward", "dynconv_shuffle_stack_launch_names",
     "dynconv_shuffle_stack_forward_profiled", "dynconv_network_output_shape",
     "dynconv_network_workspace_bytes", "dynconv_network_forward", "dynconv_network_launch_names",
-    "dynconv_network_forward_profiled",
+    "dynconv_network_forward_profiled", "dynconv_stack_noalloc_max_workspace_bytes",
+    "dynconv_stack_forward_noalloc",
 )
 
 
@@ -114,6 +115,11 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
                                                    ctypes.POINTER(Block), i32, i32, vp, vp, vp, sz,
                                                    vp, ctypes.POINTER(ctypes.c_void_p), i32]
     lib.dynconv_stack_forward_profiled.restype = ctypes.c_int
+    lib.dynconv_stack_noalloc_max_workspace_bytes.argtypes = []
+    lib.dynconv_stack_noalloc_max_workspace_bytes.restype = sz
+    lib.dynconv_stack_forward_noalloc.argtypes = [vp, vp, Shape, ctypes.c_int, ctypes.POINTER(Block), i32,
+                                                  i32, vp, vp, vp]
+    lib.dynconv_stack_forward_noalloc.restype = ctypes.c_int
     lib.dynconv_shuffle_stack_workspace_bytes.argtypes = [Shape, ctypes.POINTER(Block), i32,
                                                           ctypes.c_int, i32]
     lib.dynconv_shuffle_stack_workspace_bytes.restype = sz
@@ -368,6 +374,23 @@ class Stack:
 def stack_forward(x: torch.Tensor, y: torch.Tensor, blocks, flags=0, masks=None, counts=None,
                   ws=None, stream=None):
     return Stack(x, y, blocks, flags, masks, counts, ws)(stream)
+
+
+def stack_noalloc_max_workspace_bytes() -> int:
+    return int(load().dynconv_stack_noalloc_max_workspace_bytes())
+
+
+def stack_forward_noalloc(x: torch.Tensor, y: torch.Tensor, blocks, flags=0, masks=None, counts=None,
+                          stream=None):
+    """dynconv_stack_forward_noalloc: the stack call on the library's static
+    per-device scratch array instead of a caller workspace."""
+    lib = load()
+    arr = _blocks_array(blocks)
+    _check(lib.dynconv_stack_forward_noalloc(_ptr(x), _ptr(y), shape_of(x), dtype_code(x.dtype), arr,
+                                             len(blocks), int(flags), _ptr(masks), _ptr(counts),
+                                             _stream(stream)),
+           "dynconv_stack_forward_noalloc")
+    return y
 
 
 class ShuffleStack:
