@@ -76,9 +76,13 @@ INPUT_RECIPES = {
 }
 
 
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_block_fused_pose_stack8_traffic.md")
-KERNEL_SOURCES = ("paper_1912_03203_amd/csrc/fused.h", "paper_1912_03203_amd/csrc/kernels.h",
-                  "paper_1912_03203_amd/csrc/dynconv.hip")
+def traffic_file(kernel):
+    return os.path.join(ROOT, "profiles", "%s_pose_stack8_traffic.md" % kernel)
+
+
+KERNEL_SOURCES = ("paper_1912_03203_amd/csrc/cells.h", "paper_1912_03203_amd/csrc/fused.h",
+                  "paper_1912_03203_amd/csrc/kernels.h", "paper_1912_03203_amd/csrc/dynconv.hip")
+ONE_LAUNCH = ("k_block_cells", "k_block_fused")
 
 
 def log(msg):
@@ -96,12 +100,12 @@ def kernel_source_sha1():
     return h.hexdigest()
 
 
-def measured_traffic(workload, density):
+def measured_traffic(kernel, workload, density):
     """HBM bytes per sparse one-launch block from the committed counter
     summary, or None when it is absent, for another workload, or taken on
     other kernel sources."""
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(traffic_file(kernel)) as f:
             text = f.read()
     except OSError:
         return None
@@ -274,7 +278,9 @@ def algorithmic_bytes(name, dense, s, C, E, npos, rows, P, Pd, last=False, bands
     one-launch block reads x and writes y at every position (its output is a
     separate buffer), reads this block's mask and writes the next one's."""
     weights = 2 * E * C * s + 9 * E * s + 4 * (2 * E + C)
-    if name == "k_block_fused":
+    if name == "k_mask_cells":  # x everywhere in, the mask and the per-cell counts out
+        return npos * C * s + npos + bands
+    if name in ("k_block_fused", "k_block_cells"):
         if dense:  # x read and y written at every position
             return 2 * npos * C * s + weights
         # the fused-block ideal: the mask unit reads x everywhere, the
@@ -795,7 +801,7 @@ def bandwidth_probes(dc, inputs, torch, reps=5):
         for n, t in best.items():
             nb = algorithmic_bytes(n, dense, s, wl.c, wl.e, npos, rows, P, Pd, last=True)
             if n == "k_block_fused" and not dense:
-                nb -= npos  # a one-block stack computes its own mask: no mask read
+                nb -= npos  # the patch kernel's one-block stack computes its own mask: no mask read
             out["%s %s" % (n, tag)] = {"batch": x.shape[0], "density": None if dense else P / npos,
                                        "dilated": None if dense else Pd / npos, "bytes": nb,
                                        "best_us": 1e6 * t, "gbs": nb / t / 1e9,
@@ -808,8 +814,8 @@ def bandwidth_probes(dc, inputs, torch, reps=5):
     chain = ("k_mask", "k_expand", "k_dw_project")
     probe("dense, 2048 x 56x56x24", stage2, 64, dc.STACK_UNFUSED | dc.STACK_DENSE, None, chain)
     probe("sparse d=0.25, 2048 x 56x56x24", stage2, 64, dc.STACK_UNFUSED, 0.25, chain)
-    probe("dense, 1024 x 64x64x32", pose, 32, dc.STACK_DENSE, None, ("k_block_fused",))
-    probe("sparse d=0.25, 1024 x 64x64x32", pose, 32, 0, 0.25, ("k_block_fused",))
+    probe("dense, 1024 x 64x64x32", pose, 32, dc.STACK_DENSE, None, ONE_LAUNCH)
+    probe("sparse d=0.25, 1024 x 64x64x32", pose, 32, 0, 0.25, ONE_LAUNCH + ("k_mask_cells",))
     del scratch
     torch.cuda.empty_cache()
     return out
@@ -850,6 +856,7 @@ def summarize_traffic(args):
     wl = inputs.WORKLOADS[args.workload]
     s = 2 if wl.dtype != "f32" else 4
     copy_bytes = wl.nhw * wl.c * s
+    kern = args.traffic_kernel
     out = {}
     for counter, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
         groups = {"copy": [], "sparse": [], "dense": []}
@@ -860,13 +867,13 @@ def summarize_traffic(args):
             v = float(row["Counter_Value"])
             if "k_copy16" in name:
                 groups["copy"].append(v)
-            elif "k_block_fused" in name:
-                # template argument DENSE: mangled "...k_block_fusedI<type>Lb1E..."
-                # or demangled "k_block_fused<type, true, ...>"
+            elif kern in name:
+                # template argument DENSE: mangled "...<kernel>I<type>Lb1E..."
+                # or demangled "<kernel><type, true, ...>"
                 if "<" in name:
                     dense = name.split("<", 1)[1].split(",")[1].strip() == "true"
                 else:
-                    dense = "Lb1E" in name.split("k_block_fused", 1)[1][:12]
+                    dense = "Lb1E" in name.split(kern, 1)[1][:12]
                 groups["dense" if dense else "sparse"].append(v)
         if not all(groups.values()):
             raise SystemExit("%s: missing dispatches in %s" % (counter, path))
@@ -875,12 +882,12 @@ def summarize_traffic(args):
     f_write = copy_bytes / (1024.0 * out["WRITE_SIZE"]["copy"][0])
     kib = {k: (out["FETCH_SIZE"][k][0], out["WRITE_SIZE"][k][0]) for k in ("copy", "sparse", "dense")}
     by = {k: 1024.0 * (kib[k][0] * f_fetch + kib[k][1] * f_write) for k in ("sparse", "dense")}
-    rec = {"kernel": "k_block_fused", "workload": wl.name, "density": args.density,
+    rec = {"kernel": kern, "workload": wl.name, "density": args.density,
            "source_sha1": kernel_source_sha1(), "sparse_bytes": by["sparse"], "dense_bytes": by["dense"],
            "fetch_scale": f_fetch, "write_scale": f_write}
     lines = [
-        "# HBM traffic of k_block_fused: 8-block pose stack, 32 x 64x64x32, hidden 192, fp16, density %.2f"
-        % args.density,
+        "# HBM traffic of %s: 8-block pose stack, 32 x 64x64x32, hidden 192, fp16, density %.2f"
+        % (kern, args.density),
         "",
         "Two counter runs of the same launch sequence (`bench.py --traffic-pass`: a plain copy of "
         "%d bytes each way, the sparse stack, the dense stack, 3 times each). Each counter is scaled "
@@ -901,17 +908,17 @@ def summarize_traffic(args):
         "|---|---:|---:|---:|---:|",
         "| k_copy16 (calibration) | %d | %.1f | %.1f | %d read + %d written |"
         % (out["FETCH_SIZE"]["copy"][1], kib["copy"][0], kib["copy"][1], copy_bytes, copy_bytes),
-        "| k_block_fused sparse | %d | %.1f | %.1f | %.0f |"
-        % (out["FETCH_SIZE"]["sparse"][1], kib["sparse"][0], kib["sparse"][1], by["sparse"]),
-        "| k_block_fused dense | %d | %.1f | %.1f | %.0f |"
-        % (out["FETCH_SIZE"]["dense"][1], kib["dense"][0], kib["dense"][1], by["dense"]),
+        "| %s sparse | %d | %.1f | %.1f | %.0f |"
+        % (kern, out["FETCH_SIZE"]["sparse"][1], kib["sparse"][0], kib["sparse"][1], by["sparse"]),
+        "| %s dense | %d | %.1f | %.1f | %.0f |"
+        % (kern, out["FETCH_SIZE"]["dense"][1], kib["dense"][0], kib["dense"][1], by["dense"]),
         "",
         "Scale factors: FETCH_SIZE x %.4f, WRITE_SIZE x %.4f." % (f_fetch, f_write),
         "",
         "<!-- traffic %s -->" % json.dumps(rec),
         "",
     ]
-    with open(TRAFFIC_FILE, "w") as f:
+    with open(traffic_file(kern), "w") as f:
         f.write("\n".join(lines))
     print(json.dumps(rec))
 
@@ -938,6 +945,8 @@ def main():
     ap.add_argument("--traffic-pass", action="store_true",
                     help="untimed launches for an HBM-counter run: a plain copy of known size, "
                          "then the sparse and the dense stack")
+    ap.add_argument("--traffic-kernel", default="k_block_cells",
+                    help="the one-launch kernel whose dispatches --summarize-traffic reads")
     ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write the traffic summary from the counter CSVs of two --traffic-pass runs")
     ap.add_argument("--section", choices=("network", "pose_network", "shufflenet"),
@@ -1013,13 +1022,17 @@ def main():
     prof_dn, _ = profile_kernels(dc, torch, dn, args.profile_steps)
     s = 2 if wl.dtype != "f32" else 4
     rows = wl.n * wl.h
-    # patches of the one-launch block: column strips of at most 32, R rows,
-    # at most `own` positions and `region` ring-included slots
-    own, region = (256, 340) if wl.c <= 32 else (128, 208) if wl.c <= 64 else (64, 108)
-    strips = -(-wl.w // 32)
-    wu = -(-wl.w // strips)
-    pr = max(1, min(own // wu, region // (wu + 2) - 2, 50, wl.h))
-    bands = wl.n * -(-wl.h // pr) * -(-wl.w // wu)
+    if "k_block_cells" in sp.names:
+        # cells of 2 x 8 positions
+        bands = wl.n * -(-wl.h // 2) * -(-wl.w // 8)
+    else:
+        # patches of the one-launch block: column strips of at most 32, R rows,
+        # at most `own` positions and `region` ring-included slots
+        own, region = (256, 340) if wl.c <= 32 else (128, 208) if wl.c <= 64 else (64, 108)
+        strips = -(-wl.w // 32)
+        wu = -(-wl.w // strips)
+        pr = max(1, min(own // wu, region // (wu + 2) - 2, 50, wl.h))
+        bands = wl.n * -(-wl.h // pr) * -(-wl.w // wu)
 
     def avg_bytes(name, dense):
         if dense:
@@ -1068,7 +1081,7 @@ def main():
                      "avg_us_per_launch": prof_sp[dom]["avg_us"]},
         "work": work_counts(wl, counts, t_sp, t_dn),
     }
-    rec = measured_traffic(wl.name, args.density) if dom == "k_block_fused" else None
+    rec = measured_traffic(dom, wl.name, args.density) if dom in ONE_LAUNCH else None
     if rec is not None:
         result["roofline"]["traffic"] = rec["sparse_bytes"]
         result["roofline"]["traffic_dense"] = rec["dense_bytes"]

@@ -49,13 +49,22 @@
 extern "C" {
 #endif
 
-typedef enum {
+/* The enumerations are 32-bit integers on both sides of the ABI.  C++ gets a
+ * fixed underlying type, so that a caller's out-of-range code (rejected with
+ * DYNCONV_ERR_DTYPE) is a defined value there too. */
+#ifdef __cplusplus
+#define DYNCONV_ENUM(tag) enum tag : int32_t
+#else
+#define DYNCONV_ENUM(tag) enum tag
+#endif
+
+typedef DYNCONV_ENUM(dynconv_dtype_e) {
     DYNCONV_F32 = 0,
     DYNCONV_F16 = 1,
     DYNCONV_BF16 = 2
 } dynconv_dtype;
 
-typedef enum {
+typedef DYNCONV_ENUM(dynconv_status_e) {
     DYNCONV_OK = 0,
     DYNCONV_ERR_NULL = 1,        /* a required pointer is NULL */
     DYNCONV_ERR_SHAPE = 2,       /* non-positive / overflowing sizes, overlapping buffers */
@@ -68,7 +77,7 @@ typedef enum {
     DYNCONV_ERR_ARG = 9          /* another argument is out of range (dilation, activation, block count) */
 } dynconv_status;
 
-typedef enum {
+typedef DYNCONV_ENUM(dynconv_act_e) {
     DYNCONV_ACT_NONE = 0,
     DYNCONV_ACT_RELU = 1,
     DYNCONV_ACT_RELU6 = 2
@@ -123,8 +132,10 @@ typedef struct {
     int64_t capacity;
 } dynconv_indices;
 
-/* Text for a status code (static storage, never NULL). */
-const char *dynconv_status_str(dynconv_status status);
+/* Text for a status code, a dynconv_status value passed as an integer so
+ * that any code is accepted (static storage, never NULL; codes outside the
+ * enumeration give "unknown status"). */
+const char *dynconv_status_str(int32_t status);
 
 /* Library identification string (static storage). */
 const char *dynconv_version(void);

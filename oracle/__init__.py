@@ -32,6 +32,8 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "dynconv_oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
+# the sanitizer tests load an instrumented build of the same source instead
+_LIB_OVERRIDE = os.environ.get("ORACLE_LIB")
 
 ACT_NONE, ACT_RELU, ACT_RELU6 = 0, 1, 2
 
@@ -52,9 +54,12 @@ def _load():
     global _lib
     if _lib is not None:
         return _lib
-    if not os.path.exists(_LIB):
-        build()
-    lib = ctypes.CDLL(_LIB)
+    if _LIB_OVERRIDE:
+        lib = ctypes.CDLL(_LIB_OVERRIDE)
+    else:
+        if not os.path.exists(_LIB):
+            build()
+        lib = ctypes.CDLL(_LIB)
     P = ctypes.c_void_p
     i32 = ctypes.c_int
     lib.oracle_mask.argtypes = [P, i32, i32, i32, i32, P, ctypes.c_float, P, P]

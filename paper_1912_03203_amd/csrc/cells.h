@@ -1,0 +1,613 @@
+// cells.h -- work-balanced one-launch gated block for narrow blocks (gfx950).
+//
+// k_block_cells runs a whole spatially gated inverted-residual block (Sec.
+// 3.2) for blocks of at most 32 channels and 192 hidden channels in 16-bit
+// storage.  The image is cut into cells of 2 x 8 positions; one wave owns a
+// cell from start to end, with no barrier between waves:
+//   1. the hard-mask bytes of the cell's 4 x 10 region (the cell plus a
+//      one-position ring) become one 64-bit ballot word; the cell's active
+//      set and the part of its 3x3 dilation inside the region (every in-image
+//      region position next to an active one) follow by shifts of that word,
+//      and their raster-ordered lists by popcount ranks;
+//   2. for each 32-channel slice of the hidden layer: expansion of the
+//      needed positions on the matrix cores (the bias is the accumulator's
+//      start), activation, stored at the position's slot of the wave's
+//      region array (slots outside the image hold zeros: the depthwise
+//      padding); the depthwise 3x3 at the active positions reads its 9 taps
+//      at fixed slot offsets; its output is the B operand of the projection,
+//      accumulated over the slices on the matrix cores;
+//   3. epilogue: y = x + F at the active positions, x elsewhere, stored for
+//      every position of the cell; then the next block's mask unit on the
+//      stored values (the fp32 multiply-add chain of k_mask), and the
+//      cell's active count for the next launch's schedule.
+// Every weight of the block sits in LDS for the whole launch.  The grid is
+// persistent (one workgroup of 16 waves per CU).  Workgroup k takes the cells
+// whose weighted start lies in the k-th equal share of the total work (an
+// empty cell counts 1, a cell with active positions kCellActiveWork), from
+// the per-cell active counts that the previous launch wrote.  The range's
+// empty cells are streamed first by all threads (copy and next mask unit,
+// two positions in flight per thread); then the 16 waves pull the active
+// cells of the range through a counter in LDS.  So a dense region of the
+// mask is spread over many CUs, and the span follows the active work.
+// The arithmetic of every output element is the one of the kernel chain
+// (k_expand, k_dw_project): the same operand fragments, summation order and
+// roundings.  Input and output must be different buffers (a cell's ring is
+// another cell's output).
+#pragma once
+
+#include "fused.h"
+
+namespace dynconv {
+
+
+// A cell is 2 image rows x 8 columns: 16 own positions, one 16-position tile
+// of the depthwise / projection, and a 4 x 10 region (the cell plus its ring)
+// of at most 40 positions, so one 64-bit ballot holds the region's mask.
+constexpr int kCellRows = 2, kCellCols = 8;
+constexpr int kCellOwn = kCellRows * kCellCols;       // 16 own positions
+constexpr int kRegCols = kCellCols + 2;               // 10
+constexpr int kRegRows = kCellRows + 2;               // 4
+constexpr int kRegSlots = kRegRows * kRegCols;        // 40 region slots
+constexpr int kNeedTiles = (kRegSlots + 15) / 16;     // 3
+constexpr int kCellWaves = 16;                        // 4 waves per SIMD
+constexpr int kCellThreads = kCellWaves * kWave;
+constexpr int kCellMaxC = 32;
+constexpr int kCellMaxE = 192;
+constexpr int kCellFirstOwn = kRegCols + 1;           // slot of own position (0, 0)
+// active cells of one workgroup's share held in its LDS list at once
+constexpr int kCellList = 2048;
+
+// Region slots (row rr, column cc) -> bit rr*10 + cc.
+constexpr uint64_t kRowBits = 0xffull << 1;           // columns 1..8 of one region row
+constexpr uint64_t kOwnBits = (kRowBits << 10) | (kRowBits << 20);
+constexpr uint64_t kCol0Bits = 1ull | (1ull << 10) | (1ull << 20) | (1ull << 30);
+constexpr uint64_t kCol9Bits = kCol0Bits << 9;
+
+__host__ __device__ inline int cells_per_image(int H, int W) {
+    return ((H + kCellRows - 1) / kCellRows) * ((W + kCellCols - 1) / kCellCols);
+}
+
+template <typename T>
+struct CellWeights {
+    alignas(16) T w1[kCellMaxE][kCellMaxC + 8];   // expansion rows e, channels fastest (zero past C, E)
+    alignas(16) T w3[kCellMaxC][kCellMaxE + 8];   // projection rows c, hidden fastest (zero past C, E)
+    alignas(16) T w2[9][kCellMaxE];               // depthwise taps, transposed (zero past E)
+    alignas(16) float b1[kCellMaxE];
+    alignas(16) float b2[kCellMaxE];
+    alignas(16) float b3[kCellMaxC];
+    alignas(16) float wm[kCellMaxC];              // the next block's mask unit
+};
+
+// A slice of the expansion in region layout: slot (rr, cc) at byte
+// rr * kRegPitch + cc * kSlotBytes.  The 96 padding bytes per region row put
+// the two image rows of a 16-position tile on distinct LDS banks (a 16-byte
+// read of 16 lanes touches every bank once); a spare slot at the end takes
+// the padding lanes of the last tile.
+constexpr int kSlotBytes = kChunkPad * 2;                 // 80: 32 channels + 8 padding, 16-bit
+constexpr int kRegPitch = kRegCols * kSlotBytes + 96;     // 896
+constexpr int kSpareSlot = kRegRows * kRegPitch;          // byte offset of the spare slot
+__device__ __forceinline__ int slot_off(int q) { return (q / kRegCols) * kRegPitch + (q % kRegCols) * kSlotBytes; }
+
+template <typename T>
+struct CellWaveLds {
+    // the region array; the epilogue reuses its first 16 x 80 bytes for the
+    // cell's own rows
+    alignas(16) char h1[kSpareSlot + kSlotBytes];
+    int8_t need[48];
+    int8_t act[kCellOwn];
+};
+
+template <typename T>
+struct CellLds {
+    CellWeights<T> w;
+    CellWaveLds<T> wv[kCellWaves];
+    int list[kCellList];  // this share's active cells, raster order
+    int part[kCellWaves];
+    int next;
+};
+
+__device__ __forceinline__ void wave_sync() {
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+}
+
+// mask unit (Eq. 2, Eq. 8 at zero noise) on one stored row: the fp32
+// multiply-add chain of k_mask, channels ascending from +0, then the bias
+constexpr int kCellPieces = kCellMaxC * 2 / 16;   // 16-byte pieces of a 16-bit row
+
+template <typename T>
+__device__ __forceinline__ bool cell_mask_row(const uint4 (&row)[kCellPieces], const float *wm, int C, float bm,
+                                              int mode) {
+    constexpr int per16 = 16 / static_cast<int>(sizeof(T));
+    float a = 0.0f;
+#pragma unroll
+    for (int p = 0; p < kCellPieces; ++p) {
+        if (p < C / per16) {
+            float v[8];
+            io<T>::load8(reinterpret_cast<const T *>(&row[p]), v);
+#pragma unroll
+            for (int u = 0; u < 8; ++u) a = __builtin_fmaf(wm[p * per16 + u], v[u], a);
+        }
+    }
+    return mask_decision(a + bm, mode);
+}
+
+// Popcount of this lane's 16-lane group in a ballot (the group is one cell).
+__device__ __forceinline__ int group16_count(uint64_t b, int lane) {
+    return __popc(static_cast<uint32_t>((b >> (lane & 48)) & 0xffffull));
+}
+
+// The first block's mask unit over cells: mask bytes of every position and
+// each cell's active count (four cells per wave, lane = own position).
+constexpr int kCellsPerMaskWave = kWave / kCellOwn;
+
+template <typename T>
+__global__ void __launch_bounds__(kBlock)
+k_mask_cells(const T *__restrict__ x, int N, int H, int W, int C, const float *__restrict__ wm, float bm,
+             uint8_t *__restrict__ mask, uint8_t *__restrict__ cell_cnt, int mode) {
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int ncw = (W + kCellCols - 1) / kCellCols;
+    const int cpi = cells_per_image(H, W);
+    const int64_t ncells = static_cast<int64_t>(N) * cpi;
+    const int64_t c = (static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + wave) * kCellsPerMaskWave + lane / kCellOwn;
+    const int o = lane % kCellOwn;
+    bool bit = false;
+    if (c < ncells) {
+        const int n = static_cast<int>(c / cpi), rem = static_cast<int>(c % cpi);
+        const int h = (rem / ncw) * kCellRows + o / kCellCols;
+        const int w = (rem % ncw) * kCellCols + o % kCellCols;
+        if (h < H && w < W) {
+            const int64_t pos = (static_cast<int64_t>(n) * H + h) * W + w;
+            uint4 row[kCellPieces];
+            const uint4 *src = reinterpret_cast<const uint4 *>(x + pos * C);
+#pragma unroll
+            for (int p = 0; p < kCellPieces; ++p)
+                row[p] = (p < C * static_cast<int>(sizeof(T)) / 16) ? src[p] : make_uint4(0, 0, 0, 0);
+            bit = cell_mask_row<T>(row, wm, C, bm, mode);
+            mask[pos] = bit ? 1 : 0;
+        }
+    }
+    const uint64_t b = __ballot(bit);
+    if (c < ncells && o == 0) cell_cnt[c] = static_cast<uint8_t>(group16_count(b, lane));
+}
+
+template <typename T, bool DENSE>
+__global__ void __launch_bounds__(kCellThreads)
+k_block_cells(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int W, int C, int E, int G,
+              const uint8_t *__restrict__ mask_in, const uint8_t *__restrict__ cnt_in,
+              const T *__restrict__ w1, const float *__restrict__ b1, int act1,
+              const T *__restrict__ w2, const float *__restrict__ b2, int act2,
+              const T *__restrict__ w3, const float *__restrict__ b3, int act3,
+              const float *__restrict__ wm_next, float bm_next, uint8_t *__restrict__ mask_next,
+              uint8_t *__restrict__ cnt_next, int32_t *__restrict__ band_counts, int mask_mode) {
+    typedef mma<T> M;
+    constexpr int per16 = 16 / static_cast<int>(sizeof(T));
+    __shared__ CellLds<T> L;
+    const int tid = threadIdx.x;
+    const int wave = tid / kWave, lane = tid % kWave;
+    const int r = lane % 16, g = lane / 16;
+    // XCD-aware: workgroup b runs on XCD b % 8 and takes share k, so each XCD
+    // holds a contiguous run of shares (cells next to each other share rings)
+    const int per_xcd = (G + 7) / 8;
+    const int k = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+    if (k >= G) return;  // uniform per workgroup
+    const int ncw = (W + kCellCols - 1) / kCellCols;
+    const int cpi = cells_per_image(H, W);
+    const int ncells = N * cpi;
+    const int E32 = (E + kChunk - 1) / kChunk * kChunk;
+
+    // ---- all weights of the block into LDS (zero past C and E): every
+    // thread's global loads are issued before its LDS stores
+    {
+        constexpr int kW1 = kCellMaxE * (kCellMaxC / 8), kW3 = kCellMaxC * (kCellMaxE / 8);
+        constexpr int kS1 = (kW1 + kCellThreads - 1) / kCellThreads, kS3 = (kW3 + kCellThreads - 1) / kCellThreads;
+        constexpr int kS2 = (kCellMaxE * 9 + kCellThreads - 1) / kCellThreads;
+        uint4 v1[kS1], v3[kS3];
+        T v2[kS2];
+#pragma unroll
+        for (int sl = 0; sl < kS1; ++sl) {
+            const int i = tid + sl * kCellThreads;
+            const int e = i / (kCellMaxC / 8), c8 = (i % (kCellMaxC / 8)) * 8;
+            v1[sl] = (e < E && c8 < C) ? *reinterpret_cast<const uint4 *>(w1 + static_cast<int64_t>(e) * C + c8)
+                                       : make_uint4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int sl = 0; sl < kS3; ++sl) {
+            const int i = tid + sl * kCellThreads;
+            const int c = i / (kCellMaxE / 8), e8 = (i % (kCellMaxE / 8)) * 8;
+            v3[sl] = (c < C && e8 < E) ? *reinterpret_cast<const uint4 *>(w3 + static_cast<int64_t>(c) * E + e8)
+                                       : make_uint4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int sl = 0; sl < kS2; ++sl) {
+            const int j = tid + sl * kCellThreads;
+            v2[sl] = (j < E * 9) ? w2[j] : static_cast<T>(0.0f);
+        }
+        float vb1 = 0.0f, vb2 = 0.0f, vb3 = 0.0f, vwm = 0.0f;
+        if (tid < kCellMaxE) {
+            vb1 = (tid < E) ? b1[tid] : 0.0f;
+            vb2 = (tid < E) ? b2[tid] : 0.0f;
+        }
+        if (tid < kCellMaxC) {
+            vb3 = (tid < C) ? b3[tid] : 0.0f;
+            vwm = (wm_next && tid < C) ? wm_next[tid] : 0.0f;
+        }
+#pragma unroll
+        for (int sl = 0; sl < kS1; ++sl) {
+            const int i = tid + sl * kCellThreads;
+            if (i < kW1) *reinterpret_cast<uint4 *>(&L.w.w1[i / (kCellMaxC / 8)][(i % (kCellMaxC / 8)) * 8]) = v1[sl];
+        }
+#pragma unroll
+        for (int sl = 0; sl < kS3; ++sl) {
+            const int i = tid + sl * kCellThreads;
+            if (i < kW3) *reinterpret_cast<uint4 *>(&L.w.w3[i / (kCellMaxE / 8)][(i % (kCellMaxE / 8)) * 8]) = v3[sl];
+        }
+#pragma unroll
+        for (int sl = 0; sl < kS2; ++sl) {
+            const int j = tid + sl * kCellThreads;
+            if (j < kCellMaxE * 9) L.w.w2[j % 9][j / 9] = v2[sl];
+        }
+        if (tid < kCellMaxE) {
+            L.w.b1[tid] = vb1;
+            L.w.b2[tid] = vb2;
+        }
+        if (tid < kCellMaxC) {
+            L.w.b3[tid] = vb3;
+            L.w.wm[tid] = vwm;
+        }
+    }
+
+    // ---- this workgroup's work.  Dense: cells [u_lo, u_hi), an equal share.
+    // Gated: the empty cells of [u_lo, u_hi) are streamed (a copy and the
+    // next mask unit, memory-bound, no ring needed), and the active cells are
+    // dealt in equal shares by count: share k is the active cells with rank
+    // [a_lo, a_hi) in raster order, listed in LDS from the per-cell active
+    // counts that the previous launch wrote.  So a dense region of the mask
+    // is spread over many CUs, and the span follows the active work.
+    const int u_lo = static_cast<int>(static_cast<int64_t>(k) * ncells / G);
+    const int u_hi = static_cast<int>(static_cast<int64_t>(k + 1) * ncells / G);
+    int a_lo = 0, a_hi = u_hi - u_lo;
+    // this thread's chunks of the count buffer and the rank of its first active cell
+    int my_rank = 0, my_cnt = 0, my_q0 = 0, my_q1 = 0;
+    uint32_t my_first = 0;
+    auto active_bits = [&](uint4 v, int i) {  // bit u: cell i + u is active
+        const uint32_t wd[4] = {v.x, v.y, v.z, v.w};
+        uint32_t bits = 0;
+#pragma unroll
+        for (int u = 0; u < 16; ++u)
+            if (i + u < ncells && ((wd[u / 4] >> (8 * (u % 4))) & 0xffu)) bits |= 1u << u;
+        return bits;
+    };
+    if (!DENSE) {
+        // a thread owns a contiguous run of 16-cell chunks, read as 16-byte
+        // words (the count buffers are padded to whole 256 bytes)
+        const int nchunks = (ncells + 15) / 16;
+        const int per = (nchunks + kCellThreads - 1) / kCellThreads;
+        const int q0 = tid * per, q1 = min(q0 + per, nchunks);
+        // the first chunk stays in registers for the listing pass (one chunk
+        // per thread up to 16384 cells)
+        const uint32_t first = (q0 < q1) ? active_bits(reinterpret_cast<const uint4 *>(cnt_in)[q0], q0 * 16) : 0u;
+        int cnt = __popc(first);
+        for (int q = q0 + 1; q < q1; ++q)
+            cnt += __popc(active_bits(reinterpret_cast<const uint4 *>(cnt_in)[q], q * 16));
+        const int incl = wave_scan_incl(cnt);
+        if (lane == kWave - 1) L.part[wave] = incl;
+        __syncthreads();
+        int before = 0, total = 0;
+#pragma unroll
+        for (int i = 0; i < kCellWaves; ++i) {
+            const int v = L.part[i];
+            before += (i < wave) ? v : 0;
+            total += v;
+        }
+        a_lo = static_cast<int>(static_cast<int64_t>(k) * total / G);
+        a_hi = static_cast<int>(static_cast<int64_t>(k + 1) * total / G);
+        my_rank = before + incl - cnt;
+        my_cnt = cnt;
+        my_q0 = q0;
+        my_q1 = q1;
+        my_first = first;
+    }
+    __syncthreads();  // the weights
+    // the bounds are the same in every lane: keep them in scalar registers,
+    // so that the cell loop below is uniform control flow (with a bound in a
+    // vector register the compiler may split the loop per lane, and lanes
+    // other than lane 0 would then reread the counter's start)
+    a_lo = __builtin_amdgcn_readfirstlane(a_lo);
+    a_hi = __builtin_amdgcn_readfirstlane(a_hi);
+
+    const float lo1 = act_lo(act1), hi1 = act_hi(act1);
+    const float lo2 = act_lo(act2), hi2 = act_hi(act2);
+    const float lo3 = act_lo(act3), hi3 = act_hi(act3);
+    const int nsl = E32 / kChunk;
+    const int npieces = C / per16;
+    const int rr = lane / kRegCols, cc = lane % kRegCols;    // this lane's region slot
+    const int oi = lane / kCellCols, oj = lane % kCellCols;  // this lane's own position (lane < 16)
+    const uint64_t lt = lanemask_lt(lane);
+    CellWaveLds<T> &V = L.wv[wave];
+    T(*ys)[kChunkPad] = reinterpret_cast<T(*)[kChunkPad]>(V.h1);  // own rows in the epilogue (C + 8 <= kChunkPad)
+
+    // ---- the empty cells of the range, as a stream over their positions
+    // (all threads, two items in flight per thread): y = x, the next block's
+    // mask unit, the cells' counts.  16 consecutive items are one cell,
+    // handled by one 16-lane group of a wave.
+    if (!DENSE) {
+        const int nitems = (u_hi - u_lo) * kCellOwn;
+        // the trip count is the wave's (its first item), so the loop is uniform
+        for (int b0 = wave * kWave; b0 < nitems; b0 += 2 * kCellThreads) {
+            uint4 row[2][kCellPieces];
+            int64_t pos[2];
+            bool take[2], empty[2];
+            int cellv[2];
+#pragma unroll
+            for (int kk = 0; kk < 2; ++kk) {
+                const int i = b0 + lane + kk * kCellThreads;
+                cellv[kk] = u_lo + i / kCellOwn;
+                empty[kk] = i < nitems && cnt_in[cellv[kk]] == 0;
+                const int o = i % kCellOwn;
+                const int rem = cellv[kk] % cpi;
+                const int h = (rem / ncw) * kCellRows + o / kCellCols;
+                const int w = (rem % ncw) * kCellCols + o % kCellCols;
+                take[kk] = empty[kk] && h < H && w < W;
+                pos[kk] = (static_cast<int64_t>(cellv[kk] / cpi) * H + h) * W + w;
+#pragma unroll
+                for (int p = 0; p < kCellPieces; ++p)
+                    row[kk][p] = (take[kk] && p < npieces) ? reinterpret_cast<const uint4 *>(xin + pos[kk] * C)[p]
+                                                           : make_uint4(0, 0, 0, 0);
+            }
+#pragma unroll
+            for (int kk = 0; kk < 2; ++kk) {
+                if (take[kk]) {
+                    uint4 *dst = reinterpret_cast<uint4 *>(yout + pos[kk] * C);
+#pragma unroll
+                    for (int p = 0; p < kCellPieces; ++p)
+                        if (p < npieces) dst[p] = row[kk][p];
+                }
+                bool bit = false;
+                if (take[kk] && mask_next) {
+                    bit = cell_mask_row<T>(row[kk], L.w.wm, C, bm_next, mask_mode);
+                    mask_next[pos[kk]] = bit ? 1 : 0;
+                }
+                const int cnt = group16_count(__ballot(bit), lane);
+                if (empty[kk] && mask_next) cnt_next[cellv[kk]] = static_cast<uint8_t>(cnt);
+                if (band_counts) {
+                    // no active position; dilated: own positions next to an
+                    // active position of a neighbouring cell
+                    bool dil = false;
+                    if (take[kk]) {
+                        const int h = static_cast<int>((pos[kk] / W) % H), w = static_cast<int>(pos[kk] % W);
+                        const int64_t img = pos[kk] / (static_cast<int64_t>(H) * W) * H;
+                        for (int dh = -1; dh <= 1; ++dh)
+                            for (int dw = -1; dw <= 1; ++dw) {
+                                const int hh = h + dh, ww = w + dw;
+                                if (hh >= 0 && hh < H && ww >= 0 && ww < W && mask_in[(img + hh) * W + ww] != 0)
+                                    dil = true;
+                            }
+                    }
+                    const int nd = group16_count(__ballot(dil), lane);
+                    if (empty[kk])
+                        *reinterpret_cast<int2 *>(band_counts + 2 * static_cast<int64_t>(cellv[kk])) = make_int2(0, nd);
+                }
+            }
+        }
+    }
+
+    // rounds of at most kCellList active cells (one round unless a share is
+    // larger than the list)
+    for (int r0 = a_lo; r0 < a_hi; r0 += kCellList) {
+    const int r1 = min(a_hi, r0 + kCellList);
+    if (!DENSE) {
+        // list the round's active cells (ranks r0 .. r1 - 1) in raster order
+        int rank = my_rank;
+        if (rank < r1 && rank + my_cnt > r0) {
+            for (int q = my_q0; q < my_q1; ++q) {
+                uint32_t bits = (q == my_q0) ? my_first
+                                              : active_bits(reinterpret_cast<const uint4 *>(cnt_in)[q], q * 16);
+                while (bits) {
+                    const int u = __ffs(bits) - 1;
+                    bits &= bits - 1;
+                    if (rank >= r0 && rank < r1) L.list[rank - r0] = q * 16 + u;
+                    ++rank;
+                }
+            }
+        }
+    }
+    if (tid == 0) L.next = 0;
+    __syncthreads();  // the list and the counter
+    for (;;) {
+        // every lane adds 1 (the counter advances by 64 per cell: one LDS
+        // atomic for the wave) and every lane below stores the cell's counts
+        // itself: no lane-0-only region next to the loop's back edge, which
+        // the compiler could split per lane
+        const int cn = atomicAdd(&L.next, 1);
+        const int item = (__builtin_amdgcn_readlane(cn, 0) >> 6) + r0;
+        if (item >= r1) break;  // uniform: both sides are scalar
+        const int cell = DENSE ? u_lo + item : __builtin_amdgcn_readfirstlane(L.list[item - r0]);
+        const int n = cell / cpi, rem = cell % cpi;
+        const int h0 = (rem / ncw) * kCellRows, w0 = (rem % ncw) * kCellCols;
+        const int64_t img = static_cast<int64_t>(n) * H;
+
+        // ---- 1. mask word of the region, active set, needed set, lists
+        const int hh = h0 - 1 + rr, ww = w0 - 1 + cc;
+        const bool inimg = lane < kRegSlots && hh >= 0 && hh < H && ww >= 0 && ww < W;
+        bool mb = false;
+        if (inimg) mb = DENSE ? true : (mask_in[(img + hh) * W + ww] != 0);
+        const uint64_t IMG = __ballot(inimg);
+        const uint64_t Gw = __ballot(mb);
+        const uint64_t A = Gw & kOwnBits;
+        uint64_t Dw = A | (A << 1) | (A >> 1);     // own columns 1..8: no row wrap
+        Dw |= (Dw << kRegCols) | (Dw >> kRegCols);
+        const uint64_t NEED = Dw & IMG;
+        if (!DENSE && band_counts) {
+            // the cell's active and dilated counts (its own positions whose 3x3
+            // neighbourhood holds an active position of any cell)
+            uint64_t Gd = Gw | ((Gw << 1) & ~kCol0Bits) | ((Gw >> 1) & ~kCol9Bits);
+            Gd |= (Gd << kRegCols) | (Gd >> kRegCols);
+            Gd &= kOwnBits & IMG;
+            *reinterpret_cast<int2 *>(band_counts + 2 * static_cast<int64_t>(cell)) =
+                make_int2(__popcll(A), __popcll(Gd));  // the same value from every lane
+        }
+
+        // the cell's own row of this lane (x; becomes y)
+        const int oh = h0 + oi, ow = w0 + oj;
+        const bool ov = lane < kCellOwn && oh < H && ow < W;
+        const int64_t opos = (img + oh) * W + ow;
+        uint4 xr[kCellPieces];
+
+        if (A != 0) {
+            const int nneed = __popcll(NEED);
+            const int ntn = (nneed + 15) >> 4;
+            if ((NEED >> lane) & 1ull) V.need[__popcll(NEED & lt)] = static_cast<int8_t>(lane);
+            if ((A >> lane) & 1ull) V.act[__popcll(A & lt)] = static_cast<int8_t>(lane);
+            if (lane < kRegSlots && !inimg) {  // the depthwise's zero padding
+                uint4 *z = reinterpret_cast<uint4 *>(V.h1 + slot_off(lane));
+#pragma unroll
+                for (int p = 0; p < kChunk * 2 / 16; ++p) z[p] = make_uint4(0, 0, 0, 0);
+            }
+            wave_sync();
+            // needed slots (the expansion's output rows, as byte offsets;
+            // padding lanes: the spare slot) and their B fragments, kept for
+            // every slice
+            int nq[kNeedTiles];
+            typename M::frag bx[kNeedTiles];
+#pragma unroll
+            for (int t = 0; t < kNeedTiles; ++t) {
+                const int i = 16 * t + r;
+                const int q = (i < nneed) ? static_cast<int>(V.need[i]) : -1;
+                nq[t] = (q >= 0) ? slot_off(q) : kSpareSlot;
+                const int qx = (q >= 0) ? q : kCellFirstOwn;  // an in-image slot
+                const int64_t p = (img + h0 - 1 + qx / kRegCols) * W + (w0 - 1 + qx % kRegCols);
+                bx[t] = (t < ntn && 8 * g < C) ? M::load(xin + p * C + 8 * g) : M::zero();
+            }
+            // the tile's active position of this lane (padding lanes: -1)
+            const int aq = (r < __popcll(A)) ? static_cast<int>(V.act[r]) : -1;
+            floatx4 acc[2];
+#pragma unroll
+            for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) acc[mt][v] = L.w.b3[mt * 16 + 4 * g + v];
+            // padding lanes compute around an own slot; their projection
+            // columns are never stored
+            const char *own = V.h1 + slot_off(aq >= 0 ? aq : kCellFirstOwn) + 16 * g;
+
+            for (int ec = 0; ec < nsl; ++ec) {
+                const int eb = ec * kChunk;
+                // ---- 2a. expansion of the needed slots into the region array:
+                // the tiles' products issued back to back, then activated
+                typename M::frag a1[2];
+                floatx4 bi[2];
+#pragma unroll
+                for (int m = 0; m < 2; ++m) {
+                    a1[m] = M::load(&L.w.w1[eb + m * 16 + r][8 * g]);
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) bi[m][v] = L.w.b1[eb + m * 16 + 4 * g + v];
+                }
+                auto expand = [&](auto ntiles) {
+                    constexpr int NTL = decltype(ntiles)::value;
+                    floatx4 d[NTL][2];
+#pragma unroll
+                    for (int t = 0; t < NTL; ++t)
+#pragma unroll
+                        for (int m = 0; m < 2; ++m) d[t][m] = M::run(a1[m], bx[t], bi[m]);
+#pragma unroll
+                    for (int t = 0; t < NTL; ++t)
+#pragma unroll
+                        for (int m = 0; m < 2; ++m) {
+                            float o[4];
+#pragma unroll
+                            for (int v = 0; v < 4; ++v) o[v] = clamp_act(d[t][m][v], lo1, hi1);
+                            // a tile past the needed ones stores into the spare slot
+                            io<T>::store4(reinterpret_cast<T *>(V.h1 + nq[t]) + m * 16 + 4 * g, o);
+                        }
+                };
+                if (ntn == 3) expand(std::integral_constant<int, 3>());
+                else if (ntn == 2) expand(std::integral_constant<int, 2>());
+                else expand(std::integral_constant<int, 1>());
+                wave_sync();
+                // ---- 2b. depthwise at the tile's active positions + projection slice
+                typename M::frag a3[2];
+#pragma unroll
+                for (int mt = 0; mt < 2; ++mt) a3[mt] = M::load(&L.w.w3[mt * 16 + r][eb + 8 * g]);
+                typename io<T>::vec8 tv[9];
+#pragma unroll
+                for (int t = 0; t < 9; ++t)
+                    tv[t] = io<T>::raw8(reinterpret_cast<const T *>(
+                        own + (t / 3 - 1) * kRegPitch + (t % 3 - 1) * kSlotBytes));
+                float s[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) s[u] = L.w.b2[eb + 8 * g + u];
+#pragma unroll
+                for (int t = 0; t < 9; ++t) {
+                    const typename io<T>::vec8 wk = io<T>::raw8(&L.w.w2[t][eb + 8 * g]);
+#pragma unroll
+                    for (int u = 0; u < 8; ++u)
+                        s[u] = __builtin_fmaf(static_cast<float>(wk[u]), static_cast<float>(tv[t][u]), s[u]);
+                }
+                float hv[8];
+#pragma unroll
+                for (int u = 0; u < 8; ++u) hv[u] = clamp_act(s[u], lo2, hi2);
+                const typename M::frag bf = M::pack(hv);
+#pragma unroll
+                for (int mt = 0; mt < 2; ++mt) acc[mt] = M::run(a3[mt], bf, acc[mt]);
+                wave_sync();
+            }
+
+            // ---- 3a. residual sum at the active positions, on the own rows
+#pragma unroll
+            for (int p = 0; p < kCellPieces; ++p)
+                xr[p] = (ov && p < npieces) ? reinterpret_cast<const uint4 *>(xin + opos * C)[p] : make_uint4(0, 0, 0, 0);
+            if (ov) {
+#pragma unroll
+                for (int p = 0; p < kCellPieces; ++p)
+                    if (p < npieces) reinterpret_cast<uint4 *>(&ys[lane][0])[p] = xr[p];
+            }
+            wave_sync();
+            if (aq >= 0) {
+                const int o = (aq / kRegCols - 1) * kCellCols + (aq % kRegCols - 1);
+#pragma unroll
+                for (int mt = 0; mt < 2; ++mt) {
+                    const int c0 = mt * 16 + 4 * g;
+                    if (c0 < C) {
+                        float xv[4], out[4];
+                        io<T>::load4(&ys[o][c0], xv);
+#pragma unroll
+                        for (int v = 0; v < 4; ++v) out[v] = xv[v] + clamp_act(acc[mt][v], lo3, hi3);
+                        io<T>::store4(&ys[o][c0], out);
+                    }
+                }
+            }
+            wave_sync();
+            if (ov) {
+#pragma unroll
+                for (int p = 0; p < kCellPieces; ++p)
+                    if (p < npieces) xr[p] = reinterpret_cast<const uint4 *>(&ys[lane][0])[p];
+            }
+            wave_sync();  // the own rows are read before the next cell's lists
+        } else {
+#pragma unroll
+            for (int p = 0; p < kCellPieces; ++p)
+                xr[p] = (ov && p < npieces) ? reinterpret_cast<const uint4 *>(xin + opos * C)[p] : make_uint4(0, 0, 0, 0);
+        }
+
+        // ---- 3b. store the cell, the next block's mask unit on the stored values
+        if (ov) {
+            uint4 *dst = reinterpret_cast<uint4 *>(yout + opos * C);
+#pragma unroll
+            for (int p = 0; p < kCellPieces; ++p)
+                if (p < npieces) dst[p] = xr[p];
+        }
+        if (!DENSE && mask_next) {
+            bool bit = false;
+            if (ov) {
+                bit = cell_mask_row<T>(xr, L.w.wm, C, bm_next, mask_mode);
+                mask_next[opos] = bit ? 1 : 0;
+            }
+            const uint64_t b = __ballot(bit);
+            cnt_next[cell] = static_cast<uint8_t>(__popcll(b));  // the same value from every lane
+        }
+    }
+    __syncthreads();  // every wave is done with the list before it is rebuilt
+    }
+}
+
+}  // namespace dynconv

@@ -11,6 +11,7 @@
 #include <string.h>
 
 #include "dynconv.h"
+#include "cells.h"
 #include "fused.h"
 #include "kernels.h"
 #include "shuffle.h"
@@ -143,6 +144,13 @@ IndexScratch carve_index_scratch(void *ws, dynconv_shape s) {
 // the expanded tensor: N*H*W rows plus one all-zero row for missing neighbours
 size_t hidden_bytes(dynconv_shape s, int E, dynconv_dtype dt) {
     return align_up((static_cast<size_t>(positions(s)) + 1) * E * dtype_size(dt));
+}
+
+// base + off as an address.  The walks that only list launch names pass a
+// null base and never dereference: integer arithmetic keeps that defined.
+template <typename P = char>
+P *at(const void *base, size_t off) {
+    return reinterpret_cast<P *>(reinterpret_cast<uintptr_t>(base) + off);
 }
 
 // ------------------------------------------------------------ launches
@@ -353,6 +361,77 @@ void dispatch_fused(dynconv_dtype dt, bool dense, const void *src, void *dst, dy
 #undef DC_FUSED
 }
 
+// ------------------------------------------------------------ balanced cells
+// Compute units of the current device (the persistent grid of k_block_cells).
+int device_cus() {
+    static std::atomic<int> cached[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    int v = cached[dev].load(std::memory_order_relaxed);
+    if (v <= 0) {
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0)
+            v = 256;
+        cached[dev].store(v, std::memory_order_relaxed);
+    }
+    return v;
+}
+
+int64_t cell_count(dynconv_shape s) { return static_cast<int64_t>(s.n) * cells_per_image(s.h, s.w); }
+
+// Persistent grid: at most one workgroup per CU, at least one cell per wave.
+int cells_shares(dynconv_shape s) {
+    const int64_t by_cells = (cell_count(s) + kCellWaves - 1) / kCellWaves;
+    return static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(device_cus(), by_cells)));
+}
+
+template <typename T>
+void launch_mask_cells(const void *x, dynconv_shape s, const dynconv_block *b, uint8_t *mask, uint8_t *cnt,
+                       int mode, hipStream_t st, Marks &mk) {
+    const int64_t per_group = static_cast<int64_t>(kCellsPerMaskWave) * kWavesPerBlock;
+    const int64_t grid = (cell_count(s) + per_group - 1) / per_group;
+    launch(mk, k_mask_cells<T>, dim3(static_cast<unsigned>(grid)), dim3(kBlock), 0, st, static_cast<const T *>(x),
+           s.n, s.h, s.w, s.c, b->w_mask, b->b_mask, mask, cnt, mode);
+}
+
+struct CellMasks {
+    const uint8_t *mask_in = nullptr, *cnt_in = nullptr;
+    uint8_t *mask_next = nullptr, *cnt_next = nullptr;
+    int32_t *band_counts = nullptr;
+    int mask_mode = 0;
+};
+
+template <typename T, bool DENSE>
+void launch_cells(const void *src, void *dst, dynconv_shape s, const dynconv_block *b, const dynconv_block *next,
+                  const CellMasks &cm, hipStream_t st, Marks &mk) {
+    const int G = cells_shares(s);
+    const int grid = (G + 7) / 8 * 8;
+    launch(mk, k_block_cells<T, DENSE>, dim3(grid), dim3(kCellThreads), 0, st, static_cast<const T *>(src),
+           static_cast<T *>(dst), s.n, s.h, s.w, s.c, b->c_hidden, G, cm.mask_in, cm.cnt_in,
+           static_cast<const T *>(b->w_expand), b->b_expand, b->act_expand,
+           static_cast<const T *>(b->w_dw), b->b_dw, b->act_dw,
+           static_cast<const T *>(b->w_project), b->b_project, b->act_project,
+           next ? next->w_mask : nullptr, next ? next->b_mask : 0.0f, next ? cm.mask_next : nullptr,
+           next ? cm.cnt_next : nullptr, cm.band_counts, cm.mask_mode);
+}
+
+void dispatch_cells(dynconv_dtype dt, bool dense, const void *src, void *dst, dynconv_shape s,
+                    const dynconv_block *b, const dynconv_block *next, const CellMasks &cm, hipStream_t st,
+                    Marks &mk) {
+    if (dt == DYNCONV_F16) {
+        if (dense) launch_cells<half_t, true>(src, dst, s, b, nullptr, cm, st, mk);
+        else launch_cells<half_t, false>(src, dst, s, b, next, cm, st, mk);
+    } else {
+        if (dense) launch_cells<bf16_t, true>(src, dst, s, b, nullptr, cm, st, mk);
+        else launch_cells<bf16_t, false>(src, dst, s, b, next, cm, st, mk);
+    }
+}
+
+void dispatch_mask_cells(dynconv_dtype dt, const void *x, dynconv_shape s, const dynconv_block *b, uint8_t *mask,
+                         uint8_t *cnt, int mode, hipStream_t st, Marks &mk) {
+    if (dt == DYNCONV_F16) launch_mask_cells<half_t>(x, s, b, mask, cnt, mode, st, mk);
+    else launch_mask_cells<bf16_t>(x, s, b, mask, cnt, mode, st, mk);
+}
+
 void dispatch_block(dynconv_dtype dt, const void *x, void *y, dynconv_shape s, const dynconv_block *b,
                     const dynconv_indices *idx, void *h1, hipStream_t st, Marks &mk) {
     if (dt == DYNCONV_F32) launch_block<float>(x, y, s, b, idx, h1, st, mk);
@@ -374,18 +453,39 @@ bool use_fused(dynconv_shape s, dynconv_dtype dt, int32_t flags) {
     return !(flags & kStackUnfused) && s.c <= (dt == DYNCONV_F32 ? kMaxFusedC : kMaxFusedC16);
 }
 
+// Narrow 16-bit blocks (at most 32 channels, 192 hidden) run the
+// work-balanced cell kernel, which keeps all weights of a block in LDS.
+bool use_cells(dynconv_shape s, dynconv_dtype dt, const dynconv_block *blks, int32_t n_blocks, int32_t flags) {
+    if ((flags & kStackUnfused) || dt == DYNCONV_F32 || s.c > kCellMaxC) return false;
+    for (int32_t b = 0; b < n_blocks; ++b)
+        if (blks[b].c_hidden > kCellMaxE) return false;
+    return true;
+}
+
 struct StackLayout {
-    bool fused;
-    size_t masks, mask2, tbuf, active, dilated, nbr, counts, bands, scratch, hidden, total;
+    bool fused, cells;
+    size_t masks, mask2, tbuf, active, dilated, nbr, counts, bands, scratch, hidden, cc0, cc1, total;
 };
 
+// allow_cells: the ShuffleNetV2 units run their branch on the patch kernel
+// (its staging reads the unit's rows directly), never on the cell kernel.
 StackLayout stack_layout(dynconv_shape s, const dynconv_block *blks, int32_t n_blocks,
-                         dynconv_dtype dt, int32_t flags) {
+                         dynconv_dtype dt, int32_t flags, bool allow_cells = true) {
     StackLayout L{};
     L.fused = use_fused(s, dt, flags);
+    L.cells = allow_cells && L.fused && use_cells(s, dt, blks, n_blocks, flags);
     size_t npos = static_cast<size_t>(positions(s));
     size_t off = 0;
-    if (L.fused) {
+    if (L.cells) {
+        const size_t ncells = static_cast<size_t>(cell_count(s));
+        L.tbuf = off;   off += align_up(npos * s.c * dtype_size(dt));
+        L.masks = off;  off += align_up(npos);
+        L.mask2 = off;  off += align_up(npos);
+        L.counts = off; off += align_up(8 * static_cast<size_t>(n_blocks));
+        L.bands = off;  off += align_up(8 * static_cast<size_t>(n_blocks) * ncells);
+        L.cc0 = off;    off += align_up(ncells);
+        L.cc1 = off;    off += align_up(ncells);
+    } else if (L.fused) {
         L.tbuf = off;   off += align_up(npos * s.c * dtype_size(dt));
         L.masks = off;  off += align_up(npos);
         L.mask2 = off;  off += align_up(npos);
@@ -443,10 +543,10 @@ void stack_walk(const void *x, void *y, dynconv_shape s, dynconv_dtype dt, const
     const bool dense = flags & kStackDense;
     const size_t npos = static_cast<size_t>(positions(s));
     const size_t bytes = npos * s.c * dtype_size(dt);
-    int32_t *cnt_all = counts ? counts : reinterpret_cast<int32_t *>(base + L.counts);
-    if (L.fused) {
+    int32_t *cnt_all = counts ? counts : at<int32_t>(base, L.counts);
+    if (L.cells) {
         // Ping-pong between y and a scratch copy so that the last block writes y.
-        void *tb = base + L.tbuf;
+        void *tb = at(base, L.tbuf);
         const void *src = x;
         if (in_place && (n_blocks % 2 == 1)) {
             if (plan.note("k_copy16")) launch_copy(x, tb, bytes, st, mk);  // keeps y free for block 0
@@ -454,10 +554,48 @@ void stack_walk(const void *x, void *y, dynconv_shape s, dynconv_dtype dt, const
         }
         auto mask_of = [&](int32_t b) -> uint8_t * {
             if (masks) return masks + static_cast<size_t>(b) * npos;
-            return reinterpret_cast<uint8_t *>(base + ((b % 2) ? L.mask2 : L.masks));
+            return at<uint8_t>(base, ((b % 2) ? L.mask2 : L.masks));
+        };
+        auto cnt_of = [&](int32_t b) -> uint8_t * {
+            return at<uint8_t>(base, ((b % 2) ? L.cc1 : L.cc0));
+        };
+        const int64_t ncells = cell_count(s);
+        int32_t *band_counts = at<int32_t>(base, L.bands);
+        // the first block's mask unit and its per-cell active counts
+        if (!dense && plan.note("k_mask_cells"))
+            dispatch_mask_cells(dt, src, s, &blks[0], mask_of(0), cnt_of(0), mask_mode_of(flags), st, mk);
+        for (int32_t b = 0; b < n_blocks; ++b) {
+            void *dst = ((n_blocks - 1 - b) % 2 == 0) ? y : tb;
+            const dynconv_block *next = (b + 1 < n_blocks) ? &blks[b + 1] : nullptr;
+            CellMasks cm;
+            cm.mask_mode = mask_mode_of(flags);
+            cm.mask_in = mask_of(b);
+            cm.cnt_in = cnt_of(b);
+            cm.mask_next = next ? mask_of(b + 1) : nullptr;
+            cm.cnt_next = next ? cnt_of(b + 1) : nullptr;
+            cm.band_counts = counts ? band_counts + static_cast<size_t>(2) * ncells * b : nullptr;
+            if (plan.note("k_block_cells")) dispatch_cells(dt, dense, src, dst, s, &blks[b], next, cm, st, mk);
+            src = dst;
+        }
+        if (!dense && (counts || (!plan.exec && plan.list_counts)) && plan.note("k_band_counts"))
+            launch(mk, k_band_counts, dim3(n_blocks), dim3(kBlock), 0, st,
+                   static_cast<const int32_t *>(band_counts), static_cast<int>(ncells), cnt_all);
+        return;
+    }
+    if (L.fused) {
+        // Ping-pong between y and a scratch copy so that the last block writes y.
+        void *tb = at(base, L.tbuf);
+        const void *src = x;
+        if (in_place && (n_blocks % 2 == 1)) {
+            if (plan.note("k_copy16")) launch_copy(x, tb, bytes, st, mk);  // keeps y free for block 0
+            src = tb;
+        }
+        auto mask_of = [&](int32_t b) -> uint8_t * {
+            if (masks) return masks + static_cast<size_t>(b) * npos;
+            return at<uint8_t>(base, ((b % 2) ? L.mask2 : L.masks));
         };
         const int nbands = fused_patch_count(s, dt);
-        int32_t *band_counts = reinterpret_cast<int32_t *>(base + L.bands);
+        int32_t *band_counts = at<int32_t>(base, L.bands);
         for (int32_t b = 0; b < n_blocks; ++b) {
             void *dst = ((n_blocks - 1 - b) % 2 == 0) ? y : tb;
             const dynconv_block *next = (b + 1 < n_blocks) ? &blks[b + 1] : nullptr;
@@ -479,7 +617,7 @@ void stack_walk(const void *x, void *y, dynconv_shape s, dynconv_dtype dt, const
     }
     // Unfused chain, in place on y.
     if (!in_place && plan.note("k_copy16")) launch_copy(x, y, bytes, st, mk);
-    void *h1 = base + L.hidden;
+    void *h1 = at(base, L.hidden);
     if (dense) {
         for (int32_t b = 0; b < n_blocks; ++b) {
             bool run = plan.note("k_expand");
@@ -489,14 +627,14 @@ void stack_walk(const void *x, void *y, dynconv_shape s, dynconv_dtype dt, const
         return;
     }
     dynconv_indices idx;
-    idx.active = reinterpret_cast<int32_t *>(base + L.active);
-    idx.dilated = reinterpret_cast<int32_t *>(base + L.dilated);
-    idx.nbr = reinterpret_cast<int32_t *>(base + L.nbr);
+    idx.active = at<int32_t>(base, L.active);
+    idx.dilated = at<int32_t>(base, L.dilated);
+    idx.nbr = at<int32_t>(base, L.nbr);
     idx.capacity = static_cast<int64_t>(npos);
-    void *scratch = base + L.scratch;
+    void *scratch = at(base, L.scratch);
     for (int32_t b = 0; b < n_blocks; ++b) {
         uint8_t *mask_b = masks ? masks + static_cast<size_t>(b) * npos
-                                : reinterpret_cast<uint8_t *>(base + L.masks);
+                                : at<uint8_t>(base, L.masks);
         idx.counts = cnt_all + 2 * b;
         bool run = plan.note("k_mask");
         plan.note("k_rowcount");
@@ -550,7 +688,7 @@ ShuffleLayout shuffle_layout(dynconv_shape s, const dynconv_block *br, int32_t n
     L.xb = off;    off += rows;
     L.full = off;  off += (n_units > 1) ? align_up(npos * s.c * dtype_size(dt)) : 0;
     L.inner = off;
-    L.in = stack_layout(bs, br, n_units, dt, flags);
+    L.in = stack_layout(bs, br, n_units, dt, flags, false);
     off += L.in.total;
     L.total = off;
     return L;
@@ -611,13 +749,13 @@ void shuffle_walk(const void *x, void *y, dynconv_shape s, dynconv_dtype dt, con
     const int cb = s.c / 2, cp = bs.c;
     const int64_t npos = positions(s);
     const StackLayout &L = SL.in;
-    char *ib = base + SL.inner;
-    void *bufs[2] = {base + SL.xa, base + SL.xb};
-    void *full = base + SL.full;
-    int32_t *cnt_all = counts ? counts : reinterpret_cast<int32_t *>(ib + L.counts);
+    char *ib = at(base, SL.inner);
+    void *bufs[2] = {at(base, SL.xa), at(base, SL.xb)};
+    void *full = at(base, SL.full);
+    int32_t *cnt_all = counts ? counts : at<int32_t>(ib, L.counts);
     auto mask_of = [&](int32_t u) -> uint8_t * {
         if (masks) return masks + static_cast<size_t>(u) * npos;
-        return reinterpret_cast<uint8_t *>(ib + L.masks);
+        return at<uint8_t>(ib, L.masks);
     };
     auto out_of = [&](int32_t u) -> void * { return ((n_units - 1 - u) % 2 == 0) ? y : full; };
     // branch input of unit u: bufs[0] for the one-launch block (its output
@@ -625,7 +763,7 @@ void shuffle_walk(const void *x, void *y, dynconv_shape s, dynconv_dtype dt, con
     auto in_of = [&](int32_t u) -> void * { return L.fused ? bufs[0] : bufs[u % 2]; };
 
     const int nbands = L.fused ? fused_patch_count(bs, dt) : 0;
-    int32_t *band_counts = reinterpret_cast<int32_t *>(ib + L.bands);
+    int32_t *band_counts = at<int32_t>(ib, L.bands);
     if (SL.direct) {
         for (int32_t u = 0; u < n_units; ++u) {
             FusedMasks fm;
@@ -646,9 +784,9 @@ void shuffle_walk(const void *x, void *y, dynconv_shape s, dynconv_dtype dt, con
     }
     if (plan.note("k_shuffle_split")) dispatch_split(dt, x, in_of(0), npos, cb, cp, st, mk);
     dynconv_indices idx;
-    idx.active = reinterpret_cast<int32_t *>(ib + L.active);
-    idx.dilated = reinterpret_cast<int32_t *>(ib + L.dilated);
-    idx.nbr = reinterpret_cast<int32_t *>(ib + L.nbr);
+    idx.active = at<int32_t>(ib, L.active);
+    idx.dilated = at<int32_t>(ib, L.dilated);
+    idx.nbr = at<int32_t>(ib, L.nbr);
     idx.capacity = npos;
     for (int32_t u = 0; u < n_units; ++u) {
         const void *xu = (u == 0) ? x : out_of(u - 1);
@@ -668,7 +806,7 @@ void shuffle_walk(const void *x, void *y, dynconv_shape s, dynconv_dtype dt, con
         } else if (dense) {
             bool run = plan.note("k_expand");
             plan.note("k_dw_project");
-            if (run) dispatch_block(dt, bin, bin, bs, &br[u], nullptr, ib + L.hidden, st, mk);
+            if (run) dispatch_block(dt, bin, bin, bs, &br[u], nullptr, at(ib, L.hidden), st, mk);
         } else {
             idx.counts = cnt_all + 2 * u;
             bool run = plan.note("k_mask");
@@ -680,8 +818,8 @@ void shuffle_walk(const void *x, void *y, dynconv_shape s, dynconv_dtype dt, con
             if (run) {
                 dispatch_mask(dt, bin, bs, br[u].w_mask, br[u].b_mask, mask_of(u), nullptr, mask_mode_of(flags),
                               st, mk);
-                launch_indices(mask_of(u), bs, 1, &idx, ib + L.scratch, st, mk);
-                dispatch_block(dt, bin, bin, bs, &br[u], &idx, ib + L.hidden, st, mk);
+                launch_indices(mask_of(u), bs, 1, &idx, at(ib, L.scratch), st, mk);
+                dispatch_block(dt, bin, bin, bs, &br[u], &idx, at(ib, L.hidden), st, mk);
             }
         }
         void *next_in = (u + 1 < n_units) ? in_of(u + 1) : nullptr;
@@ -1003,9 +1141,9 @@ void launch_expand_dw(const void *x, dynconv_shape in, dynconv_shape out, const 
 void net_walk(const void *x, void *y, dynconv_shape in, dynconv_dtype dt, const dynconv_layer *layers,
               int32_t n, int32_t flags, uint8_t *masks, int32_t *counts, char *base, const NetLayout &NL,
               hipStream_t st, Marks &mk, Plan &plan) {
-    void *bufs[2] = {base + NL.act0, base + NL.act1};
-    void *h1 = base + NL.h1, *h2 = base + NL.h2;
-    char *inner = base + NL.inner;
+    void *bufs[2] = {at(base, NL.act0), at(base, NL.act1)};
+    void *h1 = at(base, NL.h1), *h2 = at(base, NL.h2);
+    char *inner = at(base, NL.inner);
     dynconv_shape cur = in;
     const void *src = x;
     size_t moff = 0;
@@ -1094,7 +1232,7 @@ dynconv_status static_scratch(char **out) {
 // ================================================================ C ABI
 extern "C" {
 
-const char *dynconv_status_str(dynconv_status status) {
+const char *dynconv_status_str(int32_t status) {
     switch (status) {
     case DYNCONV_OK: return "ok";
     case DYNCONV_ERR_NULL: return "required pointer is NULL";

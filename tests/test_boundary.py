@@ -27,6 +27,10 @@ def declared_functions():
 
 @pytest.fixture(scope="module")
 def lib():
+    # the sanitizer tests point this at an instrumented host-only build
+    override = os.environ.get("DYNCONV_TEST_LIB")
+    if override:
+        return dc.load(override)
     if not os.path.exists(dc.LIB_PATH):
         from paper_1912_03203_amd import build
 
@@ -133,11 +137,21 @@ def test_stack_validation(lib):
     def up(v):
         return (v + 255) // 256 * 256
 
-    # one-launch blocks: ping-pong copy of x, two masks, counts, per-patch
-    # counts (fp16 at 32 channels: 16 x 16 images give one patch per image at
-    # full height; a batch this small gets patches of one row, 64 in all)
+    # 16-bit blocks of at most 32 channels and 192 hidden: the cell kernel's
+    # ping-pong copy of x, two masks, counts, per-cell counts (2 x 8 cells:
+    # 16 per 16 x 16 image) and two per-cell active-count buffers
     fused = lib.dynconv_stack_workspace_bytes(s, blocks, 3, 1, 0)
-    assert fused == up(npos * 32 * 2) + 2 * up(npos) + up(8 * 3) + up(8 * 3 * 64)
+    ncells = 4 * 8 * 2
+    assert fused == up(npos * 32 * 2) + 2 * up(npos) + up(8 * 3) + up(8 * 3 * ncells) + 2 * up(ncells)
+    # fp32: the patch kernel's ping-pong copy, two masks, counts, per-patch
+    # counts (16 x 16 images give one patch per image at full height; a batch
+    # this small gets patches of one row, 64 in all)
+    assert lib.dynconv_stack_workspace_bytes(s, blocks, 3, 0, 0) == \
+        up(npos * 32 * 4) + 2 * up(npos) + up(8 * 3) + up(8 * 3 * 64)
+    # a hidden width above 192 leaves the cell kernel for the patch kernel
+    e384 = (dc.Block * 1)(fake_block(E=384))
+    assert lib.dynconv_stack_workspace_bytes(s, e384, 1, 1, 0) == \
+        up(npos * 32 * 2) + 2 * up(npos) + up(8) + up(8 * 64)
     # kernel chain: mask, lists, counts, row scratch, hidden tensor of the widest block
     need = lib.dynconv_stack_workspace_bytes(s, blocks, 3, 1, 2)
     assert need == (npos + 4 * npos + 4 * npos + 36 * npos + up(8 * 3) + up(8 * rows)
@@ -153,11 +167,14 @@ def test_stack_validation(lib):
     blk96 = (dc.Block * 1)(fake_block(C=96, E=576))
     assert lib.dynconv_stack_workspace_bytes(c96, blk96, 1, 1, 0) != \
         lib.dynconv_stack_workspace_bytes(c96, blk96, 1, 1, 2)
-    # wide images stay on the one-launch path: column strips of 25, and for
-    # a batch this small row strips of 1 (16 patches)
+    # wide images stay on the one-launch paths: 26 cells of 2 x 8; for the
+    # patch kernel (fp32) column strips of 25 and, for a batch this small,
+    # row strips of 1 (16 patches)
     wide = dc.Shape(1, 4, 100, 32)
     assert lib.dynconv_stack_workspace_bytes(wide, blocks, 3, 1, 0) == \
-        up(400 * 32 * 2) + 2 * up(400) + up(8 * 3) + up(8 * 3 * 16)
+        up(400 * 32 * 2) + 2 * up(400) + up(8 * 3) + up(8 * 3 * 26) + 2 * up(26)
+    assert lib.dynconv_stack_workspace_bytes(wide, blocks, 3, 0, 0) == \
+        up(400 * 32 * 4) + 2 * up(400) + up(8 * 3) + up(8 * 3 * 16)
     f = lib.dynconv_stack_forward
     assert f(None, FAKE, s, 1, blocks, 3, 0, None, None, FAKE, need, None) == ERR_NULL
     assert f(FAKE, None, s, 1, blocks, 3, 0, None, None, FAKE, need, None) == ERR_NULL
@@ -173,7 +190,7 @@ def test_stack_validation(lib):
     assert lib.dynconv_stack_workspace_bytes(s, blocks, 0, 1, 0) == 0
     pf = lib.dynconv_stack_forward_profiled
     ev = (ctypes.c_void_p * 6)(*([FAKE] * 6))
-    # 3 block launches (the first runs its own mask unit) + 1 count reduction need 8 events
+    # the first block's mask unit, 3 block launches and the count reduction need 10 events
     assert pf(FAKE, FAKE, s, 1, blocks, 3, 0, None, None, FAKE, fused, None, ev, 6) == ERR_ARG
     assert pf(FAKE, FAKE, s, 1, blocks, 3, 0, None, None, FAKE, fused, None, None, 8) == ERR_NULL
 
@@ -188,13 +205,20 @@ def test_stack_launch_plans(lib):
         lib.dynconv_stack_launch_names(shape, arr, n, 1, flags, in_place, out, total)
         return [x.decode() for x in out]
 
-    assert names(0, 0) == ["k_block_fused"] * 8 + ["k_band_counts"]
-    assert names(1, 1) == ["k_block_fused"] * 8
-    assert names(0, 1, n=3) == ["k_copy16"] + ["k_block_fused"] * 3 + ["k_band_counts"]
+    assert names(0, 0) == ["k_mask_cells"] + ["k_block_cells"] * 8 + ["k_band_counts"]
+    assert names(1, 1) == ["k_block_cells"] * 8
+    assert names(0, 1, n=3) == ["k_copy16", "k_mask_cells"] + ["k_block_cells"] * 3 + ["k_band_counts"]
+    assert names(5, 0) == ["k_block_cells"] * 8  # dense wins over G-Softmax: no mask units
+    wide_e = (dc.Block * 2)(*([fake_block(E=256)] * 2))
+    total = lib.dynconv_stack_launch_names(s, wide_e, 2, 1, 0, 0, None, 0)
+    out = (ctypes.c_char_p * total)()
+    lib.dynconv_stack_launch_names(s, wide_e, 2, 1, 0, 0, out, total)
+    assert [x.decode() for x in out] == ["k_block_fused"] * 2 + ["k_band_counts"]
     assert names(2, 1) == ["k_mask", "k_rowcount", "k_rowscan", "k_compact", "k_expand",
                            "k_dw_project"] * 8
     assert names(3, 0) == ["k_copy16"] + ["k_expand", "k_dw_project"] * 8
-    assert names(0, 1, shape=dc.Shape(2, 8, 300, 32), n=2) == ["k_block_fused"] * 2 + ["k_band_counts"]
+    assert names(0, 1, shape=dc.Shape(2, 8, 300, 32), n=2) == \
+        ["k_mask_cells"] + ["k_block_cells"] * 2 + ["k_band_counts"]
     arr136 = (dc.Block * 2)(*([fake_block(C=136)] * 2))
     total = lib.dynconv_stack_launch_names(dc.Shape(2, 8, 8, 136), arr136, 2, 1, 0, 1, None, 0)
     out = (ctypes.c_char_p * total)()

@@ -25,18 +25,37 @@ def _lib():
 def run_stack(x_np, blocks_np, biases, dtype, flags=0, in_place=False):
     dt = dc.NAME_TO_DTYPE[dtype]
     bw = [dc.BlockWeights.from_arrays(w, dt, b_mask=b) for w, b in zip(blocks_np, biases)]
-    x = to_dev(x_np, dtype)
-    n, h, w, _ = x.shape
+    n, h, w, c = x_np.shape
     nb = len(bw)
-    masks = torch.full((nb, n * h * w), 7, dtype=torch.uint8, device=DEV)
-    counts = torch.full((nb, 2), -5, dtype=torch.int32, device=DEV)
-    y = x if in_place else torch.full_like(x, float("nan"))
-    stack = dc.Stack(x, y, bw, flags=flags, masks=masks, counts=counts)
+    # every buffer the call writes is followed by guard bytes
+    xg = util.Guarded(n * h * w * c, dc.NAME_TO_DTYPE[dtype], fill=None)
+    x = xg.t.view(n, h, w, c)
+    x.copy_(to_dev(x_np, dtype))
+    mg = util.Guarded(nb * n * h * w, torch.uint8, fill=7)
+    cg = util.Guarded(nb * 2, torch.int32, fill=-5)
+    masks, counts = mg.t.view(nb, n * h * w), cg.t.view(nb, 2)
+    yg = xg if in_place else util.Guarded(x.numel(), x.dtype, fill=float("nan"))
+    y = x if in_place else yg.t.view(x.shape)
+    wsg = util.Guarded(dc.stack_workspace_bytes(dc.shape_of(x), bw, x.dtype, flags), torch.uint8, fill=None)
+    stack = dc.Stack(x, y, bw, flags=flags, masks=masks, counts=counts, ws=wsg.t)
     stack()
     torch.cuda.synchronize()
+    assert all(g.intact() for g in (xg, mg, cg, yg, wsg)), "a buffer written past its end"
     if not in_place:
         assert host(x).tobytes() == np.asarray(x_np, np.float32).tobytes()  # input untouched
     return {"y": y, "masks": masks, "counts": counts, "names": stack.launch_names()}
+
+
+def uses_cells(dtype, C, E):
+    """Narrow 16-bit blocks run the work-balanced cell kernel, the others the
+    patch kernel."""
+    return dtype != "f32" and C <= 32 and E <= 192
+
+
+def expected_launches(dtype, C, E, blocks=1):
+    if uses_cells(dtype, C, E):
+        return ["k_mask_cells"] + ["k_block_cells"] * blocks + ["k_band_counts"]
+    return ["k_block_fused"] * blocks + ["k_band_counts"]
 
 
 FUSED_CASES = [
@@ -62,6 +81,13 @@ FUSED_CASES = [
     ("c72_f16_h1", "f16", (3, 1, 30, 72, 144), 0.5, 15),
     ("c120_bf16_w1", "bf16", (2, 70, 1, 120, 128), 0.4, 16),
     ("c128_f16_w23", "f16", (2, 9, 23, 128, 272), 0.3, 18),
+    # cell kernel: ragged cells, a single cell, hidden widths with a partial
+    # last slice, more cells than the persistent grid's waves
+    ("cells_ragged_bf16", "bf16", (3, 7, 11, 24, 96), 0.4, 20),
+    ("cells_one_cell_f16", "f16", (1, 3, 5, 8, 16), 0.5, 21),
+    ("cells_e80_f16", "f16", (4, 13, 21, 16, 80), 0.3, 22),
+    ("cells_e176_bf16_w70", "bf16", (2, 9, 70, 32, 176), 0.35, 24),
+    ("cells_many_f16", "f16", (96, 64, 64, 32, 192), 0.25, 23),
 ]
 
 
@@ -74,10 +100,35 @@ def test_fused_block_parity(case):
     wts = inputs.block_weights(rng, C, E, dtype=dtype)
     o = util.oracle_calibrated_block(x, wts, density, dtype)
     g = run_stack(x, [wts], [o["b_m"]], dtype)
-    assert g["names"] == ["k_block_fused", "k_band_counts"]
+    assert g["names"] == expected_launches(dtype, C, E)
     assert g["masks"][0].cpu().numpy().tobytes() == o["G"].tobytes()
     assert tuple(int(v) for v in g["counts"][0].cpu()) == (o["A"].size, o["D"].size)
     check_block_output(host(g["y"]), x, o["y"], o["G"], dtype)
+    # the same arithmetic as the kernel chain, bit for bit
+    chain = run_stack(x, [wts], [o["b_m"]], dtype, flags=dc.STACK_UNFUSED)
+    assert torch.equal(g["y"], chain["y"])
+
+
+def test_cells_schedule_concentrated_work():
+    """All active positions in one image of a 16-image batch: the cell
+    kernel's equal-work shares put that image's cells on many workgroups and
+    leave the others' shares to the empty cells; masks, counts and output as
+    the oracle, over a two-block stack (the second block's shares come from
+    the first block's per-cell counts)."""
+    rng = inputs.rng_for(55)
+    N, H, W, C, E = 16, 64, 64, 32, 192
+    x = inputs.round_to_storage(inputs.blob_features(rng, N, H, W, C), "f16")
+    x[1:] = 0.0
+    blocks = [inputs.block_weights(rng, C, E, dtype="f16") for _ in range(2)]
+    xs, outs = oracle_stack(x, blocks, 0.3 / N, "f16")
+    for o in outs:
+        assert o["G"].reshape(N, -1)[1:].sum() == 0 and o["G"].sum() > 0
+    biases = [o["b_m"] for o in outs]
+    g = run_stack(x, blocks, biases, "f16")
+    assert g["names"] == expected_launches("f16", C, E, blocks=2)
+    check_stack_end_to_end(x, blocks, biases, g["masks"].cpu().numpy(), g["counts"].cpu().numpy(),
+                           host(g["y"]), "f16")
+    assert host(g["y"])[1:].tobytes() == x[1:].tobytes()
 
 
 @pytest.mark.parametrize("bias", [-np.inf, np.inf])
@@ -98,6 +149,7 @@ def test_fused_empty_and_full_masks(bias):
 
 
 @pytest.mark.parametrize("dtype,shape,nb", [("f16", (32, 64, 64, 32, 192), 8),
+                                            ("bf16", (5, 11, 19, 24, 144), 3),
                                             ("bf16", (4, 20, 28, 48, 96), 3),
                                             ("f32", (2, 16, 16, 16, 96), 2),
                                             ("f16", (2, 12, 90, 64, 128), 2),
@@ -120,7 +172,7 @@ def test_fused_stack_matches_kernel_chain(dtype, shape, nb):
     assert ref["names"][0] == "k_mask" and "k_block_fused" not in ref["names"]
     for in_place in (False, True):
         g = run_stack(x, blocks, biases, dtype, in_place=in_place)
-        assert "k_block_fused" in g["names"]
+        assert ("k_block_cells" if uses_cells(dtype, C, E) else "k_block_fused") in g["names"]
         assert torch.equal(g["masks"], ref["masks"])
         assert torch.equal(g["counts"], ref["counts"])
         assert torch.equal(g["y"], ref["y"])

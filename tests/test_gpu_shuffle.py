@@ -2,7 +2,8 @@
 the CPU oracle: masks and counts bit-exact, the pass-through half and the
 inactive branch positions bit for bit, the unit output and the branch output
 on its own within 1e-5 (fp32) / 2e-2 (fp16, bf16) normwise (the branch
-increment alone: the same, 4e-2 in bf16)."""
+increment alone: the same plus the storage rounding of the branch output
+relative to the increment's scale)."""
 import numpy as np
 import pytest
 import torch
@@ -62,12 +63,15 @@ def check_unit_output(y_gpu, x_f32, y_oracle, G, dtype):
     e_br = util.normwise(yg[:, 1::2], yo[:, 1::2])
     e_b = util.normwise(yg[G][:, 1::2].astype(np.float64) - xo[G][:, cb:],
                         yo[G][:, 1::2] - xo[G][:, cb:]) if G.any() else 0.0
-    # The bound is on the unit output y.  The branch increment F alone is
-    # also checked: in bf16 its two intermediates are stored with 8-bit
-    # significands (relative rounding 2^-9 each) and both contractions
-    # cancel, so F's own normwise error gets twice the output bound there.
-    tol_b = 2 * util.TOL[dtype] if dtype == "bf16" else util.TOL[dtype]
-    log("  normwise err: y %.3e  branch output %.3e  branch F %.3e  (tol %.0e, F %.0e)"
+    # The bound is on the unit output y and on the branch output.  The branch
+    # increment F alone is also checked; it is read off the stored branch
+    # output, so its bound adds that rounding relative to F's own scale.
+    tol_b = util.TOL[dtype]
+    if G.any():
+        f_scale = np.abs(yo[G][:, 1::2] - xo[G][:, cb:]).max()
+        if f_scale > 0:
+            tol_b += util.UNIT_ROUNDOFF[dtype] * np.abs(yo[:, 1::2]).max() / f_scale
+    log("  normwise err: y %.3e  branch output %.3e  branch F %.3e  (tol %.0e, F %.2e)"
         % (e_y, e_br, e_b, util.TOL[dtype], tol_b))
     assert e_y <= util.TOL[dtype]
     assert e_br <= util.TOL[dtype]

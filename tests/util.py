@@ -12,6 +12,8 @@ import oracle
 from paper_1912_03203_amd import inputs
 
 TOL = {"f32": 1e-5, "f16": 2e-2, "bf16": 2e-2}
+# unit roundoff of the storage types (round to nearest even)
+UNIT_ROUNDOFF = {"f32": 2.0 ** -24, "f16": 2.0 ** -11, "bf16": 2.0 ** -8}
 
 
 def workers() -> int:
@@ -37,6 +39,28 @@ def normwise(got, want):
     scale = np.max(np.abs(want)) if want.size else 0.0
     err = np.max(np.abs(got - want)) if want.size else 0.0
     return 0.0 if err == 0 else err / (scale if scale > 0 else 1.0)
+
+
+CANARY = 0xA5
+
+
+class Guarded:
+    """A device buffer of `numel` elements followed by `tail` guard bytes of
+    0xA5: a kernel that writes past the end of an output, a list or a
+    workspace changes them (checked with intact())."""
+
+    def __init__(self, numel, dtype, fill=0, device="cuda", tail=1024):
+        import torch
+
+        elem = torch.empty((), dtype=dtype).element_size()
+        self.nbytes = max(int(numel), 1) * elem
+        self.raw = torch.full((self.nbytes + tail,), CANARY, dtype=torch.uint8, device=device)
+        self.t = self.raw[:self.nbytes].view(dtype)[:int(numel)]
+        if fill is not None:
+            self.t.fill_(fill)
+
+    def intact(self):
+        return bool((self.raw[self.nbytes:] == CANARY).all())
 
 
 def elementwise(got, want):
