@@ -4,11 +4,12 @@
 // 3.2) for blocks of at most 32 channels and 192 hidden channels in 16-bit
 // storage.  The image is cut into cells of 2 x 8 positions; one wave owns a
 // cell from start to end, with no barrier between waves:
-//   1. the hard-mask bytes of the cell's 4 x 10 region (the cell plus a
-//      one-position ring) become one 64-bit ballot word; the cell's active
-//      set and the part of its 3x3 dilation inside the region (every in-image
-//      region position next to an active one) follow by shifts of that word,
-//      and their raster-ordered lists by popcount ranks;
+//   1. x and the hard-mask bytes of the cell's 4 x 10 region (the cell plus a
+//      one-position ring) are read in one round trip: x into the wave's LDS
+//      copy of the region, the mask into one 64-bit ballot word.  The cell's
+//      active set and the part of its 3x3 dilation inside the region (every
+//      in-image region position next to an active one) follow by shifts of
+//      that word, and their raster-ordered lists by popcount ranks;
 //   2. for each 32-channel slice of the hidden layer: expansion of the
 //      needed positions on the matrix cores (the bias is the accumulator's
 //      start), activation, stored at the position's slot of the wave's
@@ -21,14 +22,13 @@
 //      stored values (the fp32 multiply-add chain of k_mask), and the
 //      cell's active count for the next launch's schedule.
 // Every weight of the block sits in LDS for the whole launch.  The grid is
-// persistent (one workgroup of 16 waves per CU).  Workgroup k takes the cells
-// whose weighted start lies in the k-th equal share of the total work (an
-// empty cell counts 1, a cell with active positions kCellActiveWork), from
-// the per-cell active counts that the previous launch wrote.  The range's
-// empty cells are streamed first by all threads (copy and next mask unit,
-// two positions in flight per thread); then the 16 waves pull the active
-// cells of the range through a counter in LDS.  So a dense region of the
-// mask is spread over many CUs, and the span follows the active work.
+// persistent (one workgroup of 16 waves per CU).  The active cells, listed
+// from the per-cell counts that the previous launch wrote, are dealt to the
+// workgroups in equal shares by count; the 16 waves pull them through a
+// counter in LDS and then stream the empty cells of the workgroup's equal
+// share of the grid (copy and next mask unit, one position per lane), so
+// the copies overlap the active work of the other waves.  A dense region of
+// the mask is spread over many CUs, and the span follows the active work.
 // The arithmetic of every output element is the one of the kernel chain
 // (k_expand, k_dw_project): the same operand fragments, summation order and
 // roundings.  Input and output must be different buffers (a cell's ring is
@@ -39,7 +39,6 @@
 
 namespace dynconv {
 
-
 // A cell is 2 image rows x 8 columns: 16 own positions, one 16-position tile
 // of the depthwise / projection, and a 4 x 10 region (the cell plus its ring)
 // of at most 40 positions, so one 64-bit ballot holds the region's mask.
@@ -49,7 +48,7 @@ constexpr int kRegCols = kCellCols + 2;               // 10
 constexpr int kRegRows = kCellRows + 2;               // 4
 constexpr int kRegSlots = kRegRows * kRegCols;        // 40 region slots
 constexpr int kNeedTiles = (kRegSlots + 15) / 16;     // 3
-constexpr int kCellWaves = 16;                        // 4 waves per SIMD
+constexpr int kCellWaves = 16;                        // 4 waves per SIMD: 128 registers
 constexpr int kCellThreads = kCellWaves * kWave;
 constexpr int kCellMaxC = 32;
 constexpr int kCellMaxE = 192;
@@ -71,7 +70,8 @@ template <typename T>
 struct CellWeights {
     alignas(16) T w1[kCellMaxE][kCellMaxC + 8];   // expansion rows e, channels fastest (zero past C, E)
     alignas(16) T w3[kCellMaxC][kCellMaxE + 8];   // projection rows c, hidden fastest (zero past C, E)
-    alignas(16) T w2[9][kCellMaxE];               // depthwise taps, transposed (zero past E)
+    alignas(16) T w2[9][kCellMaxE + 8];           // depthwise taps, transposed (zero past E); the
+                                                  // padding puts the nine rows on distinct LDS banks
     alignas(16) float b1[kCellMaxE];
     alignas(16) float b2[kCellMaxE];
     alignas(16) float b3[kCellMaxC];
@@ -90,12 +90,27 @@ __device__ __forceinline__ int slot_off(int q) { return (q / kRegCols) * kRegPit
 
 template <typename T>
 struct CellWaveLds {
-    // the region array; the epilogue reuses its first 16 x 80 bytes for the
-    // cell's own rows
-    alignas(16) char h1[kSpareSlot + kSlotBytes];
+    alignas(16) char h1[kSpareSlot + kSlotBytes];  // the region array of one slice
+    alignas(16) T xr[kRegSlots][kChunkPad];        // x at the region slots; the own slots become y
     int8_t need[48];
     int8_t act[kCellOwn];
 };
+
+// Lane S of each 16-lane row of the wave, to every lane of that row (DPP
+// row_newbcast, one move per register).
+template <int S>
+__device__ __forceinline__ uint4 row_bcast16(uint4 v) {
+    static_assert(S >= 0 && S < 16, "source lane within the row");
+    uint4 o;
+    o.x = __builtin_amdgcn_mov_dpp(v.x, 0x150 + S, 0xf, 0xf, false);
+    o.y = __builtin_amdgcn_mov_dpp(v.y, 0x150 + S, 0xf, 0xf, false);
+    o.z = __builtin_amdgcn_mov_dpp(v.z, 0x150 + S, 0xf, 0xf, false);
+    o.w = __builtin_amdgcn_mov_dpp(v.w, 0x150 + S, 0xf, 0xf, false);
+    return o;
+}
+
+// Stream work unit: 4 cells (64 positions, one per lane).
+constexpr int kStreamCells = kWave / kCellOwn;
 
 template <typename T>
 struct CellLds {
@@ -103,7 +118,7 @@ struct CellLds {
     CellWaveLds<T> wv[kCellWaves];
     int list[kCellList];  // this share's active cells, raster order
     int part[kCellWaves];
-    int next;
+    int next, next_stream;
 };
 
 __device__ __forceinline__ void wave_sync() {
@@ -196,6 +211,23 @@ k_block_cells(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
     const int ncells = N * cpi;
     const int E32 = (E + kChunk - 1) / kChunk * kChunk;
 
+    // this thread's chunks of the count buffer (16 cells per 16-byte word; the
+    // count buffers are padded to whole 256 bytes); the first chunk is
+    // requested before the weights, so both latencies overlap
+    const int nchunks = (ncells + 15) / 16;
+    const int per = (nchunks + kCellThreads - 1) / kCellThreads;
+    const int q0 = tid * per, q1 = min(q0 + per, nchunks);
+    auto active_bits = [&](uint4 v, int i) {  // bit u: cell i + u is active
+        const uint32_t wd[4] = {v.x, v.y, v.z, v.w};
+        uint32_t bits = 0;
+#pragma unroll
+        for (int u = 0; u < 16; ++u)
+            if (i + u < ncells && ((wd[u / 4] >> (8 * (u % 4))) & 0xffu)) bits |= 1u << u;
+        return bits;
+    };
+    uint4 first_raw = make_uint4(0, 0, 0, 0);
+    if (!DENSE && q0 < q1) first_raw = reinterpret_cast<const uint4 *>(cnt_in)[q0];
+
     // ---- all weights of the block into LDS (zero past C and E): every
     // thread's global loads are issued before its LDS stores
     {
@@ -258,36 +290,21 @@ k_block_cells(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
     }
 
     // ---- this workgroup's work.  Dense: cells [u_lo, u_hi), an equal share.
-    // Gated: the empty cells of [u_lo, u_hi) are streamed (a copy and the
-    // next mask unit, memory-bound, no ring needed), and the active cells are
-    // dealt in equal shares by count: share k is the active cells with rank
-    // [a_lo, a_hi) in raster order, listed in LDS from the per-cell active
-    // counts that the previous launch wrote.  So a dense region of the mask
-    // is spread over many CUs, and the span follows the active work.
+    // Gated: the active cells are dealt in equal shares by count (share k is
+    // the active cells with rank [a_lo, a_hi) in raster order, listed in LDS
+    // from the per-cell active counts that the previous launch wrote), and
+    // the empty cells of [u_lo, u_hi) are streamed (a copy and the next mask
+    // unit: memory-bound, no ring needed) once a wave runs out of active
+    // cells.  So a dense region of the mask is spread over many CUs, and the
+    // span follows the active work.
     const int u_lo = static_cast<int>(static_cast<int64_t>(k) * ncells / G);
     const int u_hi = static_cast<int>(static_cast<int64_t>(k + 1) * ncells / G);
     int a_lo = 0, a_hi = u_hi - u_lo;
-    // this thread's chunks of the count buffer and the rank of its first active cell
-    int my_rank = 0, my_cnt = 0, my_q0 = 0, my_q1 = 0;
+    int my_rank = 0, my_cnt = 0;
     uint32_t my_first = 0;
-    auto active_bits = [&](uint4 v, int i) {  // bit u: cell i + u is active
-        const uint32_t wd[4] = {v.x, v.y, v.z, v.w};
-        uint32_t bits = 0;
-#pragma unroll
-        for (int u = 0; u < 16; ++u)
-            if (i + u < ncells && ((wd[u / 4] >> (8 * (u % 4))) & 0xffu)) bits |= 1u << u;
-        return bits;
-    };
     if (!DENSE) {
-        // a thread owns a contiguous run of 16-cell chunks, read as 16-byte
-        // words (the count buffers are padded to whole 256 bytes)
-        const int nchunks = (ncells + 15) / 16;
-        const int per = (nchunks + kCellThreads - 1) / kCellThreads;
-        const int q0 = tid * per, q1 = min(q0 + per, nchunks);
-        // the first chunk stays in registers for the listing pass (one chunk
-        // per thread up to 16384 cells)
-        const uint32_t first = (q0 < q1) ? active_bits(reinterpret_cast<const uint4 *>(cnt_in)[q0], q0 * 16) : 0u;
-        int cnt = __popc(first);
+        my_first = (q0 < q1) ? active_bits(first_raw, q0 * 16) : 0u;
+        int cnt = __popc(my_first);
         for (int q = q0 + 1; q < q1; ++q)
             cnt += __popc(active_bits(reinterpret_cast<const uint4 *>(cnt_in)[q], q * 16));
         const int incl = wave_scan_incl(cnt);
@@ -304,17 +321,14 @@ k_block_cells(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
         a_hi = static_cast<int>(static_cast<int64_t>(k + 1) * total / G);
         my_rank = before + incl - cnt;
         my_cnt = cnt;
-        my_q0 = q0;
-        my_q1 = q1;
-        my_first = first;
     }
-    __syncthreads();  // the weights
     // the bounds are the same in every lane: keep them in scalar registers,
-    // so that the cell loop below is uniform control flow (with a bound in a
-    // vector register the compiler may split the loop per lane, and lanes
-    // other than lane 0 would then reread the counter's start)
+    // so that the loops below are uniform control flow (with a bound in a
+    // vector register the compiler may split a loop per lane, and lanes
+    // other than lane 0 would then reread a counter's start)
     a_lo = __builtin_amdgcn_readfirstlane(a_lo);
     a_hi = __builtin_amdgcn_readfirstlane(a_hi);
+    const int n_stream = DENSE ? 0 : (u_hi - u_lo + kStreamCells - 1) / kStreamCells;
 
     const float lo1 = act_lo(act1), hi1 = act_hi(act1);
     const float lo2 = act_lo(act2), hi2 = act_hi(act2);
@@ -323,115 +337,32 @@ k_block_cells(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
     const int npieces = C / per16;
     const int rr = lane / kRegCols, cc = lane % kRegCols;    // this lane's region slot
     const int oi = lane / kCellCols, oj = lane % kCellCols;  // this lane's own position (lane < 16)
+    const int oslot = (oi + 1) * kRegCols + oj + 1;          // ... and its region slot
     const uint64_t lt = lanemask_lt(lane);
     CellWaveLds<T> &V = L.wv[wave];
-    T(*ys)[kChunkPad] = reinterpret_cast<T(*)[kChunkPad]>(V.h1);  // own rows in the epilogue (C + 8 <= kChunkPad)
 
-    // ---- the empty cells of the range, as a stream over their positions
-    // (all threads, two items in flight per thread): y = x, the next block's
-    // mask unit, the cells' counts.  16 consecutive items are one cell,
-    // handled by one 16-lane group of a wave.
-    if (!DENSE) {
-        const int nitems = (u_hi - u_lo) * kCellOwn;
-        // the trip count is the wave's (its first item), so the loop is uniform
-        for (int b0 = wave * kWave; b0 < nitems; b0 += 2 * kCellThreads) {
-            uint4 row[2][kCellPieces];
-            int64_t pos[2];
-            bool take[2], empty[2];
-            int cellv[2];
-#pragma unroll
-            for (int kk = 0; kk < 2; ++kk) {
-                const int i = b0 + lane + kk * kCellThreads;
-                cellv[kk] = u_lo + i / kCellOwn;
-                empty[kk] = i < nitems && cnt_in[cellv[kk]] == 0;
-                const int o = i % kCellOwn;
-                const int rem = cellv[kk] % cpi;
-                const int h = (rem / ncw) * kCellRows + o / kCellCols;
-                const int w = (rem % ncw) * kCellCols + o % kCellCols;
-                take[kk] = empty[kk] && h < H && w < W;
-                pos[kk] = (static_cast<int64_t>(cellv[kk] / cpi) * H + h) * W + w;
-#pragma unroll
-                for (int p = 0; p < kCellPieces; ++p)
-                    row[kk][p] = (take[kk] && p < npieces) ? reinterpret_cast<const uint4 *>(xin + pos[kk] * C)[p]
-                                                           : make_uint4(0, 0, 0, 0);
-            }
-#pragma unroll
-            for (int kk = 0; kk < 2; ++kk) {
-                if (take[kk]) {
-                    uint4 *dst = reinterpret_cast<uint4 *>(yout + pos[kk] * C);
-#pragma unroll
-                    for (int p = 0; p < kCellPieces; ++p)
-                        if (p < npieces) dst[p] = row[kk][p];
-                }
-                bool bit = false;
-                if (take[kk] && mask_next) {
-                    bit = cell_mask_row<T>(row[kk], L.w.wm, C, bm_next, mask_mode);
-                    mask_next[pos[kk]] = bit ? 1 : 0;
-                }
-                const int cnt = group16_count(__ballot(bit), lane);
-                if (empty[kk] && mask_next) cnt_next[cellv[kk]] = static_cast<uint8_t>(cnt);
-                if (band_counts) {
-                    // no active position; dilated: own positions next to an
-                    // active position of a neighbouring cell
-                    bool dil = false;
-                    if (take[kk]) {
-                        const int h = static_cast<int>((pos[kk] / W) % H), w = static_cast<int>(pos[kk] % W);
-                        const int64_t img = pos[kk] / (static_cast<int64_t>(H) * W) * H;
-                        for (int dh = -1; dh <= 1; ++dh)
-                            for (int dw = -1; dw <= 1; ++dw) {
-                                const int hh = h + dh, ww = w + dw;
-                                if (hh >= 0 && hh < H && ww >= 0 && ww < W && mask_in[(img + hh) * W + ww] != 0)
-                                    dil = true;
-                            }
-                    }
-                    const int nd = group16_count(__ballot(dil), lane);
-                    if (empty[kk])
-                        *reinterpret_cast<int2 *>(band_counts + 2 * static_cast<int64_t>(cellv[kk])) = make_int2(0, nd);
-                }
-            }
-        }
-    }
-
-    // rounds of at most kCellList active cells (one round unless a share is
-    // larger than the list)
-    for (int r0 = a_lo; r0 < a_hi; r0 += kCellList) {
-    const int r1 = min(a_hi, r0 + kCellList);
-    if (!DENSE) {
-        // list the round's active cells (ranks r0 .. r1 - 1) in raster order
-        int rank = my_rank;
-        if (rank < r1 && rank + my_cnt > r0) {
-            for (int q = my_q0; q < my_q1; ++q) {
-                uint32_t bits = (q == my_q0) ? my_first
-                                              : active_bits(reinterpret_cast<const uint4 *>(cnt_in)[q], q * 16);
-                while (bits) {
-                    const int u = __ffs(bits) - 1;
-                    bits &= bits - 1;
-                    if (rank >= r0 && rank < r1) L.list[rank - r0] = q * 16 + u;
-                    ++rank;
-                }
-            }
-        }
-    }
-    if (tid == 0) L.next = 0;
-    __syncthreads();  // the list and the counter
-    for (;;) {
-        // every lane adds 1 (the counter advances by 64 per cell: one LDS
-        // atomic for the wave) and every lane below stores the cell's counts
-        // itself: no lane-0-only region next to the loop's back edge, which
-        // the compiler could split per lane
-        const int cn = atomicAdd(&L.next, 1);
-        const int item = (__builtin_amdgcn_readlane(cn, 0) >> 6) + r0;
-        if (item >= r1) break;  // uniform: both sides are scalar
-        const int cell = DENSE ? u_lo + item : __builtin_amdgcn_readfirstlane(L.list[item - r0]);
+    // One active cell (gated) or any cell (dense), by one wave.
+    auto run_cell = [&](int cell) {
         const int n = cell / cpi, rem = cell % cpi;
         const int h0 = (rem / ncw) * kCellRows, w0 = (rem % ncw) * kCellCols;
         const int64_t img = static_cast<int64_t>(n) * H;
 
-        // ---- 1. mask word of the region, active set, needed set, lists
+        // ---- 1. x and the mask at the region slots in one round trip; the
+        // region's mask word, active set, needed set, lists
         const int hh = h0 - 1 + rr, ww = w0 - 1 + cc;
         const bool inimg = lane < kRegSlots && hh >= 0 && hh < H && ww >= 0 && ww < W;
         bool mb = false;
-        if (inimg) mb = DENSE ? true : (mask_in[(img + hh) * W + ww] != 0);
+        if (inimg) {
+            const int64_t gp = (img + hh) * W + ww;
+            const uint4 *src = reinterpret_cast<const uint4 *>(xin + gp * C);
+            uint4 xv[kCellPieces];
+#pragma unroll
+            for (int p = 0; p < kCellPieces; ++p) xv[p] = (p < npieces) ? src[p] : make_uint4(0, 0, 0, 0);
+            mb = DENSE ? true : (mask_in[gp] != 0);
+#pragma unroll
+            for (int p = 0; p < kCellPieces; ++p)
+                if (p < npieces) reinterpret_cast<uint4 *>(&V.xr[lane][0])[p] = xv[p];
+        }
         const uint64_t IMG = __ballot(inimg);
         const uint64_t Gw = __ballot(mb);
         const uint64_t A = Gw & kOwnBits;
@@ -447,12 +378,8 @@ k_block_cells(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
             *reinterpret_cast<int2 *>(band_counts + 2 * static_cast<int64_t>(cell)) =
                 make_int2(__popcll(A), __popcll(Gd));  // the same value from every lane
         }
-
-        // the cell's own row of this lane (x; becomes y)
         const int oh = h0 + oi, ow = w0 + oj;
         const bool ov = lane < kCellOwn && oh < H && ow < W;
-        const int64_t opos = (img + oh) * W + ow;
-        uint4 xr[kCellPieces];
 
         if (A != 0) {
             const int nneed = __popcll(NEED);
@@ -476,8 +403,7 @@ k_block_cells(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
                 const int q = (i < nneed) ? static_cast<int>(V.need[i]) : -1;
                 nq[t] = (q >= 0) ? slot_off(q) : kSpareSlot;
                 const int qx = (q >= 0) ? q : kCellFirstOwn;  // an in-image slot
-                const int64_t p = (img + h0 - 1 + qx / kRegCols) * W + (w0 - 1 + qx % kRegCols);
-                bx[t] = (t < ntn && 8 * g < C) ? M::load(xin + p * C + 8 * g) : M::zero();
+                bx[t] = (t < ntn && 8 * g < C) ? M::load(&V.xr[qx][8 * g]) : M::zero();
             }
             // the tile's active position of this lane (padding lanes: -1)
             const int aq = (r < __popcll(A)) ? static_cast<int>(V.act[r]) : -1;
@@ -494,13 +420,24 @@ k_block_cells(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
                 const int eb = ec * kChunk;
                 // ---- 2a. expansion of the needed slots into the region array:
                 // the tiles' products issued back to back, then activated
+                // the slice's per-channel constants, one 16-byte read per lane
+                // (lane r of a 16-lane row: tap r's depthwise weights for r < 9,
+                // the depthwise bias for r = 9, 10, the expansion bias of the
+                // two output tiles for r = 11, 12), broadcast within the row
+                const uint4 pk = *reinterpret_cast<const uint4 *>(
+                    r < 9 ? reinterpret_cast<const char *>(&L.w.w2[r][eb + 8 * g])
+                    : r < 11 ? reinterpret_cast<const char *>(&L.w.b2[eb + 8 * g + 4 * (r - 9)])
+                             : reinterpret_cast<const char *>(&L.w.b1[eb + 16 * (r == 12) + 4 * g]));
                 typename M::frag a1[2];
                 floatx4 bi[2];
 #pragma unroll
                 for (int m = 0; m < 2; ++m) {
                     a1[m] = M::load(&L.w.w1[eb + m * 16 + r][8 * g]);
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) bi[m][v] = L.w.b1[eb + m * 16 + 4 * g + v];
+                    const uint4 b = (m == 0) ? row_bcast16<11>(pk) : row_bcast16<12>(pk);
+                    bi[m][0] = __uint_as_float(b.x);
+                    bi[m][1] = __uint_as_float(b.y);
+                    bi[m][2] = __uint_as_float(b.z);
+                    bi[m][3] = __uint_as_float(b.w);
                 }
                 auto expand = [&](auto ntiles) {
                     constexpr int NTL = decltype(ntiles)::value;
@@ -524,25 +461,42 @@ k_block_cells(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
                 else if (ntn == 2) expand(std::integral_constant<int, 2>());
                 else expand(std::integral_constant<int, 1>());
                 wave_sync();
-                // ---- 2b. depthwise at the tile's active positions + projection slice
+                // ---- 2b. depthwise at the tile's positions + projection slice
                 typename M::frag a3[2];
 #pragma unroll
                 for (int mt = 0; mt < 2; ++mt) a3[mt] = M::load(&L.w.w3[mt * 16 + r][eb + 8 * g]);
+                // all nine taps and their weights requested before the first
+                // multiply-add (the LDS latency is paid once per slice)
                 typename io<T>::vec8 tv[9];
 #pragma unroll
                 for (int t = 0; t < 9; ++t)
                     tv[t] = io<T>::raw8(reinterpret_cast<const T *>(
                         own + (t / 3 - 1) * kRegPitch + (t % 3 - 1) * kSlotBytes));
                 float s[8];
-#pragma unroll
-                for (int u = 0; u < 8; ++u) s[u] = L.w.b2[eb + 8 * g + u];
-#pragma unroll
-                for (int t = 0; t < 9; ++t) {
-                    const typename io<T>::vec8 wk = io<T>::raw8(&L.w.w2[t][eb + 8 * g]);
+                {
+                    const uint4 lo = row_bcast16<9>(pk), hi = row_bcast16<10>(pk);
+                    s[0] = __uint_as_float(lo.x); s[1] = __uint_as_float(lo.y);
+                    s[2] = __uint_as_float(lo.z); s[3] = __uint_as_float(lo.w);
+                    s[4] = __uint_as_float(hi.x); s[5] = __uint_as_float(hi.y);
+                    s[6] = __uint_as_float(hi.z); s[7] = __uint_as_float(hi.w);
+                }
+                auto tap = [&](auto t) {
+                    constexpr int TT = decltype(t)::value;
+                    const uint4 wb = row_bcast16<TT>(pk);
+                    const typename io<T>::vec8 wk = *reinterpret_cast<const typename io<T>::vec8 *>(&wb);
 #pragma unroll
                     for (int u = 0; u < 8; ++u)
-                        s[u] = __builtin_fmaf(static_cast<float>(wk[u]), static_cast<float>(tv[t][u]), s[u]);
-                }
+                        s[u] = __builtin_fmaf(static_cast<float>(wk[u]), static_cast<float>(tv[TT][u]), s[u]);
+                };
+                tap(std::integral_constant<int, 0>());
+                tap(std::integral_constant<int, 1>());
+                tap(std::integral_constant<int, 2>());
+                tap(std::integral_constant<int, 3>());
+                tap(std::integral_constant<int, 4>());
+                tap(std::integral_constant<int, 5>());
+                tap(std::integral_constant<int, 6>());
+                tap(std::integral_constant<int, 7>());
+                tap(std::integral_constant<int, 8>());
                 float hv[8];
 #pragma unroll
                 for (int u = 0; u < 8; ++u) hv[u] = clamp_act(s[u], lo2, hi2);
@@ -552,61 +506,137 @@ k_block_cells(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
                 wave_sync();
             }
 
-            // ---- 3a. residual sum at the active positions, on the own rows
-#pragma unroll
-            for (int p = 0; p < kCellPieces; ++p)
-                xr[p] = (ov && p < npieces) ? reinterpret_cast<const uint4 *>(xin + opos * C)[p] : make_uint4(0, 0, 0, 0);
-            if (ov) {
-#pragma unroll
-                for (int p = 0; p < kCellPieces; ++p)
-                    if (p < npieces) reinterpret_cast<uint4 *>(&ys[lane][0])[p] = xr[p];
-            }
-            wave_sync();
+            // ---- 3a. residual sum at the active positions, in place on the
+            // staged own rows
             if (aq >= 0) {
-                const int o = (aq / kRegCols - 1) * kCellCols + (aq % kRegCols - 1);
 #pragma unroll
                 for (int mt = 0; mt < 2; ++mt) {
                     const int c0 = mt * 16 + 4 * g;
                     if (c0 < C) {
                         float xv[4], out[4];
-                        io<T>::load4(&ys[o][c0], xv);
+                        io<T>::load4(&V.xr[aq][c0], xv);
 #pragma unroll
                         for (int v = 0; v < 4; ++v) out[v] = xv[v] + clamp_act(acc[mt][v], lo3, hi3);
-                        io<T>::store4(&ys[o][c0], out);
+                        io<T>::store4(&V.xr[aq][c0], out);
                     }
                 }
             }
-            wave_sync();
-            if (ov) {
-#pragma unroll
-                for (int p = 0; p < kCellPieces; ++p)
-                    if (p < npieces) xr[p] = reinterpret_cast<const uint4 *>(&ys[lane][0])[p];
-            }
-            wave_sync();  // the own rows are read before the next cell's lists
-        } else {
-#pragma unroll
-            for (int p = 0; p < kCellPieces; ++p)
-                xr[p] = (ov && p < npieces) ? reinterpret_cast<const uint4 *>(xin + opos * C)[p] : make_uint4(0, 0, 0, 0);
         }
+        wave_sync();
 
         // ---- 3b. store the cell, the next block's mask unit on the stored values
+        uint4 yr[kCellPieces];
+#pragma unroll
+        for (int p = 0; p < kCellPieces; ++p)
+            yr[p] = (ov && p < npieces) ? reinterpret_cast<const uint4 *>(&V.xr[oslot][0])[p] : make_uint4(0, 0, 0, 0);
+        wave_sync();  // the staged rows are read before the next cell overwrites them
         if (ov) {
-            uint4 *dst = reinterpret_cast<uint4 *>(yout + opos * C);
+            uint4 *dst = reinterpret_cast<uint4 *>(yout + ((img + oh) * W + ow) * C);
 #pragma unroll
             for (int p = 0; p < kCellPieces; ++p)
-                if (p < npieces) dst[p] = xr[p];
+                if (p < npieces) dst[p] = yr[p];
         }
         if (!DENSE && mask_next) {
             bool bit = false;
             if (ov) {
-                bit = cell_mask_row<T>(xr, L.w.wm, C, bm_next, mask_mode);
-                mask_next[opos] = bit ? 1 : 0;
+                bit = cell_mask_row<T>(yr, L.w.wm, C, bm_next, mask_mode);
+                mask_next[(img + oh) * W + ow] = bit ? 1 : 0;
             }
             const uint64_t b = __ballot(bit);
             cnt_next[cell] = static_cast<uint8_t>(__popcll(b));  // the same value from every lane
         }
-    }
-    __syncthreads();  // every wave is done with the list before it is rebuilt
+    };
+
+    // Four empty cells of [u_lo, u_hi) (chunk j), one position per lane:
+    // y = x, the next block's mask unit, the cells' counts.
+    auto run_stream = [&](int j) {
+        const int i = j * kWave + lane;
+        const int cell = u_lo + i / kCellOwn;
+        const bool empty = cell < u_hi && cnt_in[cell] == 0;
+        const int o = i % kCellOwn;
+        const int rem = cell % cpi;
+        const int h = (rem / ncw) * kCellRows + o / kCellCols;
+        const int w = (rem % ncw) * kCellCols + o % kCellCols;
+        const bool take = empty && h < H && w < W;
+        const int64_t img = static_cast<int64_t>(cell / cpi) * H;
+        const int64_t pos = (img + h) * W + w;
+        uint4 row[kCellPieces];
+#pragma unroll
+        for (int p = 0; p < kCellPieces; ++p)
+            row[p] = (take && p < npieces) ? reinterpret_cast<const uint4 *>(xin + pos * C)[p] : make_uint4(0, 0, 0, 0);
+        if (take) {
+            uint4 *dst = reinterpret_cast<uint4 *>(yout + pos * C);
+#pragma unroll
+            for (int p = 0; p < kCellPieces; ++p)
+                if (p < npieces) dst[p] = row[p];
+        }
+        bool bit = false;
+        if (take && mask_next) {
+            bit = cell_mask_row<T>(row, L.w.wm, C, bm_next, mask_mode);
+            mask_next[pos] = bit ? 1 : 0;
+        }
+        const int cnt = group16_count(__ballot(bit), lane);
+        if (empty && mask_next) cnt_next[cell] = static_cast<uint8_t>(cnt);
+        if (band_counts) {
+            // no active position; dilated: own positions next to an active
+            // position of a neighbouring cell
+            bool dil = false;
+            if (take) {
+                for (int dh = -1; dh <= 1; ++dh)
+                    for (int dw = -1; dw <= 1; ++dw) {
+                        const int hh = h + dh, ww = w + dw;
+                        if (hh >= 0 && hh < H && ww >= 0 && ww < W && mask_in[(img + hh) * W + ww] != 0) dil = true;
+                    }
+            }
+            const int nd = group16_count(__ballot(dil), lane);
+            if (empty) *reinterpret_cast<int2 *>(band_counts + 2 * static_cast<int64_t>(cell)) = make_int2(0, nd);
+        }
+    };
+
+    // rounds of at most kCellList active cells (one round unless a share is
+    // larger than the list); the empty cells are streamed in the last round
+    for (int r0 = a_lo;; r0 += kCellList) {
+        const int r1 = min(a_hi, r0 + kCellList);
+        const bool last = r1 >= a_hi;
+        if (!DENSE) {
+            // list the round's active cells (ranks r0 .. r1 - 1) in raster order
+            int rank = my_rank;
+            if (rank < r1 && rank + my_cnt > r0) {
+                for (int q = q0; q < q1; ++q) {
+                    uint32_t bits = (q == q0) ? my_first
+                                              : active_bits(reinterpret_cast<const uint4 *>(cnt_in)[q], q * 16);
+                    while (bits) {
+                        const int u = __ffs(bits) - 1;
+                        bits &= bits - 1;
+                        if (rank >= r0 && rank < r1) L.list[rank - r0] = q * 16 + u;
+                        ++rank;
+                    }
+                }
+            }
+        }
+        if (tid == 0) {
+            L.next = 0;
+            L.next_stream = 0;
+        }
+        __syncthreads();  // the weights, the list and the counters
+        // every lane adds 1 to a counter (it advances by 64 per item: one LDS
+        // atomic for the wave) and every lane stores the cells' counts
+        // itself: no lane-0-only region next to a loop's back edge, which the
+        // compiler could split per lane
+        for (;;) {
+            const int item = (__builtin_amdgcn_readlane(atomicAdd(&L.next, 1), 0) >> 6) + r0;
+            if (item >= r1) break;  // uniform: both sides are scalar
+            run_cell(DENSE ? u_lo + item : __builtin_amdgcn_readfirstlane(L.list[item - r0]));
+        }
+        if (last) {
+            for (;;) {
+                const int j = __builtin_amdgcn_readlane(atomicAdd(&L.next_stream, 1), 0) >> 6;
+                if (j >= n_stream) break;
+                run_stream(j);
+            }
+            break;
+        }
+        __syncthreads();  // every wave is done with the list before it is rebuilt
     }
 }
 
