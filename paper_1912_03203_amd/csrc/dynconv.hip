@@ -902,6 +902,22 @@ struct NetLayout {
     int ngated;
 };
 
+// Consecutive gated layers keep the shape (stride 1, equal widths), so a run
+// of them is one stack: the previous block's epilogue computes the next
+// block's mask, and only the run's first block runs a mask launch of its own.
+// Returns the run's length (at most kMaxRun) and copies its blocks.
+constexpr int32_t kMaxRun = 64;
+int32_t gated_run(const dynconv_layer *layers, int32_t i, int32_t n, dynconv_block *blks) {
+    int32_t m = 0;
+    while (i + m < n && m < kMaxRun && layers[i + m].kind == DYNCONV_LAYER_BLOCK && layers[i + m].gated &&
+           layers[i + m].stride == 1 && layers[i + m].blk.c_in == layers[i].blk.c_in &&
+           layers[i + m].blk.c_out == layers[i].blk.c_in) {
+        blks[m] = layers[i + m].blk;
+        ++m;
+    }
+    return m;
+}
+
 dynconv_status net_plan(dynconv_shape in, const dynconv_layer *layers, int32_t n, dynconv_dtype dt,
                         int32_t flags, bool need_mask, NetLayout *NL, dynconv_shape *out_shape,
                         size_t *mask_total) {
@@ -917,9 +933,16 @@ dynconv_status net_plan(dynconv_shape in, const dynconv_layer *layers, int32_t n
         const size_t npos_out = static_cast<size_t>(positions(ls.out));
         act = std::max(act, npos_out * ls.out.c * sz);
         if (layers[i].kind == DYNCONV_LAYER_BLOCK && layers[i].gated) {
-            ++ngated;
-            mtot += npos_in;
-            inner = std::max(inner, stack_layout(ls.in, &layers[i].blk, 1, dt, flags).total);
+            dynconv_block blks[kMaxRun];
+            const int32_t m = gated_run(layers, i, n, blks);
+            for (int32_t j = 1; j < m; ++j) {  // the run's later layers: checked like any other
+                LayerShapes lj;
+                if (dynconv_status st = layer_shape(layers[i + j], ls.out, lj, need_mask)) return st;
+            }
+            ngated += m;
+            mtot += static_cast<size_t>(m) * npos_in;
+            inner = std::max(inner, stack_layout(ls.in, blks, m, dt, flags).total);
+            i += m - 1;
         } else if (layers[i].kind == DYNCONV_LAYER_BLOCK) {
             if (layers[i].blk.w_expand) h1 = std::max(h1, npos_in * ls.hidden * sz);
             h2 = std::max(h2, npos_out * ls.hidden * sz);
@@ -1160,12 +1183,16 @@ void net_walk(const void *x, void *y, dynconv_shape in, dynconv_dtype dt, const 
                 DC_TYPED(dt, launch_conv1x1<T>(src, positions(ls.in), L.c_in, L.w, L.b, L.c_out, L.act, nullptr,
                                                dst, st, mk));
         } else if (L.gated) {
-            StackLayout SL = stack_layout(ls.in, &L.blk, 1, dt, flags);
+            dynconv_block blks[kMaxRun];
+            const int32_t m = gated_run(layers, i, n, blks);
+            i += m - 1;  // the run's last layer
+            dst = (i == n - 1) ? y : bufs[i % 2];
+            StackLayout SL = stack_layout(ls.in, blks, m, dt, flags);
             uint8_t *mk_l = masks ? masks + moff : nullptr;
             int32_t *ct_l = counts ? counts + 2 * gi : nullptr;
-            stack_walk(src, dst, ls.in, dt, &L.blk, 1, flags, mk_l, ct_l, inner, SL, st, mk, plan, false);
-            moff += static_cast<size_t>(positions(ls.in));
-            ++gi;
+            stack_walk(src, dst, ls.in, dt, blks, m, flags, mk_l, ct_l, inner, SL, st, mk, plan, dst == src);
+            moff += static_cast<size_t>(m) * positions(ls.in);
+            gi += m;
         } else {
             const dynconv_block &b = L.blk;
             const void *hin = src;
