@@ -8,16 +8,28 @@ unconditionally, and this check scans the device assembly of each build:
 after every v_mfma it walks the following instructions (counting one state
 per instruction, N + 1 per s_nop N, up to an unconditional branch) and
 reports the first instruction that
-reads one of the MFMA's destination registers with fewer than MIN_STATES
-states in between, or another MFMA that takes them as its A or B operand
-(its C operand may chain: the hardware forwards it).  It is a heuristic
-guard against that miscompilation, not a full hazard model.
+reads one of the MFMA's destination registers with fewer states in between
+than the instruction's threshold, or another MFMA that takes them as its A
+or B operand (its C operand may chain: the hardware forwards it).
+
+The thresholds are per instruction: the fewest states the compiler itself
+leaves after that MFMA before a read on any straight-line path of this
+library (8 after the 16-bit 16x16x32 forms, 10 after the fp32 16x16x4), so a
+path that lost them, as in the miscompilation above, is reported.  It is a
+guard against that failure, not a hazard model of the hardware: the
+determinism tests (repeated runs, the one-launch kernels against the
+chain byte for byte, graph replays) are the check of the results.
 """
 from __future__ import annotations
 
 import re
 
-MIN_STATES = 4
+MIN_STATES = {
+    "v_mfma_f32_16x16x32_f16": 8,
+    "v_mfma_f32_16x16x32_bf16": 8,
+    "v_mfma_f32_16x16x4_f32": 10,
+}
+DEFAULT_STATES = 4  # any other MFMA form
 WINDOW = 60
 
 _RANGE = re.compile(r"([av])\[(\d+):(\d+)\]")
@@ -49,7 +61,9 @@ def check(asm: str) -> list:
         s = line.strip()
         if not s.startswith("v_mfma"):
             continue
-        ops = _operands(s.split(None, 1)[1])
+        name, rest = s.split(None, 1)
+        need = MIN_STATES.get(name, DEFAULT_STATES)
+        ops = _operands(rest)
         dst = _regs(ops[0])
         states = 0
         for j in range(i + 1, min(i + WINDOW, len(lines))):
@@ -74,7 +88,7 @@ def check(asm: str) -> list:
             for a in srcs:
                 reads |= _regs(a)
             if reads & dst:
-                if states < MIN_STATES:
+                if states < need:
                     found.append("%s: MFMA result read after %d states: %s" % (func, states, t))
                 break
             if dst & _regs(args[0] if args else ""):
