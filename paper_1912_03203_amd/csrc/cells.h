@@ -24,8 +24,9 @@
 // Every weight of the block sits in LDS for the whole launch.  The grid is
 // persistent (one workgroup of 16 waves per CU).  The active cells, listed
 // from the per-cell counts that the previous launch wrote, are dealt to the
-// workgroups in equal shares by count; the 16 waves pull them through a
-// counter in LDS and then stream the empty cells of the workgroup's equal
+// workgroups in equal shares by count; they go to the 16 waves in turn (so
+// they spread evenly over the SIMDs), and the waves then stream, through a
+// counter in LDS, the empty cells of the workgroup's equal
 // share of the grid (copy and next mask unit, one position per lane), so
 // the copies overlap the active work of the other waves.  A dense region of
 // the mask is spread over many CUs, and the span follows the active work.
@@ -619,14 +620,24 @@ k_block_cells(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
             L.next_stream = 0;
         }
         __syncthreads();  // the weights, the list and the counters
-        // every lane adds 1 to a counter (it advances by 64 per item: one LDS
-        // atomic for the wave) and every lane stores the cells' counts
-        // itself: no lane-0-only region next to a loop's back edge, which the
-        // compiler could split per lane
-        for (;;) {
-            const int item = (__builtin_amdgcn_readlane(atomicAdd(&L.next, 1), 0) >> 6) + r0;
-            if (item >= r1) break;  // uniform: both sides are scalar
-            run_cell(DENSE ? u_lo + item : __builtin_amdgcn_readfirstlane(L.list[item - r0]));
+        // Gated: the round's active cells go to the waves in turn (item i to
+        // wave i mod kCellWaves).  Wave w runs on SIMD w mod 4, so the cells
+        // spread evenly over the SIMDs: with a shared counter, whichever
+        // waves come first take them, and one SIMD could hold 4 of a
+        // workgroup's 11 cells while another holds 2.  Dense: every cell costs
+        // the same and a shared counter (one LDS atomic per wave, merged by
+        // the compiler) keeps the waves busy.  Bounds, items and the wave
+        // index are scalars, so both loops are uniform control flow.
+        if (!DENSE) {
+            const int wave_s = __builtin_amdgcn_readfirstlane(wave);
+            for (int item = r0 + wave_s; item < r1; item += kCellWaves)
+                run_cell(__builtin_amdgcn_readfirstlane(L.list[item - r0]));
+        } else {
+            for (;;) {
+                const int item = (__builtin_amdgcn_readlane(atomicAdd(&L.next, 1), 0) >> 6) + r0;
+                if (item >= r1) break;
+                run_cell(u_lo + item);
+            }
         }
         if (last) {
             for (;;) {
