@@ -660,17 +660,14 @@ def calibrate_network(dc, inputs, torch, x0, layers, dens, dt, labels=None):
     layers run one after another (offline, before timing).  With person
     labels (the pose network), each gated block's mask weights are first set
     to point from the background to the people in its own input features
-    (ellipse_mask_weights on the labels subsampled to its resolution)."""
+    (inputs.person_mask_weights)."""
     cur = x0
     biases = []
     gi = 0
     rng = np.random.default_rng(11)
     for L in layers:
         if L.get("gated") and labels is not None:
-            n, h, w, c = cur.shape
-            step = labels.shape[1] // h
-            lab = np.ascontiguousarray(labels[:, ::step, ::step][:, :h, :w])
-            L["w_m"] = inputs.ellipse_mask_weights(rng, cur.float().cpu().numpy(), lab, 1)[0]
+            L["w_m"] = inputs.person_mask_weights(rng, cur.float().cpu().numpy(), labels)
         one = dc.NetworkWeights([L], dt, biases=[0.0] if L.get("gated") else None)
         if L.get("gated"):
             n, h, w, c = cur.shape

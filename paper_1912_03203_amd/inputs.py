@@ -173,6 +173,17 @@ def ellipse_mask_weights(rng, x_nhwc, labels, blocks, jitter=0.02):
     return [(d + rng.normal(0.0, jitter, size=d.shape)).astype(np.float32) for _ in range(blocks)]
 
 
+def person_mask_weights(rng, feats_nhwc, labels):
+    """Mask-unit weights of one gated block of the pose network, pointing from
+    the background to the people in the block's own input features: the
+    [n, 256, 256] person labels are subsampled to the features' resolution
+    (every step-th row and column) and passed to ellipse_mask_weights."""
+    n, h, w, _ = np.asarray(feats_nhwc).shape
+    step = labels.shape[1] // h
+    lab = np.ascontiguousarray(labels[:, ::step, ::step][:, :h, :w])
+    return ellipse_mask_weights(rng, feats_nhwc, lab, 1)[0]
+
+
 def round_to_storage(a, dtype):
     """Round float values to the storage dtype (nearest even); returns float32
     values exactly representable in it.  fp32 and fp16 round once from the

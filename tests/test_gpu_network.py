@@ -58,15 +58,21 @@ def net_f16():
     return x, layers, dens
 
 
-def oracle_biases(x, layers, dens, dtype):
-    """Per gated block, the percentile bias of its oracle input (in order)."""
+def oracle_biases(x, layers, dens, dtype, labels=None):
+    """Per gated block, the percentile bias of its oracle input (in order).
+    With person labels (the pose network), each gated block's mask weights
+    are first pointed at the people in its oracle input, as the benchmark's
+    calibration does on the device's features."""
     import oracle
     biases = []
     cur = util.nchw(x).astype(np.float64)
     rnd = rounder(dtype)
     gi = 0
+    rng = np.random.default_rng(11)
     for L in layers:
         if L.get("gated"):
+            if labels is not None:
+                L["w_m"] = inputs.person_mask_weights(rng, util.nhwc(cur), labels)
             _, s = util.oracle_mask_chunked(cur, L["w_m"], 0.0)
             b = float(inputs.percentile_bias(s, dens[gi]))
             biases.append(b)
@@ -215,11 +221,13 @@ def test_gated_network_full_batch_sampled_images():
 
 def test_pose_network_end_to_end():
     """The pose network (256x256x3 ellipse images -> MobileNetV2 backbone ->
-    8 stacked gated blocks at 64x64x32) on 2 images, with the oracle's biases,
-    checked as in test_gated_network_end_to_end."""
+    8 stacked gated blocks at 64x64x32) on 2 images, in the benchmark's
+    configuration: every gated block's mask unit pointed at the people in its
+    input (concentrated masks, cells fully active on the people), the
+    oracle's biases; checked as in test_gated_network_end_to_end."""
     import oracle
-    x, layers, dens, _ = inputs.make_pose_network_inputs(7, 2, dtype="f16")
-    biases = oracle_biases(x, layers, dens, "f16")
+    x, layers, dens, labels = inputs.make_pose_network_inputs(7, 2, dtype="f16")
+    biases = oracle_biases(x, layers, dens, "f16", labels=labels)
     y, m, c = run_net(x, layers, "f16", biases=biases, masks=True)
     assert y.shape == (2, 64, 64, 32)
     rnd = rounder("f16")
