@@ -946,7 +946,7 @@ def main():
                     help="the one-launch kernel whose dispatches --summarize-traffic reads")
     ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write the traffic summary from the counter CSVs of two --traffic-pass runs")
-    ap.add_argument("--section", choices=("network", "pose_network", "shufflenet"),
+    ap.add_argument("--section", choices=("network", "pose_network", "shufflenet", "probes"),
                     help="run only this report (for a kernel trace of it) and print its JSON object")
     args = ap.parse_args()
     if args.summarize_traffic:
@@ -972,6 +972,8 @@ def main():
         g = not args.no_graph
         if args.section == "shufflenet":
             out = shufflenet_report(dc, inputs, torch, args.steps, args.warmup, g, args.profile_steps)
+        elif args.section == "probes":
+            out = bandwidth_probes(dc, inputs, torch)
         else:
             kind = "pose" if args.section == "pose_network" else "mobilenetv2"
             out = network_report(dc, inputs, torch, args.steps, args.warmup, g, args.profile_steps, kind)
