@@ -53,6 +53,7 @@ from __future__ import annotations
 
 import argparse
 import json
+import tempfile
 import os
 import sys
 import time
@@ -417,8 +418,8 @@ def cpu_baseline_parallel(inputs, wl, x0_np, blocks_np, density, budget_s=8.0):
     from concurrent.futures import ThreadPoolExecutor
 
     import oracle
-    # one thread per core this process may use, at most the 16 host cores that
-    # a one-GPU machine gives a job
+    # one thread per core this process may use, at most 16 (the host cores
+    # that a machine shares per GPU)
     affinity = len(os.sched_getaffinity(0))
     threads = max(1, min(16, affinity))
     x = np.ascontiguousarray(x0_np.transpose(0, 3, 1, 2)).astype(np.float64)
@@ -938,7 +939,8 @@ def main():
     ap.add_argument("--no-network", action="store_true", help="skip the whole-MobileNetV2 report")
     ap.add_argument("--profile-steps", type=int, default=20)
     ap.add_argument("--report", help="where the full JSON report goes "
-                                     "(default gpurun_out/bench_report.json); stdout gets the compact line")
+                                     "(default: bench_report.json in the system's temporary directory); stdout "
+                                     "gets the compact line")
     ap.add_argument("--traffic-pass", action="store_true",
                     help="untimed launches for an HBM-counter run: a plain copy of known size, "
                          "then the sparse and the dense stack")
@@ -1126,7 +1128,7 @@ def main():
         log("cpu baseline (dense oracle)")
         result["cpu_baseline_dense"] = cpu_baseline(inputs, wl, x_np, blocks_np, args.density, budget_s=8.0,
                                                     form="dense")
-    report = args.report or os.path.join(ROOT, "gpurun_out", "bench_report.json")
+    report = args.report or os.path.join(tempfile.gettempdir(), "bench_report.json")
     os.makedirs(os.path.dirname(os.path.abspath(report)), exist_ok=True)
     with open(report, "w") as f:
         json.dump(result, f, indent=1)
