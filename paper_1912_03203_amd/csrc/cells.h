@@ -54,8 +54,6 @@ constexpr int kCellThreads = kCellWaves * kWave;
 constexpr int kCellMaxC = 32;
 constexpr int kCellMaxE = 192;
 constexpr int kCellFirstOwn = kRegCols + 1;           // slot of own position (0, 0)
-// active cells of one workgroup's share held in its LDS list at once
-constexpr int kCellList = 2048;
 
 // Region slots (row rr, column cc) -> bit rr*10 + cc.
 constexpr uint64_t kRowBits = 0xffull << 1;           // columns 1..8 of one region row
@@ -117,7 +115,10 @@ template <typename T>
 struct CellLds {
     CellWeights<T> w;
     CellWaveLds<T> wv[kCellWaves];
-    int list[kCellList];  // this share's active cells, raster order
+    // per thread: its wave's inclusive active-cell count up to and including
+    // the thread's chunks of the count buffer, and the active bits of its
+    // (first) chunk
+    uint2 tab[kCellThreads];
     int part[kCellWaves];
     int next, next_stream;
 };
@@ -151,6 +152,21 @@ __device__ __forceinline__ bool cell_mask_row(const uint4 (&row)[kCellPieces], c
 // Popcount of this lane's 16-lane group in a ballot (the group is one cell).
 __device__ __forceinline__ int group16_count(uint64_t b, int lane) {
     return __popc(static_cast<uint32_t>((b >> (lane & 48)) & 0xffffull));
+}
+
+// Bit b (b < 4) set where byte b of w is nonzero: the top bit of each byte of
+// ((w & 0x7f7f7f7f) + 0x7f7f7f7f) | w, the four gathered by one multiply
+// (the partial products land on distinct bits, none of them in 21..24).
+__device__ __forceinline__ uint32_t nonzero_bytes(uint32_t w) {
+    const uint32_t h = (((w & 0x7f7f7f7fu) + 0x7f7f7f7fu) | w) & 0x80808080u;
+    return (((h >> 7) * 0x00204081u) >> 21) & 0xfu;
+}
+
+// floor(k * total / G) for 0 <= k <= G, in 32 bits when the product fits.
+__device__ __forceinline__ int share_bound(int k, int total, int G) {
+    const uint64_t p = static_cast<uint64_t>(k) * static_cast<uint32_t>(total);
+    if (p <= 0xffffffffull) return static_cast<int>(static_cast<uint32_t>(p) / static_cast<uint32_t>(G));
+    return static_cast<int>(p / static_cast<uint64_t>(G));
 }
 
 // The first block's mask unit over cells: mask bytes of every position and
@@ -218,13 +234,11 @@ k_block_cells(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
     const int nchunks = (ncells + 15) / 16;
     const int per = (nchunks + kCellThreads - 1) / kCellThreads;
     const int q0 = tid * per, q1 = min(q0 + per, nchunks);
-    auto active_bits = [&](uint4 v, int i) {  // bit u: cell i + u is active
-        const uint32_t wd[4] = {v.x, v.y, v.z, v.w};
-        uint32_t bits = 0;
-#pragma unroll
-        for (int u = 0; u < 16; ++u)
-            if (i + u < ncells && ((wd[u / 4] >> (8 * (u % 4))) & 0xffu)) bits |= 1u << u;
-        return bits;
+    auto active_bits = [&](uint4 v, int i) {  // bit u: cell i + u (< ncells) is active
+        const uint32_t bits = nonzero_bytes(v.x) | (nonzero_bytes(v.y) << 4) | (nonzero_bytes(v.z) << 8) |
+                              (nonzero_bytes(v.w) << 12);
+        const int left = ncells - i;
+        return (left >= 16) ? bits : bits & ((1u << left) - 1u);
     };
     uint4 first_raw = make_uint4(0, 0, 0, 0);
     if (!DENSE && q0 < q1) first_raw = reinterpret_cast<const uint4 *>(cnt_in)[q0];
@@ -292,36 +306,36 @@ k_block_cells(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
 
     // ---- this workgroup's work.  Dense: cells [u_lo, u_hi), an equal share.
     // Gated: the active cells are dealt in equal shares by count (share k is
-    // the active cells with rank [a_lo, a_hi) in raster order, listed in LDS
-    // from the per-cell active counts that the previous launch wrote), and
-    // the empty cells of [u_lo, u_hi) are streamed (a copy and the next mask
+    // the active cells with rank [a_lo, a_hi) in raster order, ranked from
+    // the per-cell active counts that the previous launch wrote), and the
+    // empty cells of [u_lo, u_hi) are streamed (a copy and the next mask
     // unit: memory-bound, no ring needed) once a wave runs out of active
     // cells.  So a dense region of the mask is spread over many CUs, and the
-    // span follows the active work.
+    // span follows the active work.  One barrier: the weights, the ranks and
+    // the counters.
     const int u_lo = static_cast<int>(static_cast<int64_t>(k) * ncells / G);
     const int u_hi = static_cast<int>(static_cast<int64_t>(k + 1) * ncells / G);
-    int a_lo = 0, a_hi = u_hi - u_lo;
-    int my_rank = 0, my_cnt = 0;
-    uint32_t my_first = 0;
     if (!DENSE) {
-        my_first = (q0 < q1) ? active_bits(first_raw, q0 * 16) : 0u;
-        int cnt = __popc(my_first);
+        const uint32_t first = (q0 < q1) ? active_bits(first_raw, q0 * 16) : 0u;
+        int cnt = __popc(first);
         for (int q = q0 + 1; q < q1; ++q)
             cnt += __popc(active_bits(reinterpret_cast<const uint4 *>(cnt_in)[q], q * 16));
         const int incl = wave_scan_incl(cnt);
+        L.tab[tid] = make_uint2(static_cast<uint32_t>(incl), first);
         if (lane == kWave - 1) L.part[wave] = incl;
-        __syncthreads();
-        int before = 0, total = 0;
-#pragma unroll
-        for (int i = 0; i < kCellWaves; ++i) {
-            const int v = L.part[i];
-            before += (i < wave) ? v : 0;
-            total += v;
-        }
-        a_lo = static_cast<int>(static_cast<int64_t>(k) * total / G);
-        a_hi = static_cast<int>(static_cast<int64_t>(k + 1) * total / G);
-        my_rank = before + incl - cnt;
-        my_cnt = cnt;
+    }
+    if (tid == 0) {
+        L.next = 0;
+        L.next_stream = 0;
+    }
+    __syncthreads();
+    // gated: the waves' inclusive counts in lanes 0..15, the share's ranks
+    int pw = 0, a_lo = 0, a_hi = u_hi - u_lo;
+    if (!DENSE) {
+        pw = wave_scan_incl(lane < kCellWaves ? L.part[lane] : 0);
+        const int total = __builtin_amdgcn_readlane(pw, kCellWaves - 1);
+        a_lo = share_bound(k, total, G);
+        a_hi = share_bound(k + 1, total, G);
     }
     // the bounds are the same in every lane: keep them in scalar registers,
     // so that the loops below are uniform control flow (with a bound in a
@@ -594,60 +608,53 @@ k_block_cells(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
         }
     };
 
-    // rounds of at most kCellList active cells (one round unless a share is
-    // larger than the list); the empty cells are streamed in the last round
-    for (int r0 = a_lo;; r0 += kCellList) {
-        const int r1 = min(a_hi, r0 + kCellList);
-        const bool last = r1 >= a_hi;
-        if (!DENSE) {
-            // list the round's active cells (ranks r0 .. r1 - 1) in raster order
-            int rank = my_rank;
-            if (rank < r1 && rank + my_cnt > r0) {
-                for (int q = q0; q < q1; ++q) {
-                    uint32_t bits = (q == q0) ? my_first
-                                              : active_bits(reinterpret_cast<const uint4 *>(cnt_in)[q], q * 16);
-                    while (bits) {
-                        const int u = __ffs(bits) - 1;
-                        bits &= bits - 1;
-                        if (rank >= r0 && rank < r1) L.list[rank - r0] = q * 16 + u;
-                        ++rank;
-                    }
-                }
-            }
+    // The active cell of rank R (gated): the wave whose chunks hold it (the
+    // waves' inclusive counts), the thread within that wave (its inclusive
+    // counts in LDS), the chunk of that thread, and the bit within the chunk.
+    // Every step is a ballot over the wave, so R, the result and every index
+    // on the way are uniform.
+    auto find = [&](int R) {
+        const int v = __popcll(__ballot(lane < kCellWaves && pw <= R));  // waves wholly before R
+        const int rv = R - (v > 0 ? __builtin_amdgcn_readlane(pw, v - 1) : 0);
+        const uint2 e = L.tab[v * kWave + lane];
+        const int t = __popcll(__ballot(static_cast<int>(e.x) <= rv));  // threads wholly before R
+        int local = rv - (t > 0 ? static_cast<int>(__builtin_amdgcn_readlane(e.x, t - 1)) : 0);
+        int q = (v * kWave + t) * per;
+        const int q_end = min(q + per, nchunks);
+        uint32_t bits = __builtin_amdgcn_readlane(e.y, t);
+        for (;;) {  // more than one chunk per thread: the later chunks are read again
+            const int c = __popc(bits);
+            if (local < c || q + 1 >= q_end) break;
+            local -= c;
+            ++q;
+            bits = active_bits(reinterpret_cast<const uint4 *>(cnt_in)[q], q * 16);
         }
-        if (tid == 0) {
-            L.next = 0;
-            L.next_stream = 0;
+        const bool hit = lane < 16 && ((bits >> lane) & 1u) && __popc(bits & ((1u << lane) - 1u)) == local;
+        return q * 16 + __builtin_amdgcn_readfirstlane(__ffsll(static_cast<long long>(__ballot(hit))) - 1);
+    };
+
+    // Gated: the share's active cells go to the waves in turn (rank a_lo + i
+    // to wave i mod kCellWaves).  Wave w runs on SIMD w mod 4, so the cells
+    // spread evenly over the SIMDs: with a shared counter, whichever waves
+    // come first take them, and one SIMD could hold 4 of a workgroup's 11
+    // cells while another holds 2.  Dense: every cell costs the same and a
+    // shared counter (one LDS atomic per wave, merged by the compiler) keeps
+    // the waves busy.  Bounds, items and the wave index are scalars, so both
+    // loops are uniform control flow.
+    if (!DENSE) {
+        const int wave_s = __builtin_amdgcn_readfirstlane(wave);
+        for (int item = a_lo + wave_s; item < a_hi; item += kCellWaves) run_cell(find(item));
+        for (;;) {
+            const int j = __builtin_amdgcn_readlane(atomicAdd(&L.next_stream, 1), 0) >> 6;
+            if (j >= n_stream) break;
+            run_stream(j);
         }
-        __syncthreads();  // the weights, the list and the counters
-        // Gated: the round's active cells go to the waves in turn (item i to
-        // wave i mod kCellWaves).  Wave w runs on SIMD w mod 4, so the cells
-        // spread evenly over the SIMDs: with a shared counter, whichever
-        // waves come first take them, and one SIMD could hold 4 of a
-        // workgroup's 11 cells while another holds 2.  Dense: every cell costs
-        // the same and a shared counter (one LDS atomic per wave, merged by
-        // the compiler) keeps the waves busy.  Bounds, items and the wave
-        // index are scalars, so both loops are uniform control flow.
-        if (!DENSE) {
-            const int wave_s = __builtin_amdgcn_readfirstlane(wave);
-            for (int item = r0 + wave_s; item < r1; item += kCellWaves)
-                run_cell(__builtin_amdgcn_readfirstlane(L.list[item - r0]));
-        } else {
-            for (;;) {
-                const int item = (__builtin_amdgcn_readlane(atomicAdd(&L.next, 1), 0) >> 6) + r0;
-                if (item >= r1) break;
-                run_cell(u_lo + item);
-            }
+    } else {
+        for (;;) {
+            const int item = __builtin_amdgcn_readlane(atomicAdd(&L.next, 1), 0) >> 6;
+            if (item >= a_hi) break;
+            run_cell(u_lo + item);
         }
-        if (last) {
-            for (;;) {
-                const int j = __builtin_amdgcn_readlane(atomicAdd(&L.next_stream, 1), 0) >> 6;
-                if (j >= n_stream) break;
-                run_stream(j);
-            }
-            break;
-        }
-        __syncthreads();  // every wave is done with the list before it is rebuilt
     }
 }
 
