@@ -162,11 +162,10 @@ __device__ __forceinline__ uint32_t nonzero_bytes(uint32_t w) {
     return (((h >> 7) * 0x00204081u) >> 21) & 0xfu;
 }
 
-// floor(k * total / G) for 0 <= k <= G, in 32 bits when the product fits.
+// floor(k * total / G) for 0 <= k <= G and 0 <= total <= the cell count: the
+// host launches the kernel only when the cell count times G fits in 32 bits.
 __device__ __forceinline__ int share_bound(int k, int total, int G) {
-    const uint64_t p = static_cast<uint64_t>(k) * static_cast<uint32_t>(total);
-    if (p <= 0xffffffffull) return static_cast<int>(static_cast<uint32_t>(p) / static_cast<uint32_t>(G));
-    return static_cast<int>(p / static_cast<uint64_t>(G));
+    return static_cast<int>(static_cast<uint32_t>(k) * static_cast<uint32_t>(total) / static_cast<uint32_t>(G));
 }
 
 // The first block's mask unit over cells: mask bytes of every position and
@@ -313,8 +312,8 @@ k_block_cells(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
     // cells.  So a dense region of the mask is spread over many CUs, and the
     // span follows the active work.  One barrier: the weights, the ranks and
     // the counters.
-    const int u_lo = static_cast<int>(static_cast<int64_t>(k) * ncells / G);
-    const int u_hi = static_cast<int>(static_cast<int64_t>(k + 1) * ncells / G);
+    const int u_lo = share_bound(k, ncells, G);
+    const int u_hi = share_bound(k + 1, ncells, G);
     if (!DENSE) {
         const uint32_t first = (q0 < q1) ? active_bits(first_raw, q0 * 16) : 0u;
         int cnt = __popc(first);

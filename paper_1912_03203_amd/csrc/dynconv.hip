@@ -457,6 +457,8 @@ bool use_fused(dynconv_shape s, dynconv_dtype dt, int32_t flags) {
 // work-balanced cell kernel, which keeps all weights of a block in LDS.
 bool use_cells(dynconv_shape s, dynconv_dtype dt, const dynconv_block *blks, int32_t n_blocks, int32_t flags) {
     if ((flags & kStackUnfused) || dt == DYNCONV_F32 || s.c > kCellMaxC) return false;
+    // the kernel's share bounds (cell count x workgroup count) are 32-bit
+    if (cell_count(s) * cells_shares(s) > 0xffffffffLL) return false;
     for (int32_t b = 0; b < n_blocks; ++b)
         if (blks[b].c_hidden > kCellMaxE) return false;
     return true;
