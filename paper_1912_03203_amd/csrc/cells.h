@@ -434,11 +434,16 @@ k_block_cells(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
                 const int eb = ec * kChunk;
                 // ---- 2a. expansion of the needed slots into the region array:
                 // the tiles' products issued back to back, then activated
-                // the slice's per-channel constants, one 16-byte read per lane
-                // (lane r of a 16-lane row: tap r's depthwise weights for r < 9,
-                // the depthwise bias for r = 9, 10, the expansion bias of the
-                // two output tiles for r = 11, 12), broadcast within the row
-                const uint4 pk = *reinterpret_cast<const uint4 *>(
+                // the slice's per-channel constants.  Dense launches (four busy
+                // waves per SIMD, the LDS the tighter resource): one 16-byte
+                // read per lane (lane r of a 16-lane row: tap r's depthwise
+                // weights for r < 9, the depthwise bias for r = 9, 10, the
+                // expansion bias of the two output tiles for r = 11, 12),
+                // broadcast within the row by DPP moves.  Gated launches (about
+                // three busy waves per SIMD, the vector ALU the tighter
+                // resource): row-wide broadcast reads from LDS instead, with
+                // no vector instruction.  The values are the same.
+                const uint4 pk = !DENSE ? make_uint4(0, 0, 0, 0) : *reinterpret_cast<const uint4 *>(
                     r < 9 ? reinterpret_cast<const char *>(&L.w.w2[r][eb + 8 * g])
                     : r < 11 ? reinterpret_cast<const char *>(&L.w.b2[eb + 8 * g + 4 * (r - 9)])
                              : reinterpret_cast<const char *>(&L.w.b1[eb + 16 * (r == 12) + 4 * g]));
@@ -447,11 +452,15 @@ k_block_cells(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
 #pragma unroll
                 for (int m = 0; m < 2; ++m) {
                     a1[m] = M::load(&L.w.w1[eb + m * 16 + r][8 * g]);
-                    const uint4 b = (m == 0) ? row_bcast16<11>(pk) : row_bcast16<12>(pk);
-                    bi[m][0] = __uint_as_float(b.x);
-                    bi[m][1] = __uint_as_float(b.y);
-                    bi[m][2] = __uint_as_float(b.z);
-                    bi[m][3] = __uint_as_float(b.w);
+                    if (!DENSE) {
+                        bi[m] = *reinterpret_cast<const floatx4 *>(&L.w.b1[eb + m * 16 + 4 * g]);
+                    } else {
+                        const uint4 b = (m == 0) ? row_bcast16<11>(pk) : row_bcast16<12>(pk);
+                        bi[m][0] = __uint_as_float(b.x);
+                        bi[m][1] = __uint_as_float(b.y);
+                        bi[m][2] = __uint_as_float(b.z);
+                        bi[m][3] = __uint_as_float(b.w);
+                    }
                 }
                 auto expand = [&](auto ntiles) {
                     constexpr int NTL = decltype(ntiles)::value;
@@ -487,7 +496,12 @@ k_block_cells(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
                     tv[t] = io<T>::raw8(reinterpret_cast<const T *>(
                         own + (t / 3 - 1) * kRegPitch + (t % 3 - 1) * kSlotBytes));
                 float s[8];
-                {
+                if (!DENSE) {
+                    const floatx4 lo = *reinterpret_cast<const floatx4 *>(&L.w.b2[eb + 8 * g]);
+                    const floatx4 hi = *reinterpret_cast<const floatx4 *>(&L.w.b2[eb + 8 * g + 4]);
+                    s[0] = lo[0]; s[1] = lo[1]; s[2] = lo[2]; s[3] = lo[3];
+                    s[4] = hi[0]; s[5] = hi[1]; s[6] = hi[2]; s[7] = hi[3];
+                } else {
                     const uint4 lo = row_bcast16<9>(pk), hi = row_bcast16<10>(pk);
                     s[0] = __uint_as_float(lo.x); s[1] = __uint_as_float(lo.y);
                     s[2] = __uint_as_float(lo.z); s[3] = __uint_as_float(lo.w);
@@ -496,7 +510,8 @@ k_block_cells(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
                 }
                 auto tap = [&](auto t) {
                     constexpr int TT = decltype(t)::value;
-                    const uint4 wb = row_bcast16<TT>(pk);
+                    const uint4 wb = !DENSE ? *reinterpret_cast<const uint4 *>(&L.w.w2[TT][eb + 8 * g])
+                                            : row_bcast16<TT>(pk);
                     const typename io<T>::vec8 wk = *reinterpret_cast<const typename io<T>::vec8 *>(&wb);
 #pragma unroll
                     for (int u = 0; u < 8; ++u)
