@@ -108,6 +108,15 @@ __device__ __forceinline__ uint4 row_bcast16(uint4 v) {
     return o;
 }
 
+// A 16-byte store that the next launch reads, not this one: nontemporal, so
+// that the lines leave the L2 as they are written rather than at the end of
+// the launch.
+__device__ __forceinline__ void store_stream(uint4 *dst, uint4 v) {
+    typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+    const u32x4 w = {v.x, v.y, v.z, v.w};
+    __builtin_nontemporal_store(w, reinterpret_cast<u32x4 *>(dst));
+}
+
 // Stream work unit: 4 cells (64 positions, one per lane).
 constexpr int kStreamCells = kWave / kCellOwn;
 
@@ -563,7 +572,7 @@ k_block_cells(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
             uint4 *dst = reinterpret_cast<uint4 *>(yout + ((img + oh) * W + ow) * C);
 #pragma unroll
             for (int p = 0; p < kCellPieces; ++p)
-                if (p < npieces) dst[p] = yr[p];
+                if (p < npieces) store_stream(&dst[p], yr[p]);
         }
         if (!DENSE && mask_next) {
             bool bit = false;
@@ -597,7 +606,7 @@ k_block_cells(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
             uint4 *dst = reinterpret_cast<uint4 *>(yout + pos * C);
 #pragma unroll
             for (int p = 0; p < kCellPieces; ++p)
-                if (p < npieces) dst[p] = row[p];
+                if (p < npieces) store_stream(&dst[p], row[p]);
         }
         bool bit = false;
         if (take && mask_next) {
