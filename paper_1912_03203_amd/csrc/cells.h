@@ -366,6 +366,14 @@ k_block_cells(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
 
     // One active cell (gated) or any cell (dense), by one wave.
     auto run_cell = [&](int cell) {
+        // Gated: a wave's issue priority falls as its cell progresses (3 for
+        // the region and the first two slices, 2 for the next two, 1 for the
+        // last two, 0 after the cell).  The SIMD's issue arbiter favours the
+        // oldest wave among those of the highest priority, so without this
+        // the third cell on a SIMD ran behind the other two and finished
+        // alone, latency-bound; with it the cells of a SIMD progress together
+        // and the streaming waves (priority 0) fill the gaps.
+        if (!DENSE) __builtin_amdgcn_s_setprio(3);
         const int n = cell / cpi, rem = cell % cpi;
         const int h0 = (rem / ncw) * kCellRows, w0 = (rem % ncw) * kCellCols;
         const int64_t img = static_cast<int64_t>(n) * H;
@@ -441,6 +449,10 @@ k_block_cells(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
 
             for (int ec = 0; ec < nsl; ++ec) {
                 const int eb = ec * kChunk;
+                if (!DENSE) {
+                    if (ec == 2) __builtin_amdgcn_s_setprio(2);
+                    else if (ec == 4) __builtin_amdgcn_s_setprio(1);
+                }
                 // ---- 2a. expansion of the needed slots into the region array:
                 // the tiles' products issued back to back, then activated
                 // the slice's per-channel constants.  Dense launches (four busy
@@ -583,6 +595,7 @@ k_block_cells(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
             const uint64_t b = __ballot(bit);
             cnt_next[cell] = static_cast<uint8_t>(__popcll(b));  // the same value from every lane
         }
+        if (!DENSE) __builtin_amdgcn_s_setprio(0);
     };
 
     // Four empty cells of [u_lo, u_hi) (chunk j), one position per lane:
