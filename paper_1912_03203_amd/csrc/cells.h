@@ -648,7 +648,9 @@ k_block_cells(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
     // waves' inclusive counts), the thread within that wave (its inclusive
     // counts in LDS), the chunk of that thread, and the bit within the chunk.
     // Every step is a ballot over the wave, so R, the result and every index
-    // on the way are uniform.
+    // on the way are uniform.  With more than one chunk per thread (large
+    // batches) the thread's chunks are read again, one per lane, 64 at a
+    // time, and a wave scan of their counts picks the chunk.
     auto find = [&](int R) {
         const int v = __popcll(__ballot(lane < kCellWaves && pw <= R));  // waves wholly before R
         const int rv = R - (v > 0 ? __builtin_amdgcn_readlane(pw, v - 1) : 0);
@@ -656,17 +658,28 @@ k_block_cells(const T *__restrict__ xin, T *__restrict__ yout, int N, int H, int
         const int t = __popcll(__ballot(static_cast<int>(e.x) <= rv));  // threads wholly before R
         int local = rv - (t > 0 ? static_cast<int>(__builtin_amdgcn_readlane(e.x, t - 1)) : 0);
         int q = (v * kWave + t) * per;
-        const int q_end = min(q + per, nchunks);
         uint32_t bits = __builtin_amdgcn_readlane(e.y, t);
-        for (;;) {  // more than one chunk per thread: the later chunks are read again
-            const int c = __popc(bits);
-            if (local < c || q + 1 >= q_end) break;
-            local -= c;
-            ++q;
-            bits = active_bits(reinterpret_cast<const uint4 *>(cnt_in)[q], q * 16);
+        if (per > 1) {
+            const int q_end = min(q + per, nchunks);
+            for (int base = q; base < q_end; base += kWave) {
+                const int qq = base + lane;
+                const uint32_t b = (qq < q_end) ? active_bits(reinterpret_cast<const uint4 *>(cnt_in)[qq], qq * 16) : 0u;
+                const int incl = wave_scan_incl(__popc(b));
+                const int j = __popcll(__ballot(incl <= local));  // chunks wholly before
+                q = base + j;
+                if (j < kWave) {
+                    local -= (j > 0 ? __builtin_amdgcn_readlane(incl, j - 1) : 0);
+                    bits = __builtin_amdgcn_readlane(b, j);
+                    break;
+                }
+                local -= __builtin_amdgcn_readlane(incl, kWave - 1);
+            }
         }
         const bool hit = lane < 16 && ((bits >> lane) & 1u) && __popc(bits & ((1u << lane) - 1u)) == local;
-        return q * 16 + __builtin_amdgcn_readfirstlane(__ffsll(static_cast<long long>(__ballot(hit))) - 1);
+        const uint64_t hb = __ballot(hit);
+        // (the counts are read-only in this launch, so a hit always exists; the
+        // guards only keep an index in range whatever the data)
+        return min(q, nchunks - 1) * 16 + (hb ? __builtin_amdgcn_readfirstlane(__ffsll(static_cast<long long>(hb)) - 1) : 0);
     };
 
     // Gated: the share's active cells go to the waves in turn (rank a_lo + i

@@ -149,6 +149,9 @@ def test_fused_empty_and_full_masks(bias):
 
 
 @pytest.mark.parametrize("dtype,shape,nb", [("f16", (32, 64, 64, 32, 192), 8),
+                                            # 81,920 cells: 5 count words per thread of the
+                                            # cell kernel's schedule (its search over them)
+                                            ("f16", (320, 64, 64, 32, 192), 2),
                                             ("bf16", (5, 11, 19, 24, 144), 3),
                                             ("bf16", (4, 20, 28, 48, 96), 3),
                                             ("f32", (2, 16, 16, 16, 96), 2),
