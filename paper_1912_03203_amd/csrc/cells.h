@@ -22,11 +22,12 @@
 //      stored values (the fp32 multiply-add chain of k_mask), and the
 //      cell's active count for the next launch's schedule.
 // Every weight of the block sits in LDS for the whole launch.  The grid is
-// persistent (one workgroup of 16 waves per CU).  The active cells, listed
-// from the per-cell counts that the previous launch wrote, are dealt to the
-// workgroups in equal shares by count; they go to the 16 waves in turn (so
-// they spread evenly over the SIMDs), and the waves then stream, through a
-// counter in LDS, the empty cells of the workgroup's equal
+// persistent (one workgroup of 16 waves per CU).  The active cells, ranked
+// in raster order from the per-cell counts that the previous launch wrote,
+// are dealt to the workgroups in equal shares by count; they go to the 16
+// waves in turn (so they spread evenly over the SIMDs), each wave finding
+// the cell of its rank by ballots over the counts, and the waves then
+// stream, through a counter in LDS, the empty cells of the workgroup's equal
 // share of the grid (copy and next mask unit, one position per lane), so
 // the copies overlap the active work of the other waves.  A dense region of
 // the mask is spread over many CUs, and the span follows the active work.
