@@ -219,6 +219,10 @@ def test_stack_launch_plans(lib):
     assert names(3, 0) == ["k_copy16"] + ["k_expand", "k_dw_project"] * 8
     assert names(0, 1, shape=dc.Shape(2, 8, 300, 32), n=2) == \
         ["k_mask_cells"] + ["k_block_cells"] * 2 + ["k_band_counts"]
+    # the cell kernel's share bounds are 32-bit: with cells x workgroups past
+    # 2^32 (a 1x1 image is one cell; 10^8 cells on any GPU of 43 CUs or more)
+    # the stack takes the patch kernel
+    assert names(0, 0, shape=dc.Shape(100_000_000, 1, 1, 32), n=2) == ["k_block_fused"] * 2 + ["k_band_counts"]
     arr136 = (dc.Block * 2)(*([fake_block(C=136)] * 2))
     total = lib.dynconv_stack_launch_names(dc.Shape(2, 8, 8, 136), arr136, 2, 1, 0, 1, None, 0)
     out = (ctypes.c_char_p * total)()
