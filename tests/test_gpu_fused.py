@@ -88,6 +88,10 @@ FUSED_CASES = [
     ("cells_e80_f16", "f16", (4, 13, 21, 16, 80), 0.3, 22),
     ("cells_e176_bf16_w70", "bf16", (2, 9, 70, 32, 176), 0.35, 24),
     ("cells_many_f16", "f16", (96, 64, 64, 32, 192), 0.25, 23),
+    # the pose shape nearly dense (about 32 active cells per workgroup, two
+    # or more per wave) and very sparse (most workgroups with 0-2 cells)
+    ("pose_d0.90_bf16", "bf16", (32, 64, 64, 32, 192), 0.90, 25),
+    ("pose_d0.05_f16", "f16", (32, 64, 64, 32, 192), 0.05, 26),
 ]
 
 
